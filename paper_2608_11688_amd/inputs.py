@@ -1,0 +1,110 @@
+"""Seeded synthetic inputs for the MoE-decode hot path.
+
+This module only draws random numbers and stores them in the formats the hot path
+consumes (fp32 hidden states, bf16 bit patterns for weights).  It holds none of the
+method's arithmetic, so both the HIP path and the CPU oracle may take their inputs
+from it.
+
+Every tensor comes from its own stream
+``Generator(PCG64(SeedSequence([seed, cfg_id, tag, layer, index])))`` so that any
+single expert, layer or batch row can be regenerated on its own.
+
+Recipe (the paper evaluates on text benchmarks; these generators stand in for the
+hidden states such text would produce, at the models' shapes):
+
+* pre-attention hidden state per (layer, batch row): an AR(1) process
+  h_0 ~ N(0, I), h_t = 0.7 h_{t-1} + 0.714 z_t, z_t ~ N(0, I), stored as fp32;
+* post-attention hidden state: h_post = h_pre + 0.3 N(0, I), fp32;
+* expert weights W1, W3 (I x d) and W2 (d x I): N(0, 0.02^2), rounded to bf16 (RNE);
+* gate router W_g = s N(0, 0.02^2) and prefetch router W_pf = W_g + 0.1 s N(0, 0.02^2),
+  with s = 2 / (0.02 sqrt(1.09 d)) so that gate logits have standard deviation 2;
+* optional per-expert logit bias b ~ N(0, 1) (Zipf-like expert load), shared by both
+  routers.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from .configs import MoEConfig
+
+# stream tags
+TAG_H0, TAG_HZ, TAG_HPOST, TAG_WG, TAG_WPF, TAG_W1, TAG_W3, TAG_W2, TAG_BIAS, TAG_CDF, \
+    TAG_MISC = range(1, 12)
+
+AR_RHO = 0.7
+AR_SIGMA = 0.714
+POST_NOISE = 0.3
+W_STD = 0.02
+PF_NOISE = 0.1
+GATE_LOGIT_STD = 2.0
+
+
+def rng(seed: int, cfg_id: int, tag: int, layer: int = 0, index: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(
+        np.random.SeedSequence([int(seed), int(cfg_id), int(tag), int(layer), int(index)])))
+
+
+def to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round fp32 values to the nearest bf16 (ties to even); returns uint16 bit patterns."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    return ((u + (((u >> 16) & 1) + 0x7FFF)) >> 16).astype(np.uint16)
+
+
+def hidden_states(cfg: MoEConfig, layer: int, rows: int, steps: int, seed: int = 0):
+    """(h_pre, h_post), each fp32 [steps, rows, d]; one AR(1) stream per (layer, row)."""
+    d = cfg.d
+    h_pre = np.empty((steps, rows, d), np.float32)
+    h_post = np.empty((steps, rows, d), np.float32)
+    for r in range(rows):
+        h = rng(seed, cfg.cfg_id, TAG_H0, layer, r).standard_normal(d)
+        z = rng(seed, cfg.cfg_id, TAG_HZ, layer, r).standard_normal((steps, d))
+        nz = rng(seed, cfg.cfg_id, TAG_HPOST, layer, r).standard_normal((steps, d))
+        for t in range(steps):
+            if t > 0:
+                h = AR_RHO * h + AR_SIGMA * z[t]
+            h_pre[t, r] = h
+            h_post[t, r] = h_pre[t, r].astype(np.float64) + POST_NOISE * nz[t]
+    return h_pre, h_post
+
+
+def router_scale(d: int) -> float:
+    return GATE_LOGIT_STD / (W_STD * np.sqrt((1.0 + POST_NOISE ** 2) * d))
+
+
+def router_weights(cfg: MoEConfig, layer: int, seed: int = 0):
+    """(W_g bits [E,d], W_pf bits [E,d], bias fp32 [E] or None)."""
+    s = router_scale(cfg.d)
+    base = rng(seed, cfg.cfg_id, TAG_WG, layer).standard_normal((cfg.E, cfg.d)) * (W_STD * s)
+    noise = rng(seed, cfg.cfg_id, TAG_WPF, layer).standard_normal((cfg.E, cfg.d))
+    w_pf = base + noise * (PF_NOISE * W_STD * s)
+    bias = None
+    if cfg.bias_skew:
+        bias = rng(seed, cfg.cfg_id, TAG_BIAS, layer).standard_normal(cfg.E).astype(np.float32)
+    return to_bf16_bits(base.astype(np.float32)), to_bf16_bits(w_pf.astype(np.float32)), bias
+
+
+def expert_weights(cfg: MoEConfig, layer: int, expert: int, seed: int = 0):
+    """(W1 bits [I,d], W3 bits [I,d], W2 bits [d,I]) of one SwiGLU expert."""
+    out = []
+    for tag, shape in ((TAG_W1, (cfg.I, cfg.d)), (TAG_W3, (cfg.I, cfg.d)), (TAG_W2, (cfg.d, cfg.I))):
+        g = rng(seed, cfg.cfg_id, tag, layer, expert)
+        w = g.standard_normal(shape, dtype=np.float32)
+        w *= np.float32(W_STD)
+        out.append(to_bf16_bits(w))
+    return tuple(out)
+
+
+def cdf_params(cfg: MoEConfig, layer: int, seed: int = 0):
+    """Random ordinal-model parameters (w fp32 [E], theta fp32 [E-k+1], non-decreasing).
+
+    Used to exercise the ordinal selection rule where no fitted model is at hand.
+    """
+    g = rng(seed, cfg.cfg_id, TAG_CDF, layer)
+    w = g.standard_normal(cfg.E).astype(np.float32)
+    theta = np.sort(g.standard_normal(cfg.E - cfg.k + 1) * 2.0 + 1.0).astype(np.float32)
+    return w, theta
+
+
+def uniform(seed: int, tag_index: int, shape, lo=0.0, hi=1.0, cfg_id: int = 999):
+    """Generic seeded uniforms for edge-case tests."""
+    return rng(seed, cfg_id, TAG_MISC, 0, tag_index).uniform(lo, hi, size=shape)
