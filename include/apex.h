@@ -1,0 +1,267 @@
+/*
+ * apex.h - C ABI of the MI355X (gfx950) hot path of adaptive expert prefetching for
+ * Mixture-of-Experts decode (APEX: Adaptive Expert Prefetching for Memory-Efficient
+ * Edge MoE Inference).
+ *
+ * One MoE layer, one decode step, runs as:
+ *   apex_prefetch_route   prefetch router on the pre-attention state, ranked list,
+ *                         adaptive prefetch set K_p                  (Sec. IV-A..IV-C)
+ *   apex_expert_prefetch  cache plan + host-to-HBM copies of non-resident experts of
+ *                         K_p on a side stream while attention runs  (Sec. IV-A, IV-D)
+ *   apex_gate_topk        original router top-k K_r; executed set in correctness-
+ *                         preserving or stall-free mode              (Sec. IV-E, Alg. 1)
+ *   apex_moe_ffn          gated SwiGLU experts read from HBM slots   (Sec. III-A, IV-E)
+ *   apex_expert_fetch_misses + a second apex_moe_ffn pass (accumulate = 1): the
+ *                         asynchronous miss correction of the correctness-preserving
+ *                         mode                                       (Sec. IV-E)
+ *
+ * Conventions, for every entry point:
+ *  - Buffers are owned by the caller.  No entry point allocates or frees memory.
+ *  - "device" pointers are HBM addresses (hipMalloc or equivalent); "host" pointers
+ *    are ordinary host memory; "pinned" pointers are page-locked host memory
+ *    (hipHostMalloc or equivalent).  Device pointers must be 16-byte aligned.
+ *  - Matrices are row-major.  bf16 values are passed as uint16_t bit patterns.
+ *  - Work is enqueued on the given stream and runs asynchronously to the host unless
+ *    the entry point says otherwise.  A NULL stream is the default stream.
+ *  - Arguments are validated before anything is enqueued; on an invalid argument the
+ *    call returns an error, enqueues nothing and leaves every output untouched.  The
+ *    message of the last failing call on the calling thread is apex_last_error().
+ *  - Supported sizes: 1 <= E <= 64 experts, 1 <= k <= k_max <= E, d and I multiples
+ *    of 8 (16-byte rows of bf16), B >= 0 tokens (B = 0 enqueues nothing).
+ */
+#ifndef APEX_H
+#define APEX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define APEX_ABI_VERSION 1
+#define APEX_MAX_EXPERTS 64
+#define APEX_MAX_PAIRS 1024     /* B * k limit of apex_moe_ffn */
+
+typedef enum {
+    APEX_OK = 0,
+    APEX_E_INVAL = -1,        /* invalid argument (NULL, size, alignment, range)     */
+    APEX_E_UNSUPPORTED = -2,  /* valid but outside the supported sizes above        */
+    APEX_E_HIP = -3,          /* a HIP runtime call failed; message names it        */
+    APEX_E_CAPACITY = -4      /* workspace or cache capacity too small              */
+} apex_status;
+
+/* Prefetch-set selection rule of apex_prefetch_route. */
+typedef enum {
+    APEX_SEL_CUMPROB = 0,     /* smallest ranked prefix whose prefetch probabilities
+                                 sum to >= tau, clamped to [k, k_max]               */
+    APEX_SEL_ORDINAL_CDF = 1, /* Eq. 8-9: delta_hat = min{delta : sigmoid(theta_delta
+                                 - w.x) >= tau}, m = min(k + delta_hat, k_max)      */
+    APEX_SEL_STATIC = 2       /* m = min(k + static_delta, k_max) (static over-fetch) */
+} apex_policy;
+
+/* Execution mode of apex_gate_topk (Sec. IV-E). */
+typedef enum {
+    APEX_MODE_EXACT = 0,      /* correctness-preserving: executed set = K_r          */
+    APEX_MODE_STALL_FREE = 1  /* stall-free: top-k of the available experts (Alg. 1) */
+} apex_mode;
+
+int apex_abi_version(void);
+const char *apex_last_error(void);
+
+/*
+ * Prefetch stage (Sec. IV-A step 1; Sec. IV-B Eq. 1; Sec. IV-C Eq. 8-9; Sec. IV-D).
+ * For each token b: z = W_pf h_pre[b] (+ b_pf), q_p = softmax(z), the ranked list E
+ * (descending z, lower expert id first on equal logits) and the prefetch set
+ * K_p = first m entries of E, m chosen by `policy`:
+ *   CUMPROB     first m with q_p(e_1) + ... + q_p(e_m) >= tau (m = E if none), then
+ *               clamped to [k, k_max];
+ *   ORDINAL_CDF x = q_p in ranked (descending) order, s = cdf_w . x; delta_hat = the
+ *               first delta in 0..E-k with cdf_theta[delta] - s >= ln(tau/(1-tau))
+ *               (E-k if none); m = min(k + delta_hat, k_max);
+ *   STATIC      m = min(k + static_delta, k_max).
+ * Arithmetic in fp32 (bf16 weights widened exactly).
+ *   h_pre      device fp32 [B, d]
+ *   w_pf       device bf16 [E, d]
+ *   b_pf       device fp32 [E] or NULL (no bias)
+ *   tau        coverage target in [0, 1] (CUMPROB, ORDINAL_CDF)
+ *   static_delta >= 0 (STATIC)
+ *   cdf_w      device fp32 [E], cdf_theta device fp32 [E-k+1] (ORDINAL_CDF only; may
+ *              be NULL otherwise)
+ *   pf_idx     device int32 [B, k_max] out: K_p in ranked order, -1 after position m
+ *   pf_count   device int32 [B] out: m
+ *   pf_prob    device fp32 [B, E] out, or NULL: q_p
+ */
+apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w_pf, const float *b_pf,
+                                int B, int d, int E, int k, int k_max,
+                                int policy, float tau, int static_delta,
+                                const float *cdf_w, const float *cdf_theta,
+                                int32_t *pf_idx, int32_t *pf_count, float *pf_prob,
+                                hipStream_t stream);
+
+/*
+ * Execution stage router (Sec. III-A; Sec. IV-E and Algorithm 1).
+ * For each token b: z = W_g h_post[b] (+ b_g), alpha = softmax(z),
+ * K_r = the k experts of largest z (lower id first on equal logits), and the executed
+ * set K~: K_r in EXACT mode; in STALL_FREE mode the k available experts of largest z,
+ * which is the set Algorithm 1 builds (routed experts that are available, topped up
+ * with the highest-weight available substitutes).  Gates are alpha renormalised over
+ * the set they belong to, so each row sums to 1.  If fewer than k experts are
+ * available, all of them are executed and the remaining positions hold -1 / 0.
+ * Arithmetic in fp32.
+ *   h_post        device fp32 [B, d]
+ *   w_g           device bf16 [E, d];  b_g device fp32 [E] or NULL
+ *   mode          apex_mode
+ *   avail         device uint8 (STALL_FREE only; may be NULL in EXACT mode): expert e
+ *                 is available to token b iff avail[b * avail_stride + e] != 0
+ *   avail_stride  0 (one mask shared by the batch) or >= E (one mask per token)
+ *   route_idx     device int32 [B, k] out: K_r in descending-logit order
+ *   route_gate    device fp32 [B, k] out: alpha renormalised over K_r
+ *   exec_idx      device int32 [B, k] out: K~ in descending-logit order (-1 padded)
+ *   exec_gate     device fp32 [B, k] out: alpha renormalised over K~ (0 padded)
+ *   gate_prob     device fp32 [B, E] out, or NULL: alpha
+ */
+apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, const float *b_g,
+                           int B, int d, int E, int k, int mode,
+                           const uint8_t *avail, int avail_stride,
+                           int32_t *route_idx, float *route_gate,
+                           int32_t *exec_idx, float *exec_gate,
+                           float *gate_prob, hipStream_t stream);
+
+/*
+ * Expert slot layout.  One expert occupies apex_expert_bytes(d, I) = 6 d I bytes:
+ * rows i = 0..I-1 of [W1[i, 0:d] | W3[i, 0:d]] (2 d bf16 each), then W2 [d, I]
+ * row-major.  apex_pack_expert writes that layout (host memory to host memory), so
+ * one expert moves between host and HBM as one contiguous copy.
+ */
+size_t apex_expert_bytes(int d, int I);
+apex_status apex_pack_expert(const uint16_t *w1, const uint16_t *w3, const uint16_t *w2,
+                             int d, int I, uint16_t *out);
+
+/*
+ * Gated SwiGLU experts (Sec. III-A weighted sum; Sec. IV-E aggregation with the
+ * original router weights).  For every token b and position j with e = exec_idx[b, j]
+ * in [0, E) and s = slot_of_expert[e] in [0, n_slots):
+ *   y[b] (+)= exec_gate[b, j] * W2_e (silu(W1_e x[b]) * (W3_e x[b])),
+ * silu(u) = u / (1 + exp(-u)), with W1_e, W3_e, W2_e read from slot s of `slots`.
+ * Pairs whose expert has no slot are left out of this pass, which is how the miss
+ * correction runs the missing experts in a second pass with accumulate = 1.
+ * Each expert's weights are read from HBM once per call whatever the number of
+ * tokens routed to it.  Arithmetic: fp32 accumulation of bf16 weights times fp32
+ * activations.  Result is deterministic for given inputs.
+ *   x               device fp32 [B, d]
+ *   exec_idx        device int32 [B, k];  exec_gate device fp32 [B, k]
+ *   slot_of_expert  device int32 [E]: slot index or -1
+ *   slots           device bf16 slot pool, slot s at byte offset s * apex_expert_bytes
+ *   y               device fp32 [B, d] out: overwritten (accumulate = 0) or added to
+ *                   (accumulate = 1); rows of tokens with no executed expert in this
+ *                   pass become 0 (accumulate = 0) or stay unchanged
+ *   workspace       device, >= apex_moe_ffn_workspace_bytes(B, k, I) bytes; contents
+ *                   on entry are ignored; must not be shared by calls that may overlap
+ * Requires B * k <= APEX_MAX_PAIRS.
+ */
+size_t apex_moe_ffn_workspace_bytes(int B, int k, int I);
+apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
+                         const int32_t *exec_idx, const float *exec_gate,
+                         const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,
+                         float *y, int accumulate, void *workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
+/*
+ * Cache plan of one layer for one decode step (pure host function, no HIP calls).
+ * The paper keeps a per-layer buffer that receives the prefetched set (Sec. V-C);
+ * here each layer owns C persistent HBM slots.  Rule:
+ *   P = union of the tokens' prefetched sets; an expert's count is the number of
+ *   tokens whose set holds it, its best rank the smallest position it takes in them;
+ *   target T = P if |P| <= C, else the first C of P by (count desc, best rank asc,
+ *   id asc).  Experts of T already resident stay; each other expert of T, in that
+ *   order, goes to the next free slot: empty slots (ascending) first, then slots of
+ *   residents outside T by (last_used asc, id asc).  last_used[e] = step for e in T.
+ *   pf_idx, pf_count   host [B, k_max], [B] (as written by apex_prefetch_route)
+ *   expert_of_slot     host int32 [C] in/out (-1 = empty slot)
+ *   last_used          host int64 [E] in/out (-1 = never)
+ *   copy_expert, copy_slot  host int32 [C] out: the copies in issue order
+ *   n_copies           host out
+ */
+apex_status apex_plan_residency(int E, int C, const int32_t *pf_idx, const int32_t *pf_count,
+                                int B, int k_max, int64_t step,
+                                int32_t *expert_of_slot, int64_t *last_used,
+                                int32_t *copy_expert, int32_t *copy_slot, int *n_copies);
+
+/*
+ * Prefetch of one layer (Sec. IV-A: asynchronous transfers for K_p issued while
+ * attention runs; Sec. V-B prefetch-overlap bound, Eq. 12).
+ * Runs apex_plan_residency on the host copy of the route output, then:
+ *   side:    wait readers_done (if not NULL); one host-to-device copy per planned
+ *            expert, host_experts[e] -> slots[s]; record `ready`;
+ *   compute: write the new table to slot_of_expert_dev[E] and, if not NULL, the
+ *            resident mask to avail_dev[E] (1 = resident).
+ * The caller must make the expert FFN wait for `ready` (apex_stream_wait_event)
+ * before it reads the slots, and record readers_done on the compute stream after the
+ * last kernel that reads this layer's slots.  The host call returns once everything
+ * is enqueued; the copies run on the DMA engines.
+ *   host_experts      pinned bf16 [E][expert_bytes/2] (apex_pack_expert layout)
+ *   slots             device [C][expert_bytes/2]
+ *   pf_idx, pf_count  host (pinned or pageable) copies of apex_prefetch_route's output;
+ *                     they must be complete when the call is made
+ *   expert_of_slot, last_used  host tables as in apex_plan_residency (in/out)
+ *   copied_experts    host int32 [C] out or NULL; n_copied host out or NULL
+ */
+apex_status apex_expert_prefetch(const uint16_t *host_experts, uint16_t *slots,
+                                 int E, int C, size_t expert_bytes,
+                                 const int32_t *pf_idx, const int32_t *pf_count,
+                                 int B, int k_max, int64_t step,
+                                 int32_t *expert_of_slot, int64_t *last_used,
+                                 int32_t *slot_of_expert_dev, uint8_t *avail_dev,
+                                 hipStream_t side, hipStream_t compute,
+                                 hipEvent_t readers_done, hipEvent_t ready,
+                                 int32_t *copied_experts, int *n_copied);
+
+/*
+ * Miss correction of the correctness-preserving mode (Sec. IV-E, asynchronous miss
+ * correction): the routed experts of the batch that are not resident,
+ *   M = union_b K_r[b] minus {expert_of_slot[s]},
+ * in ascending id order, are copied host -> scratch slot i (i = 0..|M|-1) on `side`
+ * after waiting for scratch_free (if not NULL), then `ready` is recorded on side.
+ * On `compute`, miss_table_dev[E] is written with miss_table[e] = i for the i-th
+ * missing expert and -1 otherwise, so a second apex_moe_ffn pass over the scratch
+ * pool with accumulate = 1 adds exactly the missing experts.  Returns APEX_E_CAPACITY
+ * (enqueueing nothing) if |M| > n_scratch.
+ *   route_idx        host int32 [B, k] (apex_gate_topk route output, complete)
+ *   expert_of_slot   host int32 [C] (resident set after this step's prefetch)
+ *   missing          host int32 [min(B*k, E)] out or NULL;  n_missing host out
+ */
+apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scratch,
+                                     int n_scratch, int E, int C, size_t expert_bytes,
+                                     const int32_t *route_idx, int B, int k,
+                                     const int32_t *expert_of_slot,
+                                     int32_t *miss_table_dev,
+                                     hipStream_t side, hipStream_t compute,
+                                     hipEvent_t scratch_free, hipEvent_t ready,
+                                     int32_t *missing, int *n_missing);
+
+/*
+ * Attention-window stand-in: one wavefront that spins for `us` microseconds of the
+ * device's constant-rate clock on `stream` (0 <= us <= 1e6), then exits.
+ */
+apex_status apex_spin_us(double us, hipStream_t stream);
+
+/* Thin event and stream helpers for callers without their own HIP bindings. */
+apex_status apex_event_create(hipEvent_t *event, int timing);
+apex_status apex_event_destroy(hipEvent_t event);
+apex_status apex_event_record(hipEvent_t event, hipStream_t stream);
+apex_status apex_event_synchronize(hipEvent_t event);
+apex_status apex_event_elapsed_ms(hipEvent_t start, hipEvent_t stop, float *ms);
+apex_status apex_stream_wait_event(hipStream_t stream, hipEvent_t event);
+apex_status apex_stream_synchronize(hipStream_t stream);
+
+/* Copy `bytes` (multiple of 16) from device src to device dst with a streaming
+ * vector-load/store kernel; used to calibrate memory counters and bandwidth. */
+apex_status apex_copy_kernel(void *dst, const void *src, size_t bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* APEX_H */

@@ -1,0 +1,283 @@
+// Prefetch router (apex_prefetch_route) and original-router top-k (apex_gate_topk).
+//
+// One workgroup of 16 wavefronts per token.  The token's hidden state is staged in
+// LDS; every wavefront streams whole rows of the bf16 router matrix with 16-byte
+// loads (4 experts at a time, so each LDS read of the hidden state feeds 4 rows) and
+// reduces its dot products with cross-lane shuffles.  Softmax, ranking and the
+// selection rules then run in wavefront 0 with one lane per expert (E <= 64).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "common.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kExpertsPerPass = 4;
+constexpr int kMaxD = 8192;            // LDS holds the fp32 hidden state (32 KB)
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+__device__ __forceinline__ float dot8(uint4 w, float4 a, float4 b, float acc) {
+    acc = fmaf(bf_lo(w.x), a.x, acc);
+    acc = fmaf(bf_hi(w.x), a.y, acc);
+    acc = fmaf(bf_lo(w.y), a.z, acc);
+    acc = fmaf(bf_hi(w.y), a.w, acc);
+    acc = fmaf(bf_lo(w.z), b.x, acc);
+    acc = fmaf(bf_hi(w.z), b.y, acc);
+    acc = fmaf(bf_lo(w.w), b.z, acc);
+    acc = fmaf(bf_hi(w.w), b.w, acc);
+    return acc;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+// z[e] = W[e, :] . h (+ bias[e]) for all experts, into LDS.  All threads call it.
+__device__ void token_logits(const float *__restrict__ h, const uint16_t *__restrict__ W,
+                             const float *__restrict__ bias, int d, int E, float *x_lds,
+                             float *z_lds) {
+    const float4 *h4 = reinterpret_cast<const float4 *>(h);
+    float4 *x4 = reinterpret_cast<float4 *>(x_lds);
+    for (int i = threadIdx.x; i < d / 4; i += kThreads) x4[i] = h4[i];
+    __syncthreads();
+
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int nch = d / 8;
+    for (int e0 = wave; e0 < E; e0 += kWaves * kExpertsPerPass) {
+        float acc[kExpertsPerPass] = {0.f, 0.f, 0.f, 0.f};
+        const uint4 *rows[kExpertsPerPass];
+#pragma unroll
+        for (int u = 0; u < kExpertsPerPass; ++u) {
+            const int e = e0 + u * kWaves;
+            rows[u] = reinterpret_cast<const uint4 *>(W + size_t(e < E ? e : 0) * d);
+        }
+        for (int c = lane; c < nch; c += kWave) {
+            const float4 a = x4[2 * c], b = x4[2 * c + 1];
+#pragma unroll
+            for (int u = 0; u < kExpertsPerPass; ++u)
+                if (e0 + u * kWaves < E) acc[u] = dot8(rows[u][c], a, b, acc[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kExpertsPerPass; ++u) {
+            const int e = e0 + u * kWaves;
+            const float s = wave_sum(acc[u]);
+            if (lane == 0 && e < E) z_lds[e] = s + (bias ? bias[e] : 0.f);
+        }
+    }
+    __syncthreads();
+}
+
+// Position of expert `lane` when experts are ordered by descending logit, lower id
+// first on equal logits, counting only experts whose bit is set in `mask`.
+__device__ __forceinline__ int masked_rank(const float *z_lds, int E, float z, int lane,
+                                           unsigned long long mask) {
+    int r = 0;
+    for (int j = 0; j < E; ++j) {
+        const float zj = z_lds[j];
+        const bool beats = (zj > z) || (zj == z && j < lane);
+        r += (beats && ((mask >> j) & 1ull)) ? 1 : 0;
+    }
+    return r;
+}
+
+__device__ __forceinline__ float logit_of(float tau) {
+    if (tau <= 0.f) return -INFINITY;
+    if (tau >= 1.f) return INFINITY;
+    return logf(tau / (1.f - tau));
+}
+
+__global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
+    const float *__restrict__ h_pre, const uint16_t *__restrict__ w_pf,
+    const float *__restrict__ b_pf, int d, int E, int k, int k_max, int policy, float tau,
+    int static_delta, const float *__restrict__ cdf_w, const float *__restrict__ cdf_theta,
+    int32_t *__restrict__ pf_idx, int32_t *__restrict__ pf_count, float *__restrict__ pf_prob) {
+    extern __shared__ float x_lds[];
+    __shared__ float z_lds[APEX_MAX_EXPERTS];
+    __shared__ float sorted_q[APEX_MAX_EXPERTS];
+    __shared__ int sorted_id[APEX_MAX_EXPERTS];
+
+    const int b = blockIdx.x;
+    token_logits(h_pre + size_t(b) * d, w_pf, b_pf, d, E, x_lds, z_lds);
+
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    if (wave != 0) return;   // selection is one wavefront's work; no barriers follow
+
+    const bool live = lane < E;
+    const float z = live ? z_lds[lane] : -INFINITY;
+    const float mx = wave_max(z);
+    const float p = live ? expf(z - mx) : 0.f;
+    const float q = p / wave_sum(p);
+    const unsigned long long all = (E == 64) ? ~0ull : ((1ull << E) - 1ull);
+    if (live) {
+        const int r = masked_rank(z_lds, E, z, lane, all);
+        sorted_q[r] = q;
+        sorted_id[r] = lane;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    const float qs = live ? sorted_q[lane] : 0.f;
+
+    int m;
+    if (policy == APEX_SEL_CUMPROB) {
+        float S = qs;   // inclusive prefix sum in ranked order
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const float t = __shfl_up(S, o, kWave);
+            if (lane >= o) S += t;
+        }
+        const unsigned long long hit = __ballot(live && S >= tau);
+        const int m_star = hit ? __ffsll(static_cast<long long>(hit)) : E;
+        m = min(max(m_star, k), k_max);
+    } else if (policy == APEX_SEL_ORDINAL_CDF) {
+        const float s = wave_sum(live ? cdf_w[lane] * qs : 0.f);
+        const float thr = logit_of(tau);
+        const bool ok = (lane <= E - k) && (cdf_theta[lane <= E - k ? lane : 0] - s >= thr);
+        const unsigned long long hit = __ballot(ok);
+        const int delta_hat = hit ? __ffsll(static_cast<long long>(hit)) - 1 : E - k;
+        m = min(k + delta_hat, k_max);
+    } else {
+        m = min(k + static_delta, k_max);
+    }
+    if (lane < k_max) pf_idx[size_t(b) * k_max + lane] = lane < m ? sorted_id[lane] : -1;
+    if (lane == 0) pf_count[b] = m;
+    if (pf_prob && live) pf_prob[size_t(b) * E + lane] = q;
+}
+
+__global__ __launch_bounds__(kThreads) void gate_topk_kernel(
+    const float *__restrict__ h_post, const uint16_t *__restrict__ w_g,
+    const float *__restrict__ b_g, int d, int E, int k, int mode,
+    const uint8_t *__restrict__ avail, int avail_stride, int32_t *__restrict__ route_idx,
+    float *__restrict__ route_gate, int32_t *__restrict__ exec_idx,
+    float *__restrict__ exec_gate, float *__restrict__ gate_prob) {
+    extern __shared__ float x_lds[];
+    __shared__ float z_lds[APEX_MAX_EXPERTS];
+
+    const int b = blockIdx.x;
+    token_logits(h_post + size_t(b) * d, w_g, b_g, d, E, x_lds, z_lds);
+
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    if (wave != 0) return;
+
+    const bool live = lane < E;
+    const float z = live ? z_lds[lane] : -INFINITY;
+    const float mx = wave_max(z);
+    const float p = live ? expf(z - mx) : 0.f;
+    const float psum = wave_sum(p);
+    const unsigned long long all = (E == 64) ? ~0ull : ((1ull << E) - 1ull);
+
+    const int r = live ? masked_rank(z_lds, E, z, lane, all) : kWave;
+    const bool sel_r = live && r < k;
+    const float rsum = wave_sum(sel_r ? p : 0.f);
+    const size_t row = size_t(b) * k;
+    if (sel_r) {
+        route_idx[row + r] = lane;
+        route_gate[row + r] = p / rsum;
+    }
+    if (mode == APEX_MODE_EXACT) {
+        if (sel_r) {
+            exec_idx[row + r] = lane;
+            exec_gate[row + r] = p / rsum;
+        }
+    } else {
+        const bool a = live && avail[size_t(b) * avail_stride + lane] != 0;
+        const unsigned long long amask = __ballot(a);
+        const int ra = a ? masked_rank(z_lds, E, z, lane, amask) : kWave;
+        const bool sel = a && ra < k;
+        const int n_sel = __popcll(__ballot(sel));
+        const float xsum = wave_sum(sel ? p : 0.f);
+        if (sel) {
+            exec_idx[row + ra] = lane;
+            exec_gate[row + ra] = p / xsum;
+        }
+        if (lane >= n_sel && lane < k) {
+            exec_idx[row + lane] = -1;
+            exec_gate[row + lane] = 0.f;
+        }
+    }
+    if (gate_prob && live) gate_prob[size_t(b) * E + lane] = p / psum;
+}
+
+apex_status check_router_args(const char *fn, const float *h, const uint16_t *w, int B, int d,
+                              int E, int k) {
+    APEX_REQUIRE(B >= 0, "%s: B=%d must be >= 0", fn, B);
+    APEX_REQUIRE(E >= 1, "%s: E=%d must be >= 1", fn, E);
+    if (E > APEX_MAX_EXPERTS)
+        return apex::fail(APEX_E_UNSUPPORTED, "%s: E=%d exceeds %d", fn, E, APEX_MAX_EXPERTS);
+    APEX_REQUIRE(k >= 1 && k <= E, "%s: k=%d out of [1, E=%d]", fn, k, E);
+    APEX_REQUIRE(d >= 8 && d % 8 == 0, "%s: d=%d must be a positive multiple of 8", fn, d);
+    if (d > kMaxD) return apex::fail(APEX_E_UNSUPPORTED, "%s: d=%d exceeds %d", fn, d, kMaxD);
+    if (B == 0) return APEX_OK;
+    APEX_REQUIRE(h && w, "%s: NULL input pointer", fn);
+    APEX_REQUIRE(apex::aligned16(h) && apex::aligned16(w), "%s: inputs must be 16-byte aligned",
+                 fn);
+    return APEX_OK;
+}
+
+}  // namespace
+
+extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w_pf,
+                                           const float *b_pf, int B, int d, int E, int k,
+                                           int k_max, int policy, float tau, int static_delta,
+                                           const float *cdf_w, const float *cdf_theta,
+                                           int32_t *pf_idx, int32_t *pf_count, float *pf_prob,
+                                           hipStream_t stream) {
+    const char *fn = "apex_prefetch_route";
+    apex_status st = check_router_args(fn, h_pre, w_pf, B, d, E, k);
+    if (st != APEX_OK) return st;
+    APEX_REQUIRE(k_max >= k && k_max <= E, "%s: k_max=%d out of [k=%d, E=%d]", fn, k_max, k, E);
+    APEX_REQUIRE(policy == APEX_SEL_CUMPROB || policy == APEX_SEL_ORDINAL_CDF ||
+                     policy == APEX_SEL_STATIC,
+                 "%s: unknown policy %d", fn, policy);
+    APEX_REQUIRE(policy == APEX_SEL_STATIC || (tau >= 0.f && tau <= 1.f),
+                 "%s: tau=%g out of [0, 1]", fn, double(tau));
+    APEX_REQUIRE(policy != APEX_SEL_STATIC || static_delta >= 0, "%s: static_delta=%d < 0", fn,
+                 static_delta);
+    APEX_REQUIRE(policy != APEX_SEL_ORDINAL_CDF || (cdf_w && cdf_theta),
+                 "%s: ORDINAL_CDF needs cdf_w and cdf_theta", fn);
+    if (B == 0) return APEX_OK;
+    APEX_REQUIRE(pf_idx && pf_count, "%s: NULL output pointer", fn);
+    hipLaunchKernelGGL(prefetch_route_kernel, dim3(B), dim3(kThreads), size_t(d) * sizeof(float),
+                       stream, h_pre, w_pf, b_pf, d, E, k, k_max, policy, tau, static_delta,
+                       cdf_w, cdf_theta, pf_idx, pf_count, pf_prob);
+    APEX_HIP(hipGetLastError());
+    return APEX_OK;
+}
+
+extern "C" apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, const float *b_g,
+                                      int B, int d, int E, int k, int mode,
+                                      const uint8_t *avail, int avail_stride, int32_t *route_idx,
+                                      float *route_gate, int32_t *exec_idx, float *exec_gate,
+                                      float *gate_prob, hipStream_t stream) {
+    const char *fn = "apex_gate_topk";
+    apex_status st = check_router_args(fn, h_post, w_g, B, d, E, k);
+    if (st != APEX_OK) return st;
+    APEX_REQUIRE(mode == APEX_MODE_EXACT || mode == APEX_MODE_STALL_FREE, "%s: unknown mode %d",
+                 fn, mode);
+    if (mode == APEX_MODE_STALL_FREE) {
+        APEX_REQUIRE(avail_stride == 0 || avail_stride >= E,
+                     "%s: avail_stride=%d must be 0 or >= E", fn, avail_stride);
+        APEX_REQUIRE(B == 0 || avail, "%s: STALL_FREE needs avail", fn);
+    }
+    if (B == 0) return APEX_OK;
+    APEX_REQUIRE(route_idx && route_gate && exec_idx && exec_gate, "%s: NULL output pointer", fn);
+    hipLaunchKernelGGL(gate_topk_kernel, dim3(B), dim3(kThreads), size_t(d) * sizeof(float),
+                       stream, h_post, w_g, b_g, d, E, k, mode, avail, avail_stride, route_idx,
+                       route_gate, exec_idx, exec_gate, gate_prob);
+    APEX_HIP(hipGetLastError());
+    return APEX_OK;
+}

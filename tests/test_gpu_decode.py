@@ -1,0 +1,96 @@
+"""End-to-end decode parity: the runner's per-layer results against the oracle.
+
+Teacher-forced where the result depends on history: the oracle's cache replay is fed
+the GPU's prefetched sets (identical to the oracle's except at counted near ties), and
+the oracle FFN is evaluated on the GPU's executed sets and gates, which are checked
+against the oracle's own separately.
+"""
+import numpy as np
+import pytest
+
+from oracle import ffn as offn
+from oracle import gating, routing
+from oracle.residency import Residency
+from paper_2608_11688_amd import configs, inputs, native
+from tests.parity import TieLedger, ffn_close
+
+pytestmark = pytest.mark.gpu
+
+
+def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau=None,
+                 ffn_every=1):
+    from paper_2608_11688_amd.runtime import DecodeRunner
+    tau = cfg.tau if tau is None else tau
+    tau32 = float(np.float32(tau))
+    runner = DecodeRunner(cfg, batch=batch, mode=mode, tau=tau32, policy=policy, steps=steps,
+                          layers=layers, t_attn_us=2.0, record=True)
+    ledger = TieLedger()
+    res = {l: Residency(cfg.E, cfg.C) for l in layers}
+    routers = {l: inputs.router_weights(cfg, l) for l in layers}
+    hs = {l: inputs.hidden_states(cfg, l, batch, steps) for l in layers}
+    cdfs = {l: inputs.cdf_params(cfg, l) for l in layers}
+    stats = dict(copies=0, misses=0, ffn_checked=0, worst_l1=0.0)
+    try:
+        for t in range(steps):
+            logs = runner.step()
+            for l in layers:
+                log = logs[l]
+                wg, wpf, bias = routers[l]
+                h_pre, h_post = hs[l][0][t], hs[l][1][t]
+                cw, ct = cdfs[l] if policy == native.SEL_ORDINAL_CDF else (None, None)
+                r = routing.prefetch_route(h_pre, wpf, bias, cfg.k, cfg.k_max, policy, tau32, 0,
+                                           cw, ct)
+                ledger.compare_rows(log.pf_count[:, None], r["pf_count"][:, None], r["margin"],
+                                    f"pf_count t{t} l{l}")
+                ledger.compare_rows(log.pf_idx, r["pf_idx"], r["margin"], f"pf_idx t{t} l{l}")
+                lists = [list(log.pf_idx[b, :log.pf_count[b]]) for b in range(batch)]
+                copies = res[l].plan(lists, t)
+                R = res[l].resident()
+                assert sorted(R) == log.resident, (t, l)
+                assert len(copies) == log.copies, (t, l)
+                avail = np.array([e in R for e in range(cfg.E)])
+                g = gating.gate_topk(h_post, wg, bias, cfg.k, mode, avail)
+                ledger.compare_rows(log.route_idx, g["route_idx"], g["margin"], f"route t{t} l{l}")
+                ledger.compare_rows(log.exec_idx, g["exec_idx"], g["margin"], f"exec t{t} l{l}")
+                if mode == native.MODE_EXACT:
+                    want = sorted(set(int(e) for e in log.route_idx.ravel()) - R)
+                    assert log.missing == want, (t, l, log.missing, want)
+                    stats["misses"] += len(want)
+                else:
+                    assert set(int(e) for e in log.exec_idx.ravel() if e >= 0) <= R
+                stats["copies"] += log.copies
+                if (t * len(layers) + layers.index(l)) % ffn_every == 0:
+                    bits = lambda e, l=l: inputs.expert_weights(cfg, l, e)
+                    y_ref = offn.moe_ffn(h_post, log.exec_idx, log.exec_gate.astype(np.float64),
+                                         bits)
+                    _, l1 = ffn_close(log.y, y_ref, f"y t{t} l{l}")
+                    stats["worst_l1"] = max(stats["worst_l1"], l1)
+                    stats["ffn_checked"] += 1
+    finally:
+        runner.close()
+    print(cfg.name, batch, mode, ledger, stats)
+    return stats
+
+
+@pytest.mark.parametrize("mode", [native.MODE_EXACT, native.MODE_STALL_FREE])
+def test_decode_tiny_all_steps(mode):
+    cfg = configs.TINY
+    st = check_decode(cfg, 1, mode, cfg.steps, [0])
+    assert st["copies"] > 0
+
+
+def test_decode_granite1b_exact():
+    cfg = configs.GRANITE_1B
+    st = check_decode(cfg, 1, native.MODE_EXACT, 4, list(range(cfg.L)), ffn_every=3)
+    assert st["copies"] > 0
+
+
+def test_decode_granite3b_batch8_stall_free_ordinal():
+    cfg = configs.GRANITE_3B
+    check_decode(cfg, 8, native.MODE_STALL_FREE, 3, [0, 17, 31],
+                 policy=native.SEL_ORDINAL_CDF)
+
+
+def test_decode_olmoe_batch16_exact():
+    cfg = configs.OLMOE
+    check_decode(cfg, 16, native.MODE_EXACT, 3, [0, 9], ffn_every=2)

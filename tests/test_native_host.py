@@ -1,0 +1,157 @@
+"""Host-side checks of the C ABI (CPU only, no compute calls).
+
+* both libraries load and export every function include/apex.h declares;
+* the C++ cache plan equals the oracle's replay, slot for slot;
+* apex_pack_expert writes the documented slot layout;
+* invalid arguments are rejected before anything is enqueued (no HIP call is made on
+  these paths, so they run without a GPU).
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+from oracle.residency import Residency
+from paper_2608_11688_amd import native
+
+
+@pytest.fixture(scope="module")
+def plan_lib():
+    return native.plan_lib()
+
+
+@pytest.fixture(scope="module")
+def hip_lib():
+    return native.lib()
+
+
+def test_header_lists_the_hot_path_entry_points():
+    names = native.header_functions()
+    for n in ("apex_prefetch_route", "apex_gate_topk", "apex_moe_ffn", "apex_expert_prefetch"):
+        assert n in names
+    assert set(names) == set(native.SIGNATURES), set(names) ^ set(native.SIGNATURES)
+
+
+def test_libraries_export_every_declared_symbol(hip_lib, plan_lib):
+    for name in native.header_functions():
+        assert hasattr(hip_lib, name), name
+    for name in native.HOST_ONLY:
+        assert hasattr(plan_lib, name), name
+    assert native.abi_version(hip_lib) == 1 and native.abi_version(plan_lib) == 1
+
+
+@pytest.mark.parametrize("E,Cs,B,k_max,steps", [(8, 4, 1, 4, 60), (32, 16, 1, 16, 80),
+                                                 (40, 16, 8, 16, 60), (64, 24, 16, 16, 40),
+                                                 (64, 64, 64, 64, 10), (5, 5, 3, 2, 30)])
+def test_cpp_plan_matches_oracle_replay(plan_lib, E, Cs, B, k_max, steps):
+    rng = np.random.default_rng(E * 1000 + Cs * 10 + B)
+    ref = Residency(E, Cs)
+    eos = np.array([s if s < E else -1 for s in range(Cs)], np.int32)
+    lu = np.full(E, -1, np.int64)
+    ce = np.zeros(Cs, np.int32)
+    cs = np.zeros(Cs, np.int32)
+    for t in range(steps):
+        pf_idx = np.full((B, k_max), -1, np.int32)
+        pf_count = np.zeros(B, np.int32)
+        lists = []
+        for b in range(B):
+            m = int(rng.integers(1, k_max + 1))
+            lst = rng.choice(E, size=m, replace=False).astype(np.int32)
+            pf_idx[b, :m] = lst
+            pf_count[b] = m
+            lists.append(list(lst))
+        want = ref.plan(lists, t)
+        n = native.apex_plan_residency(E, Cs, pf_idx, pf_count, B, k_max, t, eos, lu, ce, cs,
+                                       L=plan_lib)
+        assert [(int(ce[i]), int(cs[i])) for i in range(n)] == want
+        assert list(eos) == ref.expert_of_slot
+        assert list(lu) == ref.last_used
+
+
+def test_plan_rejects_bad_tables_without_touching_outputs(plan_lib):
+    eos = np.array([0, 0], np.int32)           # expert 0 in two slots
+    lu = np.full(4, -1, np.int64)
+    ce = np.full(2, 77, np.int32)
+    cs = np.full(2, 77, np.int32)
+    pf = np.array([[1]], np.int32)
+    cnt = np.array([1], np.int32)
+    with pytest.raises(native.ApexError) as ei:
+        native.apex_plan_residency(4, 2, pf, cnt, 1, 1, 0, eos, lu, ce, cs, L=plan_lib)
+    assert ei.value.status == native.APEX_E_INVAL and "two slots" in ei.value.message
+    assert (ce == 77).all() and (lu == -1).all()
+    eos = np.array([0, 1], np.int32)
+    with pytest.raises(native.ApexError):
+        native.apex_plan_residency(4, 2, np.array([[9]], np.int32), cnt, 1, 1, 0, eos, lu, ce,
+                                   cs, L=plan_lib)
+    assert list(eos) == [0, 1]
+
+
+def test_pack_expert_layout(plan_lib):
+    d, I = 16, 24
+    rng = np.random.default_rng(3)
+    w1 = rng.integers(0, 65535, (I, d), dtype=np.uint16)
+    w3 = rng.integers(0, 65535, (I, d), dtype=np.uint16)
+    w2 = rng.integers(0, 65535, (d, I), dtype=np.uint16)
+    nbytes = native.apex_expert_bytes(d, I, L=plan_lib)
+    assert nbytes == 6 * d * I
+    out = np.zeros(nbytes // 2, np.uint16)
+    native.apex_pack_expert(w1, w3, w2, d, I, out, L=plan_lib)
+    rows = out[:2 * I * d].reshape(I, 2 * d)
+    assert np.array_equal(rows[:, :d], w1) and np.array_equal(rows[:, d:], w3)
+    assert np.array_equal(out[2 * I * d:].reshape(d, I), w2)
+
+
+def _expect(status, fn, *args):
+    with pytest.raises(native.ApexError) as ei:
+        fn(*args)
+    assert ei.value.status == status, ei.value
+    return ei.value.message
+
+
+def test_entry_points_validate_before_enqueue(hip_lib):
+    A = 4096   # a fake, aligned, never-dereferenced address
+    # prefetch route
+    _expect(native.APEX_E_UNSUPPORTED, native.apex_prefetch_route, A, A, None, 1, 64, 65, 2, 4,
+            0, 0.9, 0, None, None, A, A, None)
+    _expect(native.APEX_E_INVAL, native.apex_prefetch_route, A, A, None, 1, 64, 8, 9, 9, 0, 0.9,
+            0, None, None, A, A, None)
+    _expect(native.APEX_E_INVAL, native.apex_prefetch_route, A, A, None, 1, 60, 8, 2, 4, 0, 0.9,
+            0, None, None, A, A, None)
+    _expect(native.APEX_E_INVAL, native.apex_prefetch_route, A, A, None, 1, 64, 8, 2, 4, 0, 1.5,
+            0, None, None, A, A, None)
+    _expect(native.APEX_E_INVAL, native.apex_prefetch_route, A, A, None, 1, 64, 8, 2, 4, 1, 0.9,
+            0, None, None, A, A, None)       # ordinal without parameters
+    _expect(native.APEX_E_INVAL, native.apex_prefetch_route, A + 4, A, None, 1, 64, 8, 2, 4, 0,
+            0.9, 0, None, None, A, A, None)  # misaligned
+    _expect(native.APEX_E_INVAL, native.apex_prefetch_route, A, A, None, 1, 64, 8, 2, 4, 0, 0.9,
+            0, None, None, None, A, None)    # NULL output
+    # gate
+    _expect(native.APEX_E_INVAL, native.apex_gate_topk, A, A, None, 1, 64, 8, 2, 1, None, 0, A, A,
+            A, A, None)                      # stall-free without a mask
+    _expect(native.APEX_E_INVAL, native.apex_gate_topk, A, A, None, 1, 64, 8, 2, 1, A, 3, A, A,
+            A, A, None)                      # stride below E
+    _expect(native.APEX_E_INVAL, native.apex_gate_topk, A, A, None, 1, 64, 8, 2, 7, A, 0, A, A,
+            A, A, None)                      # unknown mode
+    # ffn
+    msg = _expect(native.APEX_E_UNSUPPORTED, native.apex_moe_ffn, A, 129, 64, 64, 8, 8, A, A, A,
+                  A, 1, A, 0, A, 1 << 30)
+    assert "B*k" in msg
+    _expect(native.APEX_E_CAPACITY, native.apex_moe_ffn, A, 2, 64, 64, 8, 2, A, A, A, A, 1, A, 0,
+            A, 16)
+    _expect(native.APEX_E_INVAL, native.apex_moe_ffn, A, 2, 64, 60, 8, 2, A, A, A, A, 1, A, 0, A,
+            1 << 20)
+    # B = 0 is a no-op that needs no device
+    native.apex_prefetch_route(None, None, None, 0, 64, 8, 2, 4, 0, 0.9, 0, None, None, None,
+                               None, None)
+    native.apex_moe_ffn(None, 0, 64, 64, 8, 2, None, None, None, None, 1, None, 0, None, 0)
+    # misses beyond scratch capacity are refused before any copy is enqueued
+    eos = np.array([0, 1], np.int32)
+    route = np.array([[2, 3]], np.int32)
+    msg = _expect(native.APEX_E_CAPACITY, native.apex_expert_fetch_misses, A, A, 1, 4, 2, 96,
+                  route, 1, 2, eos, A, None, None, None, A)
+    assert "scratch" in msg
+
+
+def test_workspace_size():
+    assert native.apex_moe_ffn_workspace_bytes(1, 8, 512) == 8 * 512 * 4
+    assert native.apex_moe_ffn_workspace_bytes(3, 2, 24) % 256 == 0
