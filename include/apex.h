@@ -243,6 +243,83 @@ apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scr
                                      int32_t *missing, int *n_missing);
 
 /*
+ * Decode driver: one decode step through every MoE layer, in native code, composed of
+ * the entry points above in the order of the paper's two-stage runtime (Sec. IV-A;
+ * Sec. IV-D "Runtime Operation"; Sec. IV-E).  Per layer:
+ *   compute: apex_prefetch_route (K_p written to pinned host memory); attention-window
+ *            stand-in (apex_spin_us, t_attn_us);
+ *   host:    poll until the route is done; apex_expert_prefetch (copies on side);
+ *   compute: apex_gate_topk; wait for the copies; apex_moe_ffn pass 1;
+ *   EXACT:   host waits for the gate, apex_expert_fetch_misses, and if any expert is
+ *            missing: compute waits for it and runs apex_moe_ffn pass 2 (accumulate).
+ * Layers are processed in order on the compute stream, so a layer's router starts after
+ * the previous layer's FFN, as in a model where each layer feeds the next.
+ *
+ * apex_decode_create copies the configuration and the per-layer descriptors (the
+ * buffers themselves stay caller-owned and must outlive the driver) and allocates the
+ * driver's own events and pinned staging (setup time, not the hot path).
+ */
+typedef struct {
+    int L, B, d, E, k, I, C, k_max;
+    int policy;            /* apex_policy */
+    float tau;
+    int static_delta;
+    int mode;              /* apex_mode */
+    double t_attn_us;      /* attention-window stand-in per layer, >= 0 */
+    int n_scratch;         /* miss-scratch slots (EXACT), >= min(E, B*k) recommended */
+} apex_decode_config;
+
+typedef struct {
+    const uint16_t *w_pf, *w_g;            /* device bf16 [E, d] */
+    const float *b_pf, *b_g;               /* device fp32 [E] or NULL */
+    const float *cdf_w, *cdf_theta;        /* device (ORDINAL_CDF only) or NULL */
+    const uint16_t *host_experts;          /* pinned, apex_pack_expert layout, [E] experts */
+    uint16_t *slots;                       /* device, [C] experts */
+    int32_t *slot_of_expert_dev;           /* device int32 [E] (kept equal to the tables) */
+    uint8_t *avail_dev;                    /* device uint8 [E] resident mask */
+    int32_t *expert_of_slot;               /* host int32 [C] in/out */
+    int64_t *last_used;                    /* host int64 [E] in/out */
+} apex_decode_layer;
+
+typedef struct {   /* counters the driver adds to at every layer-step */
+    double overlap_sum;        /* sum over tokens of |K_r & K_p| / k (Sec. V-C overlap) */
+    double hit_sum;            /* sum over tokens of |K_r & resident| / k */
+    int64_t coverage_count;    /* tokens with K_r subset of K_p (Eq. 2) */
+    int64_t delta_hat_sum;     /* sum of m - k */
+    int64_t tokens, layer_steps, copies, misses;
+} apex_decode_stats;
+
+typedef struct {   /* optional per-step record, host arrays (caller-owned), any may be NULL */
+    int32_t *pf_idx;       /* [L][B][k_max] */
+    int32_t *pf_count;     /* [L][B] */
+    int32_t *route_idx;    /* [L][B][k] */
+    float *route_gate;     /* [L][B][k] */
+    int32_t *exec_idx;     /* [L][B][k] */
+    float *exec_gate;      /* [L][B][k] */
+    int32_t *resident;     /* [L][C] expert_of_slot after the step's prefetch */
+    int32_t *n_copies;     /* [L] */
+    int32_t *missing;      /* [L][E] missing routed experts (EXACT) */
+    int32_t *n_missing;    /* [L] */
+} apex_decode_record;
+
+typedef struct apex_decode apex_decode;
+
+apex_status apex_decode_create(apex_decode **out, const apex_decode_config *cfg,
+                               const apex_decode_layer *layers, uint16_t *scratch,
+                               int32_t *miss_table_dev, int32_t *exec_idx_dev,
+                               float *exec_gate_dev, void *workspace, size_t workspace_bytes,
+                               hipStream_t compute, hipStream_t side);
+/* One decode step.  h_pre, h_post, y: host arrays of L device pointers to [B, d] fp32.
+ * Returns when everything is enqueued (with `record`, after the step has completed and
+ * the record is filled).  stats (may be NULL) is added to. */
+apex_status apex_decode_step(apex_decode *dec, int64_t step, const float *const *h_pre,
+                             const float *const *h_post, float *const *y,
+                             apex_decode_stats *stats, apex_decode_record *record);
+/* Waits for all enqueued work and folds the statistics of the last layers into stats. */
+apex_status apex_decode_finish(apex_decode *dec, apex_decode_stats *stats);
+apex_status apex_decode_destroy(apex_decode *dec);
+
+/*
  * Attention-window stand-in: one wavefront that spins for `us` microseconds of the
  * device's constant-rate clock on `stream` (0 <= us <= 1e6), then exits.
  */

@@ -1,0 +1,299 @@
+// Decode driver: every layer of one decode step in native code (see apex.h).
+//
+// The host only has to see the prefetched set (to plan and issue the copies) and, in
+// the correctness-preserving mode, the routed set (to fetch misses).  Both are written
+// by the kernels straight into pinned host memory; the host polls the events that
+// follow them instead of sleeping, so the hand-off costs microseconds.  Overlap
+// statistics are folded in lazily, once a layer's gate is known to have finished.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <vector>
+
+#include "common.h"
+
+struct apex_decode {
+    apex_decode_config cfg;
+    std::vector<apex_decode_layer> layers;
+    uint16_t *scratch = nullptr;
+    int32_t *miss_table = nullptr;
+    int32_t *exec_idx = nullptr;
+    float *exec_gate = nullptr;
+    void *ws = nullptr;
+    size_t ws_bytes = 0;
+    hipStream_t compute = nullptr, side = nullptr;
+    size_t expert_bytes = 0;
+    // pinned staging
+    int32_t *pf_idx_h = nullptr;      // [B][k_max]
+    int32_t *pf_count_h = nullptr;    // [B]
+    int32_t *route_idx_h = nullptr;   // [L][B][k]
+    float *route_gate_h = nullptr;    // [L][B][k]
+    // events
+    hipEvent_t ev_route = nullptr, ready_miss = nullptr, scratch_free = nullptr;
+    std::vector<hipEvent_t> ready, readers_done, gate_done;
+    // statistics of layers whose gate may still be running
+    struct Pending {
+        int layer;
+        std::vector<int32_t> pf;       // [B][k_max]
+        std::vector<int32_t> cnt;      // [B]
+        std::vector<char> resident;    // [E]
+        int copies, misses;
+    };
+    std::vector<Pending> pending;
+};
+
+namespace {
+
+// Busy-polls an event (lower wake-up latency than a blocking wait); gives up after
+// 30 s so that a device that stopped making progress surfaces as an error.
+apex_status poll(hipEvent_t ev) {
+    const auto t0 = std::chrono::steady_clock::now();
+    for (unsigned it = 0;; ++it) {
+        const hipError_t e = hipEventQuery(ev);
+        if (e == hipSuccess) return APEX_OK;
+        if (e != hipErrorNotReady)
+            return apex::fail(APEX_E_HIP, "hipEventQuery failed: %s", hipGetErrorString(e));
+        if ((it & 1023u) == 1023u &&
+            std::chrono::steady_clock::now() - t0 > std::chrono::seconds(30))
+            return apex::fail(APEX_E_HIP, "apex_decode_step: event not reached after 30 s");
+    }
+}
+
+void fold(apex_decode *dec, const apex_decode::Pending &p, apex_decode_stats *st) {
+    if (!st) return;
+    const apex_decode_config &c = dec->cfg;
+    const int32_t *route = dec->route_idx_h + size_t(p.layer) * c.B * c.k;
+    for (int b = 0; b < c.B; ++b) {
+        char in_p[APEX_MAX_EXPERTS] = {0};
+        for (int j = 0; j < p.cnt[b]; ++j) in_p[p.pf[size_t(b) * c.k_max + j]] = 1;
+        int both = 0, hit = 0;
+        for (int j = 0; j < c.k; ++j) {
+            const int e = route[size_t(b) * c.k + j];
+            if (e < 0 || e >= c.E) continue;
+            both += in_p[e];
+            hit += p.resident[e];
+        }
+        st->overlap_sum += double(both) / c.k;
+        st->hit_sum += double(hit) / c.k;
+        st->coverage_count += both == c.k ? 1 : 0;
+        st->delta_hat_sum += p.cnt[b] - c.k;
+    }
+    st->tokens += c.B;
+    st->layer_steps += 1;
+    st->copies += p.copies;
+    st->misses += p.misses;
+}
+
+void fold_pending(apex_decode *dec, apex_decode_stats *st) {
+    for (const auto &p : dec->pending) fold(dec, p, st);
+    dec->pending.clear();
+}
+
+}  // namespace
+
+extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_config *cfg,
+                                          const apex_decode_layer *layers, uint16_t *scratch,
+                                          int32_t *miss_table_dev, int32_t *exec_idx_dev,
+                                          float *exec_gate_dev, void *workspace,
+                                          size_t workspace_bytes, hipStream_t compute,
+                                          hipStream_t side) {
+    const char *fn = "apex_decode_create";
+    APEX_REQUIRE(out && cfg && layers, "%s: NULL argument", fn);
+    const apex_decode_config &c = *cfg;
+    APEX_REQUIRE(c.L >= 1 && c.B >= 1, "%s: L=%d B=%d", fn, c.L, c.B);
+    APEX_REQUIRE(c.E >= 1 && c.E <= APEX_MAX_EXPERTS, "%s: E=%d", fn, c.E);
+    APEX_REQUIRE(c.k >= 1 && c.k <= c.k_max && c.k_max <= c.C && c.C <= c.E,
+                 "%s: need 1 <= k <= k_max <= C <= E (k=%d k_max=%d C=%d E=%d)", fn, c.k,
+                 c.k_max, c.C, c.E);
+    APEX_REQUIRE(c.t_attn_us >= 0.0 && c.t_attn_us <= 1e6, "%s: t_attn_us=%g", fn, c.t_attn_us);
+    APEX_REQUIRE(c.mode == APEX_MODE_EXACT || c.mode == APEX_MODE_STALL_FREE, "%s: mode %d", fn,
+                 c.mode);
+    APEX_REQUIRE(c.mode != APEX_MODE_EXACT || (scratch && miss_table_dev && c.n_scratch >= 1),
+                 "%s: EXACT mode needs a miss scratch pool", fn);
+    APEX_REQUIRE(exec_idx_dev && exec_gate_dev && workspace, "%s: NULL buffer", fn);
+    for (int l = 0; l < c.L; ++l) {
+        const apex_decode_layer &y = layers[l];
+        APEX_REQUIRE(y.w_pf && y.w_g && y.host_experts && y.slots && y.slot_of_expert_dev &&
+                         y.expert_of_slot && y.last_used,
+                     "%s: layer %d has a NULL buffer", fn, l);
+    }
+    auto *dec = new apex_decode();
+    dec->cfg = c;
+    dec->layers.assign(layers, layers + c.L);
+    dec->scratch = scratch;
+    dec->miss_table = miss_table_dev;
+    dec->exec_idx = exec_idx_dev;
+    dec->exec_gate = exec_gate_dev;
+    dec->ws = workspace;
+    dec->ws_bytes = workspace_bytes;
+    dec->compute = compute;
+    dec->side = side;
+    dec->expert_bytes = apex_expert_bytes(c.d, c.I);
+    auto cleanup = [&](apex_status st) {
+        apex_decode_destroy(dec);
+        return st;
+    };
+    hipError_t e = hipSuccess;
+    e = hipHostMalloc(reinterpret_cast<void **>(&dec->pf_idx_h), sizeof(int32_t) * c.B * c.k_max);
+    if (e == hipSuccess)
+        e = hipHostMalloc(reinterpret_cast<void **>(&dec->pf_count_h), sizeof(int32_t) * c.B);
+    if (e == hipSuccess)
+        e = hipHostMalloc(reinterpret_cast<void **>(&dec->route_idx_h),
+                          sizeof(int32_t) * c.L * c.B * c.k);
+    if (e == hipSuccess)
+        e = hipHostMalloc(reinterpret_cast<void **>(&dec->route_gate_h),
+                          sizeof(float) * c.L * c.B * c.k);
+    if (e != hipSuccess)
+        return cleanup(apex::fail(APEX_E_HIP, "%s: hipHostMalloc failed: %s", fn,
+                                  hipGetErrorString(e)));
+    auto mk = [&](hipEvent_t *ev) {
+        return hipEventCreateWithFlags(ev, hipEventDisableTiming);
+    };
+    if (mk(&dec->ev_route) != hipSuccess || mk(&dec->ready_miss) != hipSuccess ||
+        mk(&dec->scratch_free) != hipSuccess)
+        return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
+    dec->ready.resize(c.L);
+    dec->readers_done.resize(c.L);
+    dec->gate_done.resize(c.L);
+    for (int l = 0; l < c.L; ++l)
+        if (mk(&dec->ready[l]) != hipSuccess || mk(&dec->readers_done[l]) != hipSuccess ||
+            mk(&dec->gate_done[l]) != hipSuccess)
+            return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
+    *out = dec;
+    return APEX_OK;
+}
+
+extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
+                                        const float *const *h_pre, const float *const *h_post,
+                                        float *const *y, apex_decode_stats *stats,
+                                        apex_decode_record *rec) {
+    const char *fn = "apex_decode_step";
+    APEX_REQUIRE(dec && h_pre && h_post && y, "%s: NULL argument", fn);
+    const apex_decode_config &c = dec->cfg;
+    const hipStream_t cs = dec->compute, ss = dec->side;
+    std::vector<int32_t> copied(c.C), missing(c.E);
+    apex_status st;
+    for (int l = 0; l < c.L; ++l) {
+        const apex_decode_layer &Ly = dec->layers[l];
+        // prefetch stage: router on the pre-attention state, then the attention window
+        st = apex_prefetch_route(h_pre[l], Ly.w_pf, Ly.b_pf, c.B, c.d, c.E, c.k, c.k_max,
+                                 c.policy, c.tau, c.static_delta, Ly.cdf_w, Ly.cdf_theta,
+                                 dec->pf_idx_h, dec->pf_count_h, nullptr, cs);
+        if (st != APEX_OK) return st;
+        APEX_HIP(hipEventRecord(dec->ev_route, cs));
+        if (c.t_attn_us > 0) {
+            st = apex_spin_us(c.t_attn_us, cs);
+            if (st != APEX_OK) return st;
+        }
+        st = poll(dec->ev_route);
+        if (st != APEX_OK) return st;
+        // earlier layers' gates precede this route on the stream: fold their statistics
+        fold_pending(dec, stats);
+        int n_copy = 0;
+        st = apex_expert_prefetch(Ly.host_experts, Ly.slots, c.E, c.C, dec->expert_bytes,
+                                  dec->pf_idx_h, dec->pf_count_h, c.B, c.k_max, step,
+                                  Ly.expert_of_slot, Ly.last_used, Ly.slot_of_expert_dev,
+                                  Ly.avail_dev, ss, cs, dec->readers_done[l], dec->ready[l],
+                                  copied.data(), &n_copy);
+        if (st != APEX_OK) return st;
+        apex_decode::Pending p;
+        p.layer = l;
+        p.pf.assign(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max);
+        p.cnt.assign(dec->pf_count_h, dec->pf_count_h + c.B);
+        p.resident.assign(c.E, 0);
+        for (int s = 0; s < c.C; ++s)
+            if (Ly.expert_of_slot[s] >= 0) p.resident[Ly.expert_of_slot[s]] = 1;
+        p.copies = n_copy;
+        p.misses = 0;
+        if (rec) {
+            if (rec->pf_idx)
+                std::memcpy(rec->pf_idx + size_t(l) * c.B * c.k_max, dec->pf_idx_h,
+                            sizeof(int32_t) * c.B * c.k_max);
+            if (rec->pf_count)
+                std::memcpy(rec->pf_count + size_t(l) * c.B, dec->pf_count_h,
+                            sizeof(int32_t) * c.B);
+            if (rec->resident)
+                std::memcpy(rec->resident + size_t(l) * c.C, Ly.expert_of_slot,
+                            sizeof(int32_t) * c.C);
+            if (rec->n_copies) rec->n_copies[l] = n_copy;
+        }
+        // execution stage: original router, then the experts once the copies landed
+        int32_t *route_h = dec->route_idx_h + size_t(l) * c.B * c.k;
+        float *route_g = dec->route_gate_h + size_t(l) * c.B * c.k;
+        st = apex_gate_topk(h_post[l], Ly.w_g, Ly.b_g, c.B, c.d, c.E, c.k, c.mode, Ly.avail_dev,
+                            0, route_h, route_g, dec->exec_idx, dec->exec_gate, nullptr, cs);
+        if (st != APEX_OK) return st;
+        APEX_HIP(hipEventRecord(dec->gate_done[l], cs));
+        APEX_HIP(hipStreamWaitEvent(cs, dec->ready[l], 0));
+        st = apex_moe_ffn(h_post[l], c.B, c.d, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate,
+                          Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], 0, dec->ws, dec->ws_bytes,
+                          cs);
+        if (st != APEX_OK) return st;
+        int n_miss = 0;
+        if (c.mode == APEX_MODE_EXACT) {
+            // asynchronous miss correction: the resident experts run while misses copy
+            st = poll(dec->gate_done[l]);
+            if (st != APEX_OK) return st;
+            st = apex_expert_fetch_misses(Ly.host_experts, dec->scratch, c.n_scratch, c.E, c.C,
+                                          dec->expert_bytes, route_h, c.B, c.k,
+                                          Ly.expert_of_slot, dec->miss_table, ss, cs,
+                                          dec->scratch_free, dec->ready_miss, missing.data(),
+                                          &n_miss);
+            if (st != APEX_OK) return st;
+            if (n_miss > 0) {
+                APEX_HIP(hipStreamWaitEvent(cs, dec->ready_miss, 0));
+                st = apex_moe_ffn(h_post[l], c.B, c.d, c.I, c.E, c.k, dec->exec_idx,
+                                  dec->exec_gate, dec->miss_table, dec->scratch, c.n_scratch,
+                                  y[l], 1, dec->ws, dec->ws_bytes, cs);
+                if (st != APEX_OK) return st;
+                APEX_HIP(hipEventRecord(dec->scratch_free, cs));
+            }
+        }
+        APEX_HIP(hipEventRecord(dec->readers_done[l], cs));
+        p.misses = n_miss;
+        dec->pending.push_back(std::move(p));
+        if (rec) {
+            APEX_HIP(hipStreamSynchronize(cs));
+            const size_t bk = size_t(c.B) * c.k;
+            if (rec->route_idx) std::memcpy(rec->route_idx + l * bk, route_h, 4 * bk);
+            if (rec->route_gate) std::memcpy(rec->route_gate + l * bk, route_g, 4 * bk);
+            if (rec->exec_idx)
+                APEX_HIP(hipMemcpy(rec->exec_idx + l * bk, dec->exec_idx, 4 * bk,
+                                   hipMemcpyDeviceToHost));
+            if (rec->exec_gate)
+                APEX_HIP(hipMemcpy(rec->exec_gate + l * bk, dec->exec_gate, 4 * bk,
+                                   hipMemcpyDeviceToHost));
+            if (rec->missing)
+                for (int i = 0; i < n_miss; ++i) rec->missing[size_t(l) * c.E + i] = missing[i];
+            if (rec->n_missing) rec->n_missing[l] = n_miss;
+        }
+    }
+    if (rec) fold_pending(dec, stats);
+    return APEX_OK;
+}
+
+extern "C" apex_status apex_decode_finish(apex_decode *dec, apex_decode_stats *stats) {
+    APEX_REQUIRE(dec, "apex_decode_finish: NULL driver");
+    APEX_HIP(hipStreamSynchronize(dec->compute));
+    APEX_HIP(hipStreamSynchronize(dec->side));
+    fold_pending(dec, stats);
+    return APEX_OK;
+}
+
+extern "C" apex_status apex_decode_destroy(apex_decode *dec) {
+    if (!dec) return APEX_OK;
+    if (dec->compute) (void)hipStreamSynchronize(dec->compute);
+    if (dec->side) (void)hipStreamSynchronize(dec->side);
+    for (hipEvent_t e : {dec->ev_route, dec->ready_miss, dec->scratch_free})
+        if (e) (void)hipEventDestroy(e);
+    for (auto *v : {&dec->ready, &dec->readers_done, &dec->gate_done})
+        for (hipEvent_t e : *v)
+            if (e) (void)hipEventDestroy(e);
+    for (void *p : {static_cast<void *>(dec->pf_idx_h), static_cast<void *>(dec->pf_count_h),
+                    static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h)})
+        if (p) (void)hipHostFree(p);
+    delete dec;
+    return APEX_OK;
+}

@@ -1,10 +1,10 @@
 // Prefetch router (apex_prefetch_route) and original-router top-k (apex_gate_topk).
 //
-// One workgroup of 16 wavefronts per token.  The token's hidden state is staged in
-// LDS; every wavefront streams whole rows of the bf16 router matrix with 16-byte
-// loads (4 experts at a time, so each LDS read of the hidden state feeds 4 rows) and
-// reduces its dot products with cross-lane shuffles.  Softmax, ranking and the
-// selection rules then run in wavefront 0 with one lane per expert (E <= 64).
+// One workgroup of 16 wavefronts per token.  Every wavefront streams whole rows of the
+// bf16 router matrix with 16-byte loads (up to 4 experts at a time, sharing each read of
+// the hidden state) and reduces its dot products with cross-lane shuffles.  Softmax,
+// ranking and the selection rules then run in wavefront 0 with one lane per expert
+// (E <= 64), exchanging values through registers (readlane, shuffles, ballots).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -17,7 +17,7 @@ constexpr int kWave = 64;
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kExpertsPerPass = 4;
-constexpr int kMaxD = 8192;            // LDS holds the fp32 hidden state (32 KB)
+constexpr int kMaxD = 65536;
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -47,14 +47,11 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // z[e] = W[e, :] . h (+ bias[e]) for all experts, into LDS.  All threads call it.
+// The hidden state is read straight from global memory (every wavefront reads the same
+// chunks, so after the first they hit the vector cache); no load waits on another.
 __device__ void token_logits(const float *__restrict__ h, const uint16_t *__restrict__ W,
-                             const float *__restrict__ bias, int d, int E, float *x_lds,
-                             float *z_lds) {
+                             const float *__restrict__ bias, int d, int E, float *z_lds) {
     const float4 *h4 = reinterpret_cast<const float4 *>(h);
-    float4 *x4 = reinterpret_cast<float4 *>(x_lds);
-    for (int i = threadIdx.x; i < d / 4; i += kThreads) x4[i] = h4[i];
-    __syncthreads();
-
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int nch = d / 8;
     for (int e0 = wave; e0 < E; e0 += kWaves * kExpertsPerPass) {
@@ -66,10 +63,14 @@ __device__ void token_logits(const float *__restrict__ h, const uint16_t *__rest
             rows[u] = reinterpret_cast<const uint4 *>(W + size_t(e < E ? e : 0) * d);
         }
         for (int c = lane; c < nch; c += kWave) {
-            const float4 a = x4[2 * c], b = x4[2 * c + 1];
+            uint4 w[kExpertsPerPass];
 #pragma unroll
             for (int u = 0; u < kExpertsPerPass; ++u)
-                if (e0 + u * kWaves < E) acc[u] = dot8(rows[u][c], a, b, acc[u]);
+                if (e0 + u * kWaves < E) w[u] = rows[u][c];
+            const float4 a = h4[2 * c], b = h4[2 * c + 1];
+#pragma unroll
+            for (int u = 0; u < kExpertsPerPass; ++u)
+                if (e0 + u * kWaves < E) acc[u] = dot8(w[u], a, b, acc[u]);
         }
 #pragma unroll
         for (int u = 0; u < kExpertsPerPass; ++u) {
@@ -82,12 +83,13 @@ __device__ void token_logits(const float *__restrict__ h, const uint16_t *__rest
 }
 
 // Position of expert `lane` when experts are ordered by descending logit, lower id
-// first on equal logits, counting only experts whose bit is set in `mask`.
-__device__ __forceinline__ int masked_rank(const float *z_lds, int E, float z, int lane,
-                                           unsigned long long mask) {
+// first on equal logits, counting only experts whose bit is set in `mask`.  Other
+// lanes' logits are read with readlane (register to scalar), not through LDS.
+__device__ __forceinline__ int masked_rank(float z, int E, int lane, unsigned long long mask) {
     int r = 0;
+    const int zi = __float_as_int(z);
     for (int j = 0; j < E; ++j) {
-        const float zj = z_lds[j];
+        const float zj = __int_as_float(__builtin_amdgcn_readlane(zi, j));
         const bool beats = (zj > z) || (zj == z && j < lane);
         r += (beats && ((mask >> j) & 1ull)) ? 1 : 0;
     }
@@ -105,13 +107,12 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     const float *__restrict__ b_pf, int d, int E, int k, int k_max, int policy, float tau,
     int static_delta, const float *__restrict__ cdf_w, const float *__restrict__ cdf_theta,
     int32_t *__restrict__ pf_idx, int32_t *__restrict__ pf_count, float *__restrict__ pf_prob) {
-    extern __shared__ float x_lds[];
     __shared__ float z_lds[APEX_MAX_EXPERTS];
     __shared__ float sorted_q[APEX_MAX_EXPERTS];
     __shared__ int sorted_id[APEX_MAX_EXPERTS];
 
     const int b = blockIdx.x;
-    token_logits(h_pre + size_t(b) * d, w_pf, b_pf, d, E, x_lds, z_lds);
+    token_logits(h_pre + size_t(b) * d, w_pf, b_pf, d, E, z_lds);
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     if (wave != 0) return;   // selection is one wavefront's work; no barriers follow
@@ -122,8 +123,8 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     const float p = live ? expf(z - mx) : 0.f;
     const float q = p / wave_sum(p);
     const unsigned long long all = (E == 64) ? ~0ull : ((1ull << E) - 1ull);
+    const int r = masked_rank(z, E, lane, all);   // whole wavefront: readlane inside
     if (live) {
-        const int r = masked_rank(z_lds, E, z, lane, all);
         sorted_q[r] = q;
         sorted_id[r] = lane;
     }
@@ -164,11 +165,10 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     const uint8_t *__restrict__ avail, int avail_stride, int32_t *__restrict__ route_idx,
     float *__restrict__ route_gate, int32_t *__restrict__ exec_idx,
     float *__restrict__ exec_gate, float *__restrict__ gate_prob) {
-    extern __shared__ float x_lds[];
     __shared__ float z_lds[APEX_MAX_EXPERTS];
 
     const int b = blockIdx.x;
-    token_logits(h_post + size_t(b) * d, w_g, b_g, d, E, x_lds, z_lds);
+    token_logits(h_post + size_t(b) * d, w_g, b_g, d, E, z_lds);
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     if (wave != 0) return;
@@ -180,7 +180,7 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     const float psum = wave_sum(p);
     const unsigned long long all = (E == 64) ? ~0ull : ((1ull << E) - 1ull);
 
-    const int r = live ? masked_rank(z_lds, E, z, lane, all) : kWave;
+    const int r = masked_rank(z, E, lane, all);
     const bool sel_r = live && r < k;
     const float rsum = wave_sum(sel_r ? p : 0.f);
     const size_t row = size_t(b) * k;
@@ -196,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     } else {
         const bool a = live && avail[size_t(b) * avail_stride + lane] != 0;
         const unsigned long long amask = __ballot(a);
-        const int ra = a ? masked_rank(z_lds, E, z, lane, amask) : kWave;
+        const int ra = masked_rank(z, E, lane, amask);
         const bool sel = a && ra < k;
         const int n_sel = __popcll(__ballot(sel));
         const float xsum = wave_sum(sel ? p : 0.f);
@@ -251,7 +251,7 @@ extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w
                  "%s: ORDINAL_CDF needs cdf_w and cdf_theta", fn);
     if (B == 0) return APEX_OK;
     APEX_REQUIRE(pf_idx && pf_count, "%s: NULL output pointer", fn);
-    hipLaunchKernelGGL(prefetch_route_kernel, dim3(B), dim3(kThreads), size_t(d) * sizeof(float),
+    hipLaunchKernelGGL(prefetch_route_kernel, dim3(B), dim3(kThreads), 0,
                        stream, h_pre, w_pf, b_pf, d, E, k, k_max, policy, tau, static_delta,
                        cdf_w, cdf_theta, pf_idx, pf_count, pf_prob);
     APEX_HIP(hipGetLastError());
@@ -275,7 +275,7 @@ extern "C" apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, 
     }
     if (B == 0) return APEX_OK;
     APEX_REQUIRE(route_idx && route_gate && exec_idx && exec_gate, "%s: NULL output pointer", fn);
-    hipLaunchKernelGGL(gate_topk_kernel, dim3(B), dim3(kThreads), size_t(d) * sizeof(float),
+    hipLaunchKernelGGL(gate_topk_kernel, dim3(B), dim3(kThreads), 0,
                        stream, h_post, w_g, b_g, d, E, k, mode, avail, avail_stride, route_idx,
                        route_gate, exec_idx, exec_gate, gate_prob);
     APEX_HIP(hipGetLastError());

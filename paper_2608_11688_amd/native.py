@@ -40,6 +40,31 @@ class ApexLibraryMissing(ImportError):
 P = C.c_void_p
 I32, I64, F32, F64, SZ = C.c_int, C.c_int64, C.c_float, C.c_double, C.c_size_t
 
+
+class DecodeConfig(C.Structure):
+    _fields_ = [(n, C.c_int) for n in ("L", "B", "d", "E", "k", "I", "C", "k_max", "policy")] + [
+        ("tau", C.c_float), ("static_delta", C.c_int), ("mode", C.c_int),
+        ("t_attn_us", C.c_double), ("n_scratch", C.c_int)]
+
+
+class DecodeLayer(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in (
+        "w_pf", "w_g", "b_pf", "b_g", "cdf_w", "cdf_theta", "host_experts", "slots",
+        "slot_of_expert_dev", "avail_dev", "expert_of_slot", "last_used")]
+
+
+class DecodeStats(C.Structure):
+    _fields_ = [("overlap_sum", C.c_double), ("hit_sum", C.c_double),
+                ("coverage_count", C.c_int64), ("delta_hat_sum", C.c_int64),
+                ("tokens", C.c_int64), ("layer_steps", C.c_int64), ("copies", C.c_int64),
+                ("misses", C.c_int64)]
+
+
+class DecodeRecord(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in (
+        "pf_idx", "pf_count", "route_idx", "route_gate", "exec_idx", "exec_gate", "resident",
+        "n_copies", "missing", "n_missing")]
+
 # name -> (restype, argtypes)
 SIGNATURES = {
     "apex_abi_version": (C.c_int, []),
@@ -56,6 +81,10 @@ SIGNATURES = {
                                    P, P, P]),
     "apex_expert_fetch_misses": (I32, [P, P, I32, I32, I32, SZ, P, I32, I32, P, P, P, P, P, P, P,
                                        P]),
+    "apex_decode_create": (I32, [P, C.POINTER(DecodeConfig), P, P, P, P, P, P, SZ, P, P]),
+    "apex_decode_step": (I32, [P, I64, P, P, P, P, P]),
+    "apex_decode_finish": (I32, [P, P]),
+    "apex_decode_destroy": (I32, [P]),
     "apex_spin_us": (I32, [F64, P]),
     "apex_event_create": (I32, [P, I32]),
     "apex_event_destroy": (I32, [P]),
@@ -197,6 +226,28 @@ def apex_expert_fetch_misses(host_experts, scratch, n_scratch, E, Cslots, expert
           expert_bytes, ptr(route_idx), B, k, ptr(expert_of_slot), ptr(miss_table_dev), side,
           compute, scratch_free, ready, ptr(missing), C.byref(n))
     return n.value
+
+
+def apex_decode_create(cfg, layers, scratch, miss_table, exec_idx, exec_gate, workspace,
+                       workspace_bytes, compute, side):
+    out = C.c_void_p()
+    arr = (DecodeLayer * len(layers))(*layers)
+    _call("apex_decode_create", C.byref(out), C.byref(cfg), arr, ptr(scratch), ptr(miss_table),
+          ptr(exec_idx), ptr(exec_gate), ptr(workspace), workspace_bytes, compute, side)
+    return out.value, arr
+
+
+def apex_decode_step(dec, step, h_pre_ptrs, h_post_ptrs, y_ptrs, stats=None, record=None):
+    _call("apex_decode_step", dec, step, h_pre_ptrs, h_post_ptrs, y_ptrs,
+          None if stats is None else C.byref(stats), None if record is None else C.byref(record))
+
+
+def apex_decode_finish(dec, stats=None):
+    _call("apex_decode_finish", dec, None if stats is None else C.byref(stats))
+
+
+def apex_decode_destroy(dec):
+    _call("apex_decode_destroy", dec)
 
 
 def apex_spin_us(us, stream=None):
