@@ -158,11 +158,11 @@ apex_status apex_pack_expert(const uint16_t *w1, const uint16_t *w3, const uint1
  *   y               device fp32 [B, d] out: overwritten (accumulate = 0) or added to
  *                   (accumulate = 1); rows of tokens with no executed expert in this
  *                   pass become 0 (accumulate = 0) or stay unchanged
- *   workspace       device, >= apex_moe_ffn_workspace_bytes(B, k, I) bytes; contents
+ *   workspace       device, >= apex_moe_ffn_workspace_bytes(B, d, I, k) bytes; contents
  *                   on entry are ignored; must not be shared by calls that may overlap
  * Requires B * k <= APEX_MAX_PAIRS.
  */
-size_t apex_moe_ffn_workspace_bytes(int B, int k, int I);
+size_t apex_moe_ffn_workspace_bytes(int B, int d, int I, int k);
 apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
                          const int32_t *exec_idx, const float *exec_gate,
                          const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,

@@ -13,6 +13,7 @@
 // pairs, a few hundred LDS operations) instead of paying a separate launch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -393,13 +394,304 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1(
     }
 }
 
+// ---------------------------------------------------------------------------------
+// Batched path (B >= 16): grouped GEMMs on the matrix cores.
+//
+// group_pairs (one workgroup) writes the (expert, token) grouping once per call; the
+// GEMM kernels take tokens as the M dimension (tiles of 16, padded), weight rows as N
+// and the hidden / intermediate dimension as K, with v_mfma_f32_16x16x32_bf16
+// (activations rounded to bf16, fp32 accumulation).  Every expert's weights are read
+// once per call whatever the number of tokens routed to it.  Per-pair outputs go to
+// the workspace and a combine kernel applies the gates in a fixed order.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+struct GroupTable {          // lives at the start of the workspace
+    int n_act;
+    int n_items;
+    int act_e[APEX_MAX_EXPERTS];
+    int act_start[APEX_MAX_EXPERTS + 1];
+    int item[APEX_MAX_PAIRS];   // pair indices sorted by (expert, pair)
+};
+
+constexpr int kGroupThreads = 1024;
+
+// Every workgroup rounds a slice of the activations to bf16 (xb [B, d], 8 values per
+// thread per step) for the matrix cores; workgroup 0 also builds the grouping.
+__global__ __launch_bounds__(kGroupThreads) void group_pairs(
+    const int32_t *__restrict__ exec_idx, const int32_t *__restrict__ slot_of_expert, int P, int E,
+    int n_slots, GroupTable *__restrict__ G, const float *__restrict__ x, int B, int d,
+    __bf16 *__restrict__ xb) {
+    const size_t n8 = size_t(B) * d / 8;
+    for (size_t i = size_t(blockIdx.x) * kGroupThreads + threadIdx.x; i < n8;
+         i += size_t(gridDim.x) * kGroupThreads) {
+        const float4 p = reinterpret_cast<const float4 *>(x)[2 * i];
+        const float4 q = reinterpret_cast<const float4 *>(x)[2 * i + 1];
+        bf16x8 v;
+        v[0] = (__bf16)p.x; v[1] = (__bf16)p.y; v[2] = (__bf16)p.z; v[3] = (__bf16)p.w;
+        v[4] = (__bf16)q.x; v[5] = (__bf16)q.y; v[6] = (__bf16)q.z; v[7] = (__bf16)q.w;
+        reinterpret_cast<bf16x8 *>(xb)[i] = v;
+    }
+    if (blockIdx.x != 0) return;
+    constexpr int kW = kGroupThreads / kWave;
+    __shared__ int cnt[kW][APEX_MAX_EXPERTS];
+    __shared__ int wave_off[kW][APEX_MAX_EXPERTS];
+    __shared__ int start[APEX_MAX_EXPERTS + 1];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    for (int base = 0; base < P; base += kGroupThreads) {
+        // pairs [base, base + 1024) this round; P <= 1024 so there is one round
+        const int p = base + threadIdx.x;
+        int e = -1;
+        if (p < P) {
+            const int x = exec_idx[p];
+            if (x >= 0 && x < E) {
+                const int s = slot_of_expert[x];
+                if (s >= 0 && s < n_slots) e = x;
+            }
+        }
+        int local = 0;
+        for (int ex = 0; ex < E; ++ex) {
+            const unsigned long long m = __ballot(e == ex);
+            if (e == ex) local = __popcll(m & ((1ull << lane) - 1ull));
+            if (lane == 0) cnt[wave][ex] = __popcll(m);
+        }
+        __syncthreads();
+        if (threadIdx.x < E) {
+            int run = 0;
+            for (int w = 0; w < kW; ++w) {
+                wave_off[w][threadIdx.x] = run;
+                run += cnt[w][threadIdx.x];
+            }
+            cnt[0][threadIdx.x] = run;   // total per expert (cnt[0] already consumed)
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            int run = 0, n_act = 0;
+            for (int ex = 0; ex < E; ++ex) {
+                start[ex] = run;
+                if (cnt[0][ex] > 0) {
+                    G->act_e[n_act] = ex;
+                    G->act_start[n_act] = run;
+                    ++n_act;
+                }
+                run += cnt[0][ex];
+            }
+            start[E] = run;
+            G->act_start[n_act] = run;
+            G->n_act = n_act;
+            G->n_items = run;
+        }
+        __syncthreads();
+        if (e >= 0) G->item[start[e] + wave_off[wave][e] + local] = p;
+    }
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// K range of wavefront w when a workgroup's 4 wavefronts split K (multiples of 32).
+__device__ __forceinline__ void split_k(int K, int w, int &kb, int &ke) {
+    const int q = ((K + 127) / 128) * 32;
+    kb = w * q;
+    ke = kb + q < K ? kb + q : K;
+}
+
+// up_mfma: grid (ceil(I / 16), max active experts).  A workgroup owns 16 rows i of W1
+// and W3 of one expert; its 4 wavefronts split K = d four ways (so four times as many
+// loads are in flight), each taking U chunks of 32 per step with every load issued
+// before the first MFMA.  Partial accumulators meet in LDS; wavefront t finishes token
+// tile t.  hb[pair, i] = bf16(silu(W1[i] . x_b) * (W3[i] . x_b)), ungated.
+template <int MT, int U>
+__global__ __launch_bounds__(256) void up_mfma(
+    const __bf16 *__restrict__ xb, int d, int I, int k, const GroupTable *__restrict__ G,
+    const int32_t *__restrict__ slot_of_expert, const uint16_t *__restrict__ slots,
+    size_t slot_elems, __bf16 *__restrict__ hb) {
+    __shared__ floatx4 red[4][MT][2][kWave];
+    const int a = blockIdx.y;
+    if (a >= G->n_act) return;
+    const int i0 = blockIdx.x * 16;
+    if (i0 >= I) return;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int e = G->act_e[a];
+    const int beg = G->act_start[a], n_e = G->act_start[a + 1] - beg;
+    const uint16_t *W = slots + size_t(slot_of_expert[e]) * slot_elems;
+    const int col = lane % 16, kq = 8 * (lane / 16);
+    const int irow = (i0 + col < I) ? i0 + col : I - 1;
+    const uint16_t *w1row = W + size_t(irow) * 2 * d;
+    const uint16_t *w3row = w1row + d;
+    const uint4 zero = make_uint4(0, 0, 0, 0);
+    int kb, ke;
+    split_k(d, wave, kb, ke);
+
+    for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
+        const __bf16 *xrow[MT];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+            const int tok = t0 + 16 * t + col;
+            xrow[t] = tok < n_e ? xb + size_t(G->item[beg + tok] / k) * d : nullptr;
+        }
+        floatx4 accu[MT], accv[MT];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) accu[t] = accv[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int k0 = kb; k0 < ke; k0 += 32 * U) {
+            uint4 w1[U], w3[U], xv[U][MT];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int kk = k0 + 32 * u + kq;
+                const bool in = kk < ke;
+                w1[u] = in ? *reinterpret_cast<const uint4 *>(w1row + kk) : zero;
+                w3[u] = in ? *reinterpret_cast<const uint4 *>(w3row + kk) : zero;
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+                    xv[u][t] = (xrow[t] && in) ? *reinterpret_cast<const uint4 *>(xrow[t] + kk)
+                                               : zero;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int t = 0; t < MT; ++t) {
+                    if (t0 + 16 * t >= n_e) continue;
+                    accu[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        as_bf16x8(xv[u][t]), as_bf16x8(w1[u]), accu[t], 0, 0, 0);
+                    accv[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        as_bf16x8(xv[u][t]), as_bf16x8(w3[u]), accv[t], 0, 0, 0);
+                }
+        }
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+            red[wave][t][0][lane] = accu[t];
+            red[wave][t][1][lane] = accv[t];
+        }
+        __syncthreads();
+        if (wave < MT && t0 + 16 * wave < n_e) {
+            const int t = wave;
+            floatx4 u = red[0][t][0][lane], v = red[0][t][1][lane];
+#pragma unroll
+            for (int w = 1; w < 4; ++w) {
+                u += red[w][t][0][lane];
+                v += red[w][t][1][lane];
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int tok = t0 + 16 * t + 4 * (lane / 16) + r;
+                if (tok < n_e && i0 + col < I)
+                    hb[size_t(G->item[beg + tok]) * I + i0 + col] = (__bf16)(silu(u[r]) * v[r]);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// down_mfma: grid (ceil(d / 16), max active experts).  A workgroup owns 16 output rows
+// j of one expert; its 4 wavefronts split K = I four ways as in up_mfma.
+// ypair[pair, j] = W2[j] . h[pair] for every token of the expert.
+template <int MT, int U>
+__global__ __launch_bounds__(256) void down_mfma(
+    int d, int I, const GroupTable *__restrict__ G, const int32_t *__restrict__ slot_of_expert,
+    const uint16_t *__restrict__ slots, size_t slot_elems, const __bf16 *__restrict__ hb,
+    float *__restrict__ ypair) {
+    __shared__ floatx4 red[4][MT][kWave];
+    const int a = blockIdx.y;
+    if (a >= G->n_act) return;
+    const int j0 = blockIdx.x * 16;
+    if (j0 >= d) return;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int e = G->act_e[a];
+    const int beg = G->act_start[a], n_e = G->act_start[a + 1] - beg;
+    const uint16_t *W2 = slots + size_t(slot_of_expert[e]) * slot_elems + size_t(2) * I * d;
+    const int col = lane % 16, kq = 8 * (lane / 16);
+    const int jrow = (j0 + col < d) ? j0 + col : d - 1;
+    const uint16_t *wrow = W2 + size_t(jrow) * I;
+    const uint4 zero = make_uint4(0, 0, 0, 0);
+    int kb, ke;
+    split_k(I, wave, kb, ke);
+
+    for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
+        const __bf16 *hrow[MT];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+            const int tok = t0 + 16 * t + col;
+            hrow[t] = tok < n_e ? hb + size_t(G->item[beg + tok]) * I : nullptr;
+        }
+        floatx4 acc[MT];
+#pragma unroll
+        for (int t = 0; t < MT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int k0 = kb; k0 < ke; k0 += 32 * U) {
+            uint4 w[U], hv[U][MT];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int kk = k0 + 32 * u + kq;
+                const bool in = kk < ke;
+                w[u] = in ? *reinterpret_cast<const uint4 *>(wrow + kk) : zero;
+#pragma unroll
+                for (int t = 0; t < MT; ++t)
+                    hv[u][t] = (hrow[t] && in) ? *reinterpret_cast<const uint4 *>(hrow[t] + kk)
+                                               : zero;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int t = 0; t < MT; ++t) {
+                    if (t0 + 16 * t >= n_e) continue;
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        as_bf16x8(hv[u][t]), as_bf16x8(w[u]), acc[t], 0, 0, 0);
+                }
+        }
+#pragma unroll
+        for (int t = 0; t < MT; ++t) red[wave][t][lane] = acc[t];
+        __syncthreads();
+        if (wave < MT && t0 + 16 * wave < n_e) {
+            const int t = wave;
+            floatx4 s = red[0][t][lane];
+#pragma unroll
+            for (int w = 1; w < 4; ++w) s += red[w][t][lane];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int tok = t0 + 16 * t + 4 * (lane / 16) + r;
+                if (tok < n_e && j0 + col < d)
+                    ypair[size_t(G->item[beg + tok]) * d + j0 + col] = s[r];
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// combine: y[b, j] (+)= sum over positions p of token b, in position order, of
+// gate[p] * ypair[p, j] for the pairs this pass executed.
+__global__ __launch_bounds__(256) void combine_pairs(
+    int B, int d, int E, int k, const int32_t *__restrict__ exec_idx,
+    const float *__restrict__ exec_gate, const int32_t *__restrict__ slot_of_expert, int n_slots,
+    const float *__restrict__ ypair, float *__restrict__ y, int accumulate) {
+    const int b = blockIdx.y;
+    const int j = blockIdx.x * 256 + threadIdx.x;
+    if (b >= B || j >= d) return;
+    float s = 0.f;
+    for (int q = 0; q < k; ++q) {
+        const int p = b * k + q;
+        const int e = exec_idx[p];
+        if (e < 0 || e >= E) continue;
+        const int sl = slot_of_expert[e];
+        if (sl < 0 || sl >= n_slots) continue;
+        s += exec_gate[p] * ypair[size_t(p) * d + j];
+    }
+    float *dst = y + size_t(b) * d + j;
+    *dst = (accumulate ? *dst : 0.f) + s;
+}
+
+constexpr int kMfmaMinBatch = 16;
+
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
-extern "C" size_t apex_moe_ffn_workspace_bytes(int B, int k, int I) {
-    if (B <= 0 || k <= 0 || I <= 0) return 256;
-    return align_up(size_t(B) * k * I * sizeof(float), 256);
+// workspace: [GroupTable][h: B*k x I fp32 (bf16 on the batched path)]
+//            then, for B >= 16: [per-pair outputs: B*k x d fp32][bf16 activations: B x d]
+extern "C" size_t apex_moe_ffn_workspace_bytes(int B, int d, int I, int k) {
+    if (B <= 0 || k <= 0 || I <= 0 || d <= 0) return 256;
+    const size_t P = size_t(B) * k;
+    size_t n = align_up(sizeof(GroupTable), 256) + align_up(P * I * sizeof(float), 256);
+    if (B >= kMfmaMinBatch)
+        n += align_up(P * d * sizeof(float), 256) + align_up(size_t(B) * d * 2, 256);
+    return n;
 }
 
 extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
@@ -424,15 +716,41 @@ extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, 
     APEX_REQUIRE(apex::aligned16(x) && apex::aligned16(slots) && apex::aligned16(workspace) &&
                      apex::aligned16(y),
                  "%s: x, slots, y and workspace must be 16-byte aligned", fn);
-    const size_t need = apex_moe_ffn_workspace_bytes(B, k, I);
+    const size_t need = apex_moe_ffn_workspace_bytes(B, d, I, k);
     if (workspace_bytes < need)
         return apex::fail(APEX_E_CAPACITY, "%s: workspace %zu < %zu bytes", fn, workspace_bytes,
                           need);
     // y rows are read back when accumulating
     const int P = B * k;
     const size_t slot_elems = size_t(3) * d * I;
-    float *h = static_cast<float *>(workspace);
+    char *wsb = static_cast<char *>(workspace);
+    GroupTable *G = reinterpret_cast<GroupTable *>(wsb);
+    float *h = reinterpret_cast<float *>(wsb + align_up(sizeof(GroupTable), 256));
     const int max_act = P < E ? P : E;
+
+    if (B >= kMfmaMinBatch) {
+        char *after_h = wsb + align_up(sizeof(GroupTable), 256) +
+                        align_up(size_t(P) * I * sizeof(float), 256);
+        float *ypair = reinterpret_cast<float *>(after_h);
+        __bf16 *xb = reinterpret_cast<__bf16 *>(after_h + align_up(size_t(P) * d * sizeof(float), 256));
+        __bf16 *hb = reinterpret_cast<__bf16 *>(h);
+        const size_t n8 = size_t(B) * d / 8;
+        const unsigned conv_blocks = unsigned(std::min<size_t>(64, (n8 + kGroupThreads - 1) / kGroupThreads));
+        hipLaunchKernelGGL(group_pairs, dim3(conv_blocks), dim3(kGroupThreads), 0, stream,
+                           exec_idx, slot_of_expert, P, E, n_slots, G, x, B, d, xb);
+        APEX_HIP(hipGetLastError());
+        const dim3 gu((I + 15) / 16, max_act), gd((d + 15) / 16, max_act);
+        hipLaunchKernelGGL((up_mfma<2, 4>), gu, dim3(256), 0, stream, xb, d, I, k, G,
+                           slot_of_expert, slots, slot_elems, hb);
+        APEX_HIP(hipGetLastError());
+        hipLaunchKernelGGL((down_mfma<2, 4>), gd, dim3(256), 0, stream, d, I, G, slot_of_expert,
+                           slots, slot_elems, hb, ypair);
+        APEX_HIP(hipGetLastError());
+        hipLaunchKernelGGL(combine_pairs, dim3((d + 255) / 256, B), dim3(256), 0, stream, B, d, E,
+                           k, exec_idx, exec_gate, slot_of_expert, n_slots, ypair, y, accumulate);
+        APEX_HIP(hipGetLastError());
+        return APEX_OK;
+    }
 
     if (B == 1) {
         // h holds gated rows per position; tile shapes measured on MI355X (streaming rate

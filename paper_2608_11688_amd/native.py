@@ -74,7 +74,7 @@ SIGNATURES = {
     "apex_gate_topk": (I32, [P, P, P, I32, I32, I32, I32, I32, P, I32, P, P, P, P, P, P]),
     "apex_expert_bytes": (SZ, [I32, I32]),
     "apex_pack_expert": (I32, [P, P, P, I32, I32, P]),
-    "apex_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32]),
+    "apex_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32, I32]),
     "apex_moe_ffn": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_plan_residency": (I32, [I32, I32, P, P, I32, I32, I64, P, P, P, P, P]),
     "apex_expert_prefetch": (I32, [P, P, I32, I32, SZ, P, P, I32, I32, I64, P, P, P, P, P, P, P,
@@ -188,8 +188,8 @@ def apex_pack_expert(w1, w3, w2, d, I, out, L=None):
     _call("apex_pack_expert", ptr(w1), ptr(w3), ptr(w2), d, I, ptr(out), L=L)
 
 
-def apex_moe_ffn_workspace_bytes(B, k, I):
-    return lib().apex_moe_ffn_workspace_bytes(B, k, I)
+def apex_moe_ffn_workspace_bytes(B, d, I, k):
+    return lib().apex_moe_ffn_workspace_bytes(B, d, I, k)
 
 
 def apex_moe_ffn(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots, y,

@@ -71,7 +71,7 @@ class DecodeRunner:
         self.exec_idx = torch.empty((B, k), **i32)
         self.exec_gate = torch.empty((B, k), dtype=torch.float32, device=self.dev)
         self.y = torch.zeros((L, B, cfg.d), dtype=torch.float32, device=self.dev)
-        self.ws_bytes = native.apex_moe_ffn_workspace_bytes(B, k, cfg.I)
+        self.ws_bytes = native.apex_moe_ffn_workspace_bytes(B, cfg.d, cfg.I, k)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
         self.scratch = torch.empty(max(1, self.n_scratch) * self.S // 2, dtype=torch.int16,
                                    device=self.dev)

@@ -231,7 +231,7 @@ class FfnCase:
     def run(self, table=None, y0=None, accumulate=0):
         torch, cfg, B = self.torch, self.cfg, self.B
         table = self.table if table is None else table
-        ws_bytes = native.apex_moe_ffn_workspace_bytes(B, cfg.k, cfg.I)
+        ws_bytes = native.apex_moe_ffn_workspace_bytes(B, cfg.d, cfg.I, cfg.k)
         ws = torch.full((ws_bytes,), 0xAB, dtype=torch.uint8, device="cuda")
         y = dev(torch, y0) if y0 is not None else torch.full((B, cfg.d), float("nan"),
                                                               device="cuda")
@@ -273,6 +273,51 @@ def test_ffn_parity_workload_shapes(torch, name, B):
     case = FfnCase(torch, cfg, B, seed=cfg.cfg_id * 10 + B)
     y = case.run()
     print(name, B, ffn_close(y, case.oracle(), f"{name} B{B}"))
+
+
+MFMA_SHAPES = [
+    # batched path (>= 16 tokens): matrix-core grouped GEMMs
+    (shape("mfma_ragged", 410, 264, 12, 3, I=200), 40),   # d % 32 != 0, I % 16 != 0
+    (shape("mfma_b48", 411, 512, 6, 2, I=256), 48),       # four token tiles per pass
+    (shape("mfma_b16", 412, 1024, 32, 8, I=512), 16),     # smallest batch on this path
+]
+
+
+@pytest.mark.parametrize("cfg,B", MFMA_SHAPES, ids=[c.name for c, _ in MFMA_SHAPES])
+def test_ffn_mfma_parity(torch, cfg, B):
+    case = FfnCase(torch, cfg, B, seed=cfg.cfg_id)
+    y = case.run()
+    print(cfg.name, B, ffn_close(y, case.oracle(), cfg.name))
+
+
+def test_ffn_mfma_skewed_expert_takes_every_token(torch):
+    # expert 0 is in every token's set: 128 tokens on one expert = several passes of
+    # four 16-token tiles; the others are spread out
+    cfg = shape("mfma_skew", 413, 256, 16, 8, I=128)
+    case = FfnCase(torch, cfg, 128, seed=5)
+    rng = np.random.default_rng(6)
+    for b in range(128):
+        others = rng.choice(np.arange(1, 16), cfg.k - 1, replace=False)
+        case.exec_idx[b] = np.concatenate([[0], others]).astype(np.int32)
+    assert all(case.table[e] >= 0 for e in range(16))   # 128 random tokens used all 16
+    y = case.run()
+    print("skew", ffn_close(y, case.oracle(), "skewed"))
+
+
+def test_ffn_mfma_two_passes_equal_one(torch):
+    cfg = shape("mfma_pass", 414, 392, 12, 4, I=200)
+    case = FfnCase(torch, cfg, 24, seed=17, n_slots_extra=2)
+    full = case.oracle()
+    res = case.resident
+    first, second = res[: len(res) // 2], res[len(res) // 2:]
+    t1 = case.table.copy()
+    t1[second] = -1
+    t2 = case.table.copy()
+    t2[first] = -1
+    y1 = case.run(t1)
+    ffn_close(y1, case.oracle(only=first), "mfma pass 1")
+    y2 = case.run(t2, y0=y1, accumulate=1)
+    ffn_close(y2, full, "mfma pass 1 + pass 2")
 
 
 def test_ffn_parity_mixtral_batch1(torch):

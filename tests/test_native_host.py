@@ -153,5 +153,7 @@ def test_entry_points_validate_before_enqueue(hip_lib):
 
 
 def test_workspace_size():
-    assert native.apex_moe_ffn_workspace_bytes(1, 8, 512) == 8 * 512 * 4
-    assert native.apex_moe_ffn_workspace_bytes(3, 2, 24) % 256 == 0
+    small = native.apex_moe_ffn_workspace_bytes(1, 1024, 512, 8)
+    assert small >= 8 * 512 * 4 and small % 256 == 0
+    big = native.apex_moe_ffn_workspace_bytes(64, 2048, 1024, 8)   # batched path: + outputs
+    assert big >= 512 * (1024 + 2048) * 4 and big % 256 == 0
