@@ -1,16 +1,21 @@
 // Gated SwiGLU experts over HBM cache slots (apex_moe_ffn).
 //
-// Two launches per call, both HBM-bound streams of bf16 weights:
-//   ffn_gate_up  grid (I tiles, active experts): each wavefront owns RW rows i of one
-//                expert and computes h[p, i] = silu(W1[i] . x_b) * (W3[i] . x_b) for every
-//                token b routed to that expert (pair p), reading each weight once;
-//   ffn_down     grid (d tiles): each wavefront owns RD output rows j and accumulates
-//                g_p * (W2_e[j] . h[p]) over the (expert, token) pairs in (expert, token)
-//                order into LDS, then writes y once - no atomics, deterministic.
-// Weights are read with 16-byte loads; lanes of a wavefront cover consecutive 16-byte
-// chunks of a row, so every wavefront load is a contiguous 1 KB burst.
-// Every workgroup derives the expert grouping of the batch itself (at most B*k <= 1024
-// pairs, a few hundred LDS operations) instead of paying a separate launch.
+// Every path streams each executed expert's bf16 weights from HBM once per call and
+// needs no atomics, so results are deterministic. Three paths, chosen by batch size:
+//
+// Batch 1 (up_b1, down_b1): one token, k experts. up_b1 reads W1/W3 rows of an expert
+//   with all row loads issued before any arithmetic and writes h[j, i]; down_b1 owns one
+//   output row of y and sums g_j * (W2_j[row] . h[j]) over the k experts in one
+//   flattened dot, so the k experts share a single launch.
+// Batch 2..15 (ffn_gate_up, ffn_down): each workgroup derives the (expert, token)
+//   grouping of the batch itself (at most B*k <= 1024 pairs) and reads each weight row
+//   once for every token routed to that expert.
+// Batch >= 16 (group_pairs, up_gemm, down_gemm, combine_pairs): a grouped GEMM on the
+//   matrix cores. group_pairs converts x to bf16 and builds one table of the pairs
+//   sorted by expert; up_gemm and down_gemm stage 64-row weight tiles and 16*MT token
+//   rows through LDS and issue v_mfma_f32_16x16x32_bf16 on them; combine_pairs sums
+//   the gated per-pair outputs of every token in pair order.
+// Weights are read with 16-byte loads that cover consecutive 16-byte chunks of a row.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -488,170 +493,184 @@ __global__ __launch_bounds__(kGroupThreads) void group_pairs(
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// K range of wavefront w when a workgroup's 4 wavefronts split K (multiples of 32).
-__device__ __forceinline__ void split_k(int K, int w, int &kb, int &ke) {
-    const int q = ((K + 127) / 128) * 32;
-    kb = w * q;
-    ke = kb + q < K ? kb + q : K;
+// Grouped-GEMM mainloop shared by the gate/up and down projections.
+// A workgroup (4 wavefronts) owns a tile of 64 weight rows of NW weight matrices and up
+// to 16*MT tokens.  K advances in blocks of 128: every thread loads 16-byte pieces so
+// that each group of 16 threads reads 256 contiguous bytes of one weight row (whole
+// cache lines), the block goes to LDS, and while the matrix cores work on it the next
+// block is already loading into registers.  Wavefront w multiplies its 16 rows with
+// every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.
+constexpr int kKB = 128;
+constexpr int kLdsRow = kKB + 8;   // +16 B per row: the 16 rows of a fragment read hit distinct banks
+
+// One K block of the tile into registers.  Every address is valid (rows and K are
+// clamped); pieces outside the tile are zeroed after the load instead of branching,
+// so all 4*NW + MT loads issue back to back.
+// Component-wise select: a select of the whole vector struct is lowered through
+// private memory by the compiler.
+__device__ __forceinline__ uint4 keep_if(uint4 v, bool c) {
+    return make_uint4(c ? v.x : 0u, c ? v.y : 0u, c ? v.z : 0u, c ? v.w : 0u);
 }
 
-// up_mfma: grid (ceil(I / 16), max active experts).  A workgroup owns 16 rows i of W1
-// and W3 of one expert; its 4 wavefronts split K = d four ways (so four times as many
-// loads are in flight), each taking U chunks of 32 per step with every load issued
-// before the first MFMA.  Partial accumulators meet in LDS; wavefront t finishes token
-// tile t.  hb[pair, i] = bf16(silu(W1[i] . x_b) * (W3[i] . x_b)), ungated.
-template <int MT, int U>
-__global__ __launch_bounds__(256) void up_mfma(
+template <int NW, int MT>
+__device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][4], uint4 (&xreg)[MT],
+                                          const uint16_t *const (&wbase)[NW], size_t wstride,
+                                          int rows_valid, int K, const uint16_t *const (&xrow)[MT],
+                                          const bool (&xok)[MT], int k0, int r0, int seg) {
+    const int kk = k0 + 8 * seg;
+    const bool in = kk < K;
+    const int kc = in ? kk : K - 8;
+#pragma unroll
+    for (int m = 0; m < NW; ++m)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int row = r0 + 16 * j;
+            const int rc = row < rows_valid ? row : rows_valid - 1;
+            const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + kc);
+            wreg[m][j] = keep_if(v, in && row < rows_valid);
+        }
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(xrow[j] + kc);
+        xreg[j] = keep_if(v, in && xok[j]);
+    }
+}
+
+template <int NW, int MT>
+__device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW], size_t wstride,
+                                              int rows_valid, int K,
+                                              const uint16_t *const (&xrow)[MT],
+                                              const bool (&xok)[MT], int n_tiles,
+                                              uint16_t (*Ws)[64][kLdsRow],
+                                              uint16_t (*Xs)[kLdsRow], floatx4 (&acc)[NW][MT]) {
+    const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
+    const int seg = t & 15, r0 = t >> 4;
+    uint4 wreg[NW][4], xreg[MT];
+#pragma unroll
+    for (int m = 0; m < NW; ++m)
+#pragma unroll
+        for (int tt = 0; tt < MT; ++tt) acc[m][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int nb = (K + kKB - 1) / kKB;
+    gemm_load<NW, MT>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, 0, r0, seg);
+    for (int b = 0; b < nb; ++b) {
+        __syncthreads();   // the previous block's fragments have been read
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                *reinterpret_cast<uint4 *>(&Ws[m][r0 + 16 * j][8 * seg]) = wreg[m][j];
+#pragma unroll
+        for (int j = 0; j < MT; ++j) *reinterpret_cast<uint4 *>(&Xs[r0 + 16 * j][8 * seg]) = xreg[j];
+        __syncthreads();
+        if (b + 1 < nb)
+            gemm_load<NW, MT>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok,
+                              (b + 1) * kKB, r0, seg);
+#pragma unroll
+        for (int q = 0; q < kKB / 32; ++q) {
+            const int kc = 32 * q + 8 * (lane >> 4);
+            uint4 wop[NW];
+#pragma unroll
+            for (int m = 0; m < NW; ++m)
+                wop[m] = *reinterpret_cast<const uint4 *>(&Ws[m][16 * wave + (lane & 15)][kc]);
+#pragma unroll
+            for (int tt = 0; tt < MT; ++tt) {
+                if (tt >= n_tiles) continue;
+                const uint4 xop = *reinterpret_cast<const uint4 *>(&Xs[16 * tt + (lane & 15)][kc]);
+#pragma unroll
+                for (int m = 0; m < NW; ++m)
+                    acc[m][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        as_bf16x8(xop), as_bf16x8(wop[m]), acc[m][tt], 0, 0, 0);
+            }
+        }
+    }
+}
+
+// up_gemm: grid (ceil(I / 64), max active experts): 64 rows of W1 and W3 of one expert,
+// every token of the expert (16*MT per pass).
+// hb[pair, i] = bf16(silu(W1[i] . x_b) * (W3[i] . x_b)), ungated.
+template <int MT>
+__global__ __launch_bounds__(256) void up_gemm(
     const __bf16 *__restrict__ xb, int d, int I, int k, const GroupTable *__restrict__ G,
     const int32_t *__restrict__ slot_of_expert, const uint16_t *__restrict__ slots,
     size_t slot_elems, __bf16 *__restrict__ hb) {
-    __shared__ floatx4 red[4][MT][2][kWave];
+    __shared__ uint16_t Ws[2][64][kLdsRow];
+    __shared__ uint16_t Xs[16 * MT][kLdsRow];
     const int a = blockIdx.y;
     if (a >= G->n_act) return;
-    const int i0 = blockIdx.x * 16;
+    const int i0 = blockIdx.x * 64;
     if (i0 >= I) return;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int e = G->act_e[a];
     const int beg = G->act_start[a], n_e = G->act_start[a + 1] - beg;
-    const uint16_t *W = slots + size_t(slot_of_expert[e]) * slot_elems;
-    const int col = lane % 16, kq = 8 * (lane / 16);
-    const int irow = (i0 + col < I) ? i0 + col : I - 1;
-    const uint16_t *w1row = W + size_t(irow) * 2 * d;
-    const uint16_t *w3row = w1row + d;
-    const uint4 zero = make_uint4(0, 0, 0, 0);
-    int kb, ke;
-    split_k(d, wave, kb, ke);
-
+    const uint16_t *W = slots + size_t(slot_of_expert[e]) * slot_elems + size_t(i0) * 2 * d;
+    const uint16_t *const wbase[2] = {W, W + d};
+    const uint16_t *xs = reinterpret_cast<const uint16_t *>(xb);
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
-        const __bf16 *xrow[MT];
+        const uint16_t *xrow[MT];
+        bool xok[MT];
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
-            const int tok = t0 + 16 * t + col;
-            xrow[t] = tok < n_e ? xb + size_t(G->item[beg + tok] / k) * d : nullptr;
+        for (int j = 0; j < MT; ++j) {
+            const int tok = t0 + (threadIdx.x >> 4) + 16 * j;
+            xok[j] = tok < n_e;
+            xrow[j] = xs + size_t(G->item[beg + (xok[j] ? tok : 0)] / k) * d;
         }
-        floatx4 accu[MT], accv[MT];
+        const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
+        floatx4 acc[2][MT];
+        gemm_mainloop<2, MT>(wbase, size_t(2) * d, I - i0, d, xrow, xok, n_tiles, Ws, Xs, acc);
+        const int i = i0 + 16 * wave + (lane & 15);
 #pragma unroll
-        for (int t = 0; t < MT; ++t) accu[t] = accv[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-        for (int k0 = kb; k0 < ke; k0 += 32 * U) {
-            uint4 w1[U], w3[U], xv[U][MT];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int kk = k0 + 32 * u + kq;
-                const bool in = kk < ke;
-                w1[u] = in ? *reinterpret_cast<const uint4 *>(w1row + kk) : zero;
-                w3[u] = in ? *reinterpret_cast<const uint4 *>(w3row + kk) : zero;
-#pragma unroll
-                for (int t = 0; t < MT; ++t)
-                    xv[u][t] = (xrow[t] && in) ? *reinterpret_cast<const uint4 *>(xrow[t] + kk)
-                                               : zero;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int t = 0; t < MT; ++t) {
-                    if (t0 + 16 * t >= n_e) continue;
-                    accu[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        as_bf16x8(xv[u][t]), as_bf16x8(w1[u]), accu[t], 0, 0, 0);
-                    accv[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        as_bf16x8(xv[u][t]), as_bf16x8(w3[u]), accv[t], 0, 0, 0);
-                }
-        }
-#pragma unroll
-        for (int t = 0; t < MT; ++t) {
-            red[wave][t][0][lane] = accu[t];
-            red[wave][t][1][lane] = accv[t];
-        }
-        __syncthreads();
-        if (wave < MT && t0 + 16 * wave < n_e) {
-            const int t = wave;
-            floatx4 u = red[0][t][0][lane], v = red[0][t][1][lane];
-#pragma unroll
-            for (int w = 1; w < 4; ++w) {
-                u += red[w][t][0][lane];
-                v += red[w][t][1][lane];
-            }
+        for (int tt = 0; tt < MT; ++tt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int tok = t0 + 16 * t + 4 * (lane / 16) + r;
-                if (tok < n_e && i0 + col < I)
-                    hb[size_t(G->item[beg + tok]) * I + i0 + col] = (__bf16)(silu(u[r]) * v[r]);
+                const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
+                if (tt < n_tiles && tok < n_e && i < I)
+                    hb[size_t(G->item[beg + tok]) * I + i] =
+                        (__bf16)(silu(acc[0][tt][r]) * acc[1][tt][r]);
             }
-        }
-        __syncthreads();
     }
 }
 
-// down_mfma: grid (ceil(d / 16), max active experts).  A workgroup owns 16 output rows
-// j of one expert; its 4 wavefronts split K = I four ways as in up_mfma.
+// down_gemm: grid (ceil(d / 64), max active experts): 64 rows j of W2 of one expert.
 // ypair[pair, j] = W2[j] . h[pair] for every token of the expert.
-template <int MT, int U>
-__global__ __launch_bounds__(256) void down_mfma(
+template <int MT>
+__global__ __launch_bounds__(256) void down_gemm(
     int d, int I, const GroupTable *__restrict__ G, const int32_t *__restrict__ slot_of_expert,
     const uint16_t *__restrict__ slots, size_t slot_elems, const __bf16 *__restrict__ hb,
     float *__restrict__ ypair) {
-    __shared__ floatx4 red[4][MT][kWave];
+    __shared__ uint16_t Ws[1][64][kLdsRow];
+    __shared__ uint16_t Xs[16 * MT][kLdsRow];
     const int a = blockIdx.y;
     if (a >= G->n_act) return;
-    const int j0 = blockIdx.x * 16;
+    const int j0 = blockIdx.x * 64;
     if (j0 >= d) return;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int e = G->act_e[a];
     const int beg = G->act_start[a], n_e = G->act_start[a + 1] - beg;
-    const uint16_t *W2 = slots + size_t(slot_of_expert[e]) * slot_elems + size_t(2) * I * d;
-    const int col = lane % 16, kq = 8 * (lane / 16);
-    const int jrow = (j0 + col < d) ? j0 + col : d - 1;
-    const uint16_t *wrow = W2 + size_t(jrow) * I;
-    const uint4 zero = make_uint4(0, 0, 0, 0);
-    int kb, ke;
-    split_k(I, wave, kb, ke);
-
+    const uint16_t *const wbase[1] = {slots + size_t(slot_of_expert[e]) * slot_elems +
+                                      size_t(2) * I * d + size_t(j0) * I};
+    const uint16_t *hs = reinterpret_cast<const uint16_t *>(hb);
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
-        const __bf16 *hrow[MT];
+        const uint16_t *hrow[MT];
+        bool hok[MT];
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
-            const int tok = t0 + 16 * t + col;
-            hrow[t] = tok < n_e ? hb + size_t(G->item[beg + tok]) * I : nullptr;
+        for (int j = 0; j < MT; ++j) {
+            const int tok = t0 + (threadIdx.x >> 4) + 16 * j;
+            hok[j] = tok < n_e;
+            hrow[j] = hs + size_t(G->item[beg + (hok[j] ? tok : 0)]) * I;
         }
-        floatx4 acc[MT];
+        const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
+        floatx4 acc[1][MT];
+        gemm_mainloop<1, MT>(wbase, size_t(I), d - j0, I, hrow, hok, n_tiles, Ws, Xs, acc);
+        const int j = j0 + 16 * wave + (lane & 15);
 #pragma unroll
-        for (int t = 0; t < MT; ++t) acc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
-        for (int k0 = kb; k0 < ke; k0 += 32 * U) {
-            uint4 w[U], hv[U][MT];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int kk = k0 + 32 * u + kq;
-                const bool in = kk < ke;
-                w[u] = in ? *reinterpret_cast<const uint4 *>(wrow + kk) : zero;
-#pragma unroll
-                for (int t = 0; t < MT; ++t)
-                    hv[u][t] = (hrow[t] && in) ? *reinterpret_cast<const uint4 *>(hrow[t] + kk)
-                                               : zero;
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u)
-#pragma unroll
-                for (int t = 0; t < MT; ++t) {
-                    if (t0 + 16 * t >= n_e) continue;
-                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        as_bf16x8(hv[u][t]), as_bf16x8(w[u]), acc[t], 0, 0, 0);
-                }
-        }
-#pragma unroll
-        for (int t = 0; t < MT; ++t) red[wave][t][lane] = acc[t];
-        __syncthreads();
-        if (wave < MT && t0 + 16 * wave < n_e) {
-            const int t = wave;
-            floatx4 s = red[0][t][lane];
-#pragma unroll
-            for (int w = 1; w < 4; ++w) s += red[w][t][lane];
+        for (int tt = 0; tt < MT; ++tt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int tok = t0 + 16 * t + 4 * (lane / 16) + r;
-                if (tok < n_e && j0 + col < d)
-                    ypair[size_t(G->item[beg + tok]) * d + j0 + col] = s[r];
+                const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
+                if (tt < n_tiles && tok < n_e && j < d)
+                    ypair[size_t(G->item[beg + tok]) * d + j] = acc[0][tt][r];
             }
-        }
-        __syncthreads();
+        __syncthreads();   // LDS is reused by the next pass
     }
 }
 
@@ -739,12 +758,27 @@ extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, 
         hipLaunchKernelGGL(group_pairs, dim3(conv_blocks), dim3(kGroupThreads), 0, stream,
                            exec_idx, slot_of_expert, P, E, n_slots, G, x, B, d, xb);
         APEX_HIP(hipGetLastError());
-        const dim3 gu((I + 15) / 16, max_act), gd((d + 15) / 16, max_act);
-        hipLaunchKernelGGL((up_mfma<2, 4>), gu, dim3(256), 0, stream, xb, d, I, k, G,
-                           slot_of_expert, slots, slot_elems, hb);
-        APEX_HIP(hipGetLastError());
-        hipLaunchKernelGGL((down_mfma<2, 4>), gd, dim3(256), 0, stream, d, I, G, slot_of_expert,
-                           slots, slot_elems, hb, ypair);
+        const dim3 gu((I + 63) / 64, max_act), gd((d + 63) / 64, max_act);
+        // token tiles per pass: enough for the whole batch on one expert up to 64 tokens
+        if (B >= 48) {
+            hipLaunchKernelGGL((up_gemm<4>), gu, dim3(256), 0, stream, xb, d, I, k, G,
+                               slot_of_expert, slots, slot_elems, hb);
+            APEX_HIP(hipGetLastError());
+            hipLaunchKernelGGL((down_gemm<4>), gd, dim3(256), 0, stream, d, I, G,
+                               slot_of_expert, slots, slot_elems, hb, ypair);
+        } else if (B >= 24) {
+            hipLaunchKernelGGL((up_gemm<2>), gu, dim3(256), 0, stream, xb, d, I, k, G,
+                               slot_of_expert, slots, slot_elems, hb);
+            APEX_HIP(hipGetLastError());
+            hipLaunchKernelGGL((down_gemm<2>), gd, dim3(256), 0, stream, d, I, G,
+                               slot_of_expert, slots, slot_elems, hb, ypair);
+        } else {
+            hipLaunchKernelGGL((up_gemm<1>), gu, dim3(256), 0, stream, xb, d, I, k, G,
+                               slot_of_expert, slots, slot_elems, hb);
+            APEX_HIP(hipGetLastError());
+            hipLaunchKernelGGL((down_gemm<1>), gd, dim3(256), 0, stream, d, I, G,
+                               slot_of_expert, slots, slot_elems, hb, ypair);
+        }
         APEX_HIP(hipGetLastError());
         hipLaunchKernelGGL(combine_pairs, dim3((d + 255) / 256, B), dim3(256), 0, stream, B, d, E,
                            k, exec_idx, exec_gate, slot_of_expert, n_slots, ypair, y, accumulate);
