@@ -1,16 +1,13 @@
 // Gated SwiGLU experts over HBM cache slots (apex_moe_ffn).
 //
-// Every path streams each executed expert's bf16 weights from HBM once per call and
-// needs no atomics, so results are deterministic. Three paths, chosen by batch size:
+// Both paths stream each executed expert's bf16 weights from HBM once per call and
+// need no atomics, so results are deterministic:
 //
 // Batch 1 (up_b1, down_b1): one token, k experts. up_b1 reads W1/W3 rows of an expert
 //   with all row loads issued before any arithmetic and writes h[j, i]; down_b1 owns one
 //   output row of y and sums g_j * (W2_j[row] . h[j]) over the k experts in one
 //   flattened dot, so the k experts share a single launch.
-// Batch 2..15 (ffn_gate_up, ffn_down): each workgroup derives the (expert, token)
-//   grouping of the batch itself (at most B*k <= 1024 pairs) and reads each weight row
-//   once for every token routed to that expert.
-// Batch >= 16 (group_pairs, up_gemm, down_gemm, combine_pairs): a grouped GEMM on the
+// Batch >= 2 (group_pairs, up_gemm, down_gemm, combine_pairs): a grouped GEMM on the
 //   matrix cores. group_pairs converts x to bf16 and builds one table of the pairs
 //   sorted by expert; up_gemm and down_gemm stage 64-row weight tiles and 16*MT token
 //   rows through LDS and issue v_mfma_f32_16x16x32_bf16 on them; combine_pairs sums
@@ -26,9 +23,6 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kThreads = 256;
-constexpr int kWavesPerGroup = kThreads / kWave;
-constexpr int kInvalidKey = 0x7fffffff;
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -52,203 +46,6 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 __device__ __forceinline__ float silu(float u) { return u / (1.f + expf(-u)); }
-
-// Pairs p = b*k + j of the batch whose expert has a slot in this pass, sorted by
-// (expert, p), and the active experts in ascending id order with their ranges.
-struct Groups {
-    int n_items;
-    int n_act;
-    unsigned int mask[2];
-    int act_e[APEX_MAX_EXPERTS];
-    int act_start[APEX_MAX_EXPERTS + 1];
-    int key[APEX_MAX_PAIRS];
-    int item[APEX_MAX_PAIRS];
-};
-
-__device__ void build_groups(Groups &G, const int32_t *__restrict__ exec_idx,
-                             const int32_t *__restrict__ slot_of_expert, int P, int E,
-                             int n_slots) {
-    const int tid = threadIdx.x;
-    if (tid == 0) {
-        G.n_items = 0;
-        G.mask[0] = G.mask[1] = 0u;
-    }
-    __syncthreads();
-    for (int p = tid; p < P; p += kThreads) {
-        const int e = exec_idx[p];
-        bool ok = e >= 0 && e < E;
-        if (ok) {
-            const int s = slot_of_expert[e];
-            ok = s >= 0 && s < n_slots;
-        }
-        G.key[p] = ok ? ((e << 16) | p) : kInvalidKey;
-        if (ok) {
-            atomicAdd(&G.n_items, 1);
-            atomicOr(&G.mask[e >> 5], 1u << (e & 31));
-        }
-    }
-    __syncthreads();
-    for (int p = tid; p < P; p += kThreads) {
-        const int kp = G.key[p];
-        if (kp == kInvalidKey) continue;
-        int pos = 0;
-        for (int q = 0; q < P; ++q) pos += G.key[q] < kp ? 1 : 0;
-        G.item[pos] = p;
-    }
-    if (tid < APEX_MAX_EXPERTS) {
-        const int e = tid;
-        const unsigned long long m =
-            (static_cast<unsigned long long>(G.mask[1]) << 32) | G.mask[0];
-        if ((m >> e) & 1ull) {
-            const int a = __popcll(m & ((1ull << e) - 1ull));
-            int start = 0;
-            for (int q = 0; q < P; ++q) start += G.key[q] < (e << 16) ? 1 : 0;
-            G.act_e[a] = e;
-            G.act_start[a] = start;
-        }
-        if (tid == 0) {
-            G.n_act = __popcll(m);
-            G.act_start[G.n_act] = G.n_items;
-        }
-    }
-    __syncthreads();
-}
-
-template <int RW, int NT>
-__global__ __launch_bounds__(kThreads) void ffn_gate_up(
-    const float *__restrict__ x, int d, int I, int E, int k, int P,
-    const int32_t *__restrict__ exec_idx, const int32_t *__restrict__ slot_of_expert,
-    const uint16_t *__restrict__ slots, int n_slots, size_t slot_elems, float *__restrict__ h) {
-    __shared__ Groups G;
-    build_groups(G, exec_idx, slot_of_expert, P, E, n_slots);
-    const int a = blockIdx.y;
-    if (a >= G.n_act) return;
-    const int e = G.act_e[a];
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int i0 = (blockIdx.x * kWavesPerGroup + wave) * RW;
-    if (i0 >= I) return;
-    const uint16_t *Wrows = slots + size_t(slot_of_expert[e]) * slot_elems;
-    const int beg = G.act_start[a], end = G.act_start[a + 1];
-    const int nch = d / 8;
-    const size_t row_stride = size_t(2) * d;
-
-    for (int t0 = beg; t0 < end; t0 += NT) {
-        int pair[NT];
-        const float4 *xr[NT];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            pair[t] = (t0 + t < end) ? G.item[t0 + t] : -1;
-            const int bb = pair[t] >= 0 ? pair[t] / k : 0;
-            xr[t] = reinterpret_cast<const float4 *>(x + size_t(bb) * d);
-        }
-        float u[RW][NT], v[RW][NT];
-#pragma unroll
-        for (int r = 0; r < RW; ++r)
-#pragma unroll
-            for (int t = 0; t < NT; ++t) u[r][t] = v[r][t] = 0.f;
-
-        for (int c = lane; c < nch; c += kWave) {
-            uint4 w1[RW], w3[RW];
-#pragma unroll
-            for (int r = 0; r < RW; ++r) {
-                const int i = (i0 + r < I) ? i0 + r : I - 1;
-                const uint4 *row = reinterpret_cast<const uint4 *>(Wrows + size_t(i) * row_stride);
-                w1[r] = row[c];
-                w3[r] = row[nch + c];
-            }
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                if (pair[t] < 0) continue;
-                const float4 xa = xr[t][2 * c], xb = xr[t][2 * c + 1];
-#pragma unroll
-                for (int r = 0; r < RW; ++r) {
-                    u[r][t] = dot8(w1[r], xa, xb, u[r][t]);
-                    v[r][t] = dot8(w3[r], xa, xb, v[r][t]);
-                }
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < RW; ++r)
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const float su = wave_sum(u[r][t]);
-                const float sv = wave_sum(v[r][t]);
-                if (lane == 0 && pair[t] >= 0 && i0 + r < I)
-                    h[size_t(pair[t]) * I + i0 + r] = silu(su) * sv;
-            }
-    }
-}
-
-template <int RD, int UI>
-__global__ __launch_bounds__(kThreads) void ffn_down(
-    int B, int d, int I, int E, int k, int P, const int32_t *__restrict__ exec_idx,
-    const float *__restrict__ exec_gate, const int32_t *__restrict__ slot_of_expert,
-    const uint16_t *__restrict__ slots, int n_slots, size_t slot_elems,
-    const float *__restrict__ h, float *__restrict__ y, int accumulate) {
-    __shared__ Groups G;
-    extern __shared__ float yacc[];   // [B][kWavesPerGroup * RD]
-    constexpr int kRows = kWavesPerGroup * RD;
-    build_groups(G, exec_idx, slot_of_expert, P, E, n_slots);
-    for (int i = threadIdx.x; i < B * kRows; i += kThreads) yacc[i] = 0.f;
-    __syncthreads();
-
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int j0 = blockIdx.x * kRows + wave * RD;
-    const int nch = I / 8;
-    const size_t w2_off = size_t(2) * I * d;
-    if (j0 < d) {
-        for (int it0 = 0; it0 < G.n_items; it0 += UI) {
-            int pair[UI];
-            const uint4 *wrow[UI];
-            const float4 *hr[UI];
-#pragma unroll
-            for (int u = 0; u < UI; ++u) {
-                pair[u] = (it0 + u < G.n_items) ? G.item[it0 + u] : -1;
-                const int p = pair[u] >= 0 ? pair[u] : G.item[it0];
-                const int e = exec_idx[p];
-                wrow[u] = reinterpret_cast<const uint4 *>(
-                    slots + size_t(slot_of_expert[e]) * slot_elems + w2_off);
-                hr[u] = reinterpret_cast<const float4 *>(h + size_t(p) * I);
-            }
-            float acc[UI][RD];
-#pragma unroll
-            for (int u = 0; u < UI; ++u)
-#pragma unroll
-                for (int r = 0; r < RD; ++r) acc[u][r] = 0.f;
-            for (int c = lane; c < nch; c += kWave) {
-#pragma unroll
-                for (int u = 0; u < UI; ++u) {
-                    if (pair[u] < 0) continue;
-                    const float4 ha = hr[u][2 * c], hb = hr[u][2 * c + 1];
-#pragma unroll
-                    for (int r = 0; r < RD; ++r) {
-                        const int j = (j0 + r < d) ? j0 + r : d - 1;
-                        acc[u][r] = dot8(wrow[u][size_t(j) * nch + c], ha, hb, acc[u][r]);
-                    }
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < UI; ++u)
-#pragma unroll
-                for (int r = 0; r < RD; ++r) {
-                    const float s = wave_sum(acc[u][r]);
-                    if (lane == 0 && pair[u] >= 0 && j0 + r < d) {
-                        const int bb = pair[u] / k;
-                        yacc[bb * kRows + wave * RD + r] += exec_gate[pair[u]] * s;
-                    }
-                }
-        }
-    }
-    __syncthreads();
-    for (int i = threadIdx.x; i < B * kRows; i += kThreads) {
-        const int bb = i / kRows, rr = i % kRows;
-        const int j = blockIdx.x * kRows + rr;
-        if (j < d) {
-            float *dst = y + size_t(bb) * d + j;
-            *dst = (accumulate ? *dst : 0.f) + yacc[i];
-        }
-    }
-}
 
 // ---------------------------------------------------------------------------------
 // Batch-1 path.  One token, so no grouping: position j of exec_idx is expert j's pair.
@@ -400,7 +197,7 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1(
 }
 
 // ---------------------------------------------------------------------------------
-// Batched path (B >= 16): grouped GEMMs on the matrix cores.
+// Batched path (B >= 2): grouped GEMMs on the matrix cores.
 //
 // group_pairs (one workgroup) writes the (expert, token) grouping once per call; the
 // GEMM kernels take tokens as the M dimension (tiles of 16, padded), weight rows as N
@@ -551,7 +348,11 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW]
 #pragma unroll
         for (int tt = 0; tt < MT; ++tt) acc[m][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
     const int nb = (K + kKB - 1) / kKB;
-    gemm_load<NW, MT>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, 0, r0, seg);
+    // Workgroups start at different K blocks: tiles that run side by side then read
+    // different offsets of their rows instead of all hitting the same DRAM channels.
+    const int rot = int((blockIdx.x * 7u + blockIdx.y * 13u) % unsigned(nb));
+    const auto kblk = [nb, rot](int b) { const int q = b + rot; return (q >= nb ? q - nb : q) * kKB; };
+    gemm_load<NW, MT>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, kblk(0), r0, seg);
     for (int b = 0; b < nb; ++b) {
         __syncthreads();   // the previous block's fragments have been read
 #pragma unroll
@@ -564,7 +365,7 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW]
         __syncthreads();
         if (b + 1 < nb)
             gemm_load<NW, MT>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok,
-                              (b + 1) * kKB, r0, seg);
+                              kblk(b + 1), r0, seg);
 #pragma unroll
         for (int q = 0; q < kKB / 32; ++q) {
             const int kc = 32 * q + 8 * (lane >> 4);
@@ -696,14 +497,14 @@ __global__ __launch_bounds__(256) void combine_pairs(
     *dst = (accumulate ? *dst : 0.f) + s;
 }
 
-constexpr int kMfmaMinBatch = 16;
+constexpr int kMfmaMinBatch = 2;
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
 // workspace: [GroupTable][h: B*k x I fp32 (bf16 on the batched path)]
-//            then, for B >= 16: [per-pair outputs: B*k x d fp32][bf16 activations: B x d]
+//            then, for B >= 2: [per-pair outputs: B*k x d fp32][bf16 activations: B x d]
 extern "C" size_t apex_moe_ffn_workspace_bytes(int B, int d, int I, int k) {
     if (B <= 0 || k <= 0 || I <= 0 || d <= 0) return 256;
     const size_t P = size_t(B) * k;
@@ -747,45 +548,6 @@ extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, 
     float *h = reinterpret_cast<float *>(wsb + align_up(sizeof(GroupTable), 256));
     const int max_act = P < E ? P : E;
 
-    if (B >= kMfmaMinBatch) {
-        char *after_h = wsb + align_up(sizeof(GroupTable), 256) +
-                        align_up(size_t(P) * I * sizeof(float), 256);
-        float *ypair = reinterpret_cast<float *>(after_h);
-        __bf16 *xb = reinterpret_cast<__bf16 *>(after_h + align_up(size_t(P) * d * sizeof(float), 256));
-        __bf16 *hb = reinterpret_cast<__bf16 *>(h);
-        const size_t n8 = size_t(B) * d / 8;
-        const unsigned conv_blocks = unsigned(std::min<size_t>(64, (n8 + kGroupThreads - 1) / kGroupThreads));
-        hipLaunchKernelGGL(group_pairs, dim3(conv_blocks), dim3(kGroupThreads), 0, stream,
-                           exec_idx, slot_of_expert, P, E, n_slots, G, x, B, d, xb);
-        APEX_HIP(hipGetLastError());
-        const dim3 gu((I + 63) / 64, max_act), gd((d + 63) / 64, max_act);
-        // token tiles per pass: enough for the whole batch on one expert up to 64 tokens
-        if (B >= 48) {
-            hipLaunchKernelGGL((up_gemm<4>), gu, dim3(256), 0, stream, xb, d, I, k, G,
-                               slot_of_expert, slots, slot_elems, hb);
-            APEX_HIP(hipGetLastError());
-            hipLaunchKernelGGL((down_gemm<4>), gd, dim3(256), 0, stream, d, I, G,
-                               slot_of_expert, slots, slot_elems, hb, ypair);
-        } else if (B >= 24) {
-            hipLaunchKernelGGL((up_gemm<2>), gu, dim3(256), 0, stream, xb, d, I, k, G,
-                               slot_of_expert, slots, slot_elems, hb);
-            APEX_HIP(hipGetLastError());
-            hipLaunchKernelGGL((down_gemm<2>), gd, dim3(256), 0, stream, d, I, G,
-                               slot_of_expert, slots, slot_elems, hb, ypair);
-        } else {
-            hipLaunchKernelGGL((up_gemm<1>), gu, dim3(256), 0, stream, xb, d, I, k, G,
-                               slot_of_expert, slots, slot_elems, hb);
-            APEX_HIP(hipGetLastError());
-            hipLaunchKernelGGL((down_gemm<1>), gd, dim3(256), 0, stream, d, I, G,
-                               slot_of_expert, slots, slot_elems, hb, ypair);
-        }
-        APEX_HIP(hipGetLastError());
-        hipLaunchKernelGGL(combine_pairs, dim3((d + 255) / 256, B), dim3(256), 0, stream, B, d, E,
-                           k, exec_idx, exec_gate, slot_of_expert, n_slots, ypair, y, accumulate);
-        APEX_HIP(hipGetLastError());
-        return APEX_OK;
-    }
-
     if (B == 1) {
         // h holds gated rows per position; tile shapes measured on MI355X (streaming rate
         // of the two launches against the plain read rate at the same sizes)
@@ -821,23 +583,43 @@ extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, 
         return APEX_OK;
     }
 
-    constexpr int RW = 4;
-    const dim3 g1((I + kWavesPerGroup * RW - 1) / (kWavesPerGroup * RW), max_act);
-    if (B == 1)
-        hipLaunchKernelGGL((ffn_gate_up<RW, 1>), g1, dim3(kThreads), 0, stream, x, d, I, E, k, P,
-                           exec_idx, slot_of_expert, slots, n_slots, slot_elems, h);
-    else
-        hipLaunchKernelGGL((ffn_gate_up<RW, 4>), g1, dim3(kThreads), 0, stream, x, d, I, E, k, P,
-                           exec_idx, slot_of_expert, slots, n_slots, slot_elems, h);
+    // B >= 2: grouped GEMM on the matrix cores
+    char *after_h = wsb + align_up(sizeof(GroupTable), 256) +
+                    align_up(size_t(P) * I * sizeof(float), 256);
+    float *ypair = reinterpret_cast<float *>(after_h);
+    __bf16 *xb = reinterpret_cast<__bf16 *>(after_h + align_up(size_t(P) * d * sizeof(float), 256));
+    __bf16 *hb = reinterpret_cast<__bf16 *>(h);
+    const size_t n8 = size_t(B) * d / 8;
+    const unsigned conv_blocks = unsigned(std::min<size_t>(64, (n8 + kGroupThreads - 1) / kGroupThreads));
+    hipLaunchKernelGGL(group_pairs, dim3(conv_blocks), dim3(kGroupThreads), 0, stream,
+                       exec_idx, slot_of_expert, P, E, n_slots, G, x, B, d, xb);
     APEX_HIP(hipGetLastError());
-
-    constexpr int RD = 1, UI = 8;
-    const int rows = kWavesPerGroup * RD;
-    const dim3 g2((d + rows - 1) / rows);
-    const size_t smem = size_t(B) * rows * sizeof(float);
-    hipLaunchKernelGGL((ffn_down<RD, UI>), g2, dim3(kThreads), smem, stream, B, d, I, E, k, P,
-                       exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h, y,
-                       accumulate);
+    const dim3 gu((I + 63) / 64, max_act), gd((d + 63) / 64, max_act);
+    // token tiles per pass: enough for the whole batch on one expert up to 64 tokens
+    if (B >= 48) {
+        hipLaunchKernelGGL((up_gemm<4>), gu, dim3(256), 0, stream, xb, d, I, k, G,
+                           slot_of_expert, slots, slot_elems, hb);
+        APEX_HIP(hipGetLastError());
+        hipLaunchKernelGGL((down_gemm<4>), gd, dim3(256), 0, stream, d, I, G,
+                           slot_of_expert, slots, slot_elems, hb, ypair);
+    } else if (B >= 24) {
+        hipLaunchKernelGGL((up_gemm<2>), gu, dim3(256), 0, stream, xb, d, I, k, G,
+                           slot_of_expert, slots, slot_elems, hb);
+        APEX_HIP(hipGetLastError());
+        hipLaunchKernelGGL((down_gemm<2>), gd, dim3(256), 0, stream, d, I, G,
+                           slot_of_expert, slots, slot_elems, hb, ypair);
+    } else {
+        hipLaunchKernelGGL((up_gemm<1>), gu, dim3(256), 0, stream, xb, d, I, k, G,
+                           slot_of_expert, slots, slot_elems, hb);
+        APEX_HIP(hipGetLastError());
+        hipLaunchKernelGGL((down_gemm<1>), gd, dim3(256), 0, stream, d, I, G,
+                           slot_of_expert, slots, slot_elems, hb, ypair);
+    }
+    APEX_HIP(hipGetLastError());
+    hipLaunchKernelGGL(combine_pairs, dim3((d + 255) / 256, B), dim3(256), 0, stream, B, d, E,
+                       k, exec_idx, exec_gate, slot_of_expert, n_slots, ypair, y, accumulate);
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }
+
+

@@ -276,10 +276,12 @@ def test_ffn_parity_workload_shapes(torch, name, B):
 
 
 MFMA_SHAPES = [
-    # batched path (>= 16 tokens): matrix-core grouped GEMMs
+    # batched path (>= 2 tokens; the shapes above with B > 1 take it too): matrix-core
+    # grouped GEMMs with one, two or four 16-token tiles per pass
     (shape("mfma_ragged", 410, 264, 12, 3, I=200), 40),   # d % 32 != 0, I % 16 != 0
     (shape("mfma_b48", 411, 512, 6, 2, I=256), 48),       # four token tiles per pass
-    (shape("mfma_b16", 412, 1024, 32, 8, I=512), 16),     # smallest batch on this path
+    (shape("mfma_b16", 412, 1024, 32, 8, I=512), 16),     # one tile per pass
+    (shape("mfma_b2", 415, 1024, 32, 8, I=512), 2),       # smallest batch on this path
 ]
 
 
