@@ -12,7 +12,11 @@ timeline with the attention-window stand-in subtracted (the MoE path's own cost
 including exposed stall); lower is better.
 
     python bench.py [--steps K] [--warmup W] [--config granite-1b-a400m] [--batch 1]
-                    [--mode exact|stall_free] [--t-attn-us 10] [--no-cpu-baseline]
+                    [--mode exact|stall_free] [--policy cumprob|ordinal|static]
+                    [--static-delta D] [--tau T] [--t-attn-us 10] [--no-cpu-baseline]
+
+With --policy ordinal, every layer's coverage model is first fitted on held-out tokens
+(the method's training stage, outside the timed region).
 """
 from __future__ import annotations
 
@@ -28,6 +32,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+FFN_KERNELS = {True: "apex_moe_ffn (up_b1 + down_b1)",
+               False: "apex_moe_ffn (group_pairs + up_gemm + down_gemm + combine_pairs)"}
 
 
 def parse():
@@ -39,6 +45,10 @@ def parse():
     p.add_argument("--batch", type=int, default=1)
     p.add_argument("--mode", default="exact", choices=["exact", "stall_free"])
     p.add_argument("--tau", type=float, default=None)
+    p.add_argument("--policy", default="cumprob", choices=["cumprob", "ordinal", "static"])
+    p.add_argument("--static-delta", type=int, default=0)
+    p.add_argument("--cdf-tokens", type=int, default=1024,
+                   help="held-out tokens per layer for the ordinal-model fit")
     p.add_argument("--t-attn-us", type=float, default=10.0)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
@@ -140,7 +150,7 @@ def measured_traffic(cfg, batch):
     return rec.get("traffic_bytes_per_call")
 
 
-def cpu_baseline(cfg, batch, mode, tau, budget_s):
+def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=None):
     """The oracle, as it stands, on the first layer-steps of the same workload."""
     from oracle import decode
     try:
@@ -151,7 +161,8 @@ def cpu_baseline(cfg, batch, mode, tau, budget_s):
         threads = 1
     layers = list(range(min(cfg.L, 4)))
     steps = 64
-    gen = decode.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers)
+    gen = decode.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers, policy=policy,
+                     static_delta=static_delta, cdf=cdf)
     # timed as the oracle runs: its seeded input generation is inside the sample
     n, elapsed = 0, 0.0
     it = iter(gen)
@@ -182,9 +193,16 @@ def main():
     cfg = configs.get(args.config)
     mode = EXACT if args.mode == "exact" else STALL_FREE
     tau = cfg.tau if args.tau is None else args.tau
+    policy = {"cumprob": native.SEL_CUMPROB, "ordinal": native.SEL_ORDINAL_CDF,
+              "static": native.SEL_STATIC}[args.policy]
+    cdf, cdf_report = None, None
+    if policy == native.SEL_ORDINAL_CDF:
+        from paper_2608_11688_amd import cdf_fit
+        cdf, cdf_report = cdf_fit.fit_model(cfg, tokens=args.cdf_tokens)
     total = args.warmup + args.steps
     runner = DecodeRunner(cfg, batch=args.batch, mode=mode, tau=tau, steps=max(total, 1),
-                          t_attn_us=args.t_attn_us)
+                          t_attn_us=args.t_attn_us, policy=policy,
+                          static_delta=args.static_delta, cdf=cdf)
     h2d_peak = pinned_h2d_peak(torch)
 
     for _ in range(args.warmup):
@@ -223,7 +241,7 @@ def main():
         "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) bf16 experts)",
         "config": {"workload": cfg.name, "layers": L, "d": cfg.d, "E": cfg.E, "k": cfg.k,
                    "I": cfg.I, "C": cfg.C, "k_max": cfg.k_max, "tau": tau, "batch": B,
-                   "mode": args.mode, "t_attn_us": args.t_attn_us},
+                   "mode": args.mode, "policy": args.policy, "t_attn_us": args.t_attn_us},
         "us_per_layer_step_incl_attn_window": round(us_layer_step, 3),
         "ffn_us": round(leg_ms * 1e3, 3),
         "ffn_hbm_GBps": round(achieved, 1),
@@ -236,15 +254,20 @@ def main():
         "h2d_GBps_over_step": round(copied_bytes_per_step / (ms_per_step * 1e-3) / 1e9, 2),
         "h2d_pinned_peak_GBps": round(h2d_peak, 2),
         "hbm_copy_kernel": calib,
-        "roofline": {"bound": "hbm", "kernel": "apex_moe_ffn (ffn_gate_up + ffn_down)",
+        "roofline": {"bound": "hbm", "kernel": FFN_KERNELS[B == 1],
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic(cfg, B),
                      "bytes_per_launch": leg_bytes, "launches": leg_n},
     }
+    if args.policy == "static":
+        out["config"]["static_delta"] = args.static_delta
+    if cdf_report is not None:
+        out["ordinal_fit"] = cdf_report
     runner.close()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, B, mode, tau, args.cpu_budget_s)
+        out["cpu_baseline"] = cpu_baseline(cfg, B, mode, tau, args.cpu_budget_s, policy,
+                                           args.static_delta, cdf)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -67,11 +67,15 @@ def layer_step(st: LayerState, t, h_pre, h_post, mode, tau, static_delta=0, run_
 
 
 def run(cfg, batch, steps, mode=gating.EXACT, tau=None, seed=0, layers=None, run_ffn=True,
-        policy=routing.CUMPROB, static_delta=0):
-    """Replay ``steps`` decode steps of ``batch`` tokens; yields (t, layer, result)."""
+        policy=routing.CUMPROB, static_delta=0, cdf=None):
+    """Replay ``steps`` decode steps of ``batch`` tokens; yields (t, layer, result).
+
+    cdf: {layer: (w, theta)} ordinal-model parameters when policy is ORDINAL_CDF.
+    """
     tau = cfg.tau if tau is None else tau
     layers = range(cfg.L) if layers is None else layers
-    states = {l: LayerState(cfg, l, seed, policy) for l in layers}
+    states = {l: LayerState(cfg, l, seed, policy, None if cdf is None else cdf[l])
+              for l in layers}
     hs = {l: inputs.hidden_states(cfg, l, batch, steps, seed) for l in layers}
     for t in range(steps):
         for l in layers:

@@ -143,7 +143,12 @@ class DecodeRunner:
                    eos=eos, last_used=np.full(cfg.E, -1, np.int64), h_pre=to_dev(h_pre),
                    h_post=to_dev(h_post), cdf_w=None, cdf_theta=None)
         if self.policy == native.SEL_ORDINAL_CDF:
-            w, theta = cdf if cdf is not None else inputs.cdf_params(cfg, l, self.seed)
+            if cdf is None:
+                w, theta = inputs.cdf_params(cfg, l, self.seed)
+            elif isinstance(cdf, dict):
+                w, theta = cdf[l]          # one fitted model per layer
+            else:
+                w, theta = cdf             # one model for every layer
             out["cdf_w"] = to_dev(np.asarray(w, np.float32))
             out["cdf_theta"] = to_dev(np.asarray(theta, np.float32))
         return out

@@ -18,18 +18,19 @@ pytestmark = pytest.mark.gpu
 
 
 def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau=None,
-                 ffn_every=1):
+                 ffn_every=1, cdf=None):
+    """cdf: {layer: (w, theta)} for the ORDINAL policy; seeded random models if None."""
     from paper_2608_11688_amd.runtime import DecodeRunner
     tau = cfg.tau if tau is None else tau
     tau32 = float(np.float32(tau))
     runner = DecodeRunner(cfg, batch=batch, mode=mode, tau=tau32, policy=policy, steps=steps,
-                          layers=layers, t_attn_us=2.0, record=True)
+                          layers=layers, t_attn_us=2.0, record=True, cdf=cdf)
     ledger = TieLedger()
     res = {l: Residency(cfg.E, cfg.C) for l in layers}
     routers = {l: inputs.router_weights(cfg, l) for l in layers}
     hs = {l: inputs.hidden_states(cfg, l, batch, steps) for l in layers}
-    cdfs = {l: inputs.cdf_params(cfg, l) for l in layers}
-    stats = dict(copies=0, misses=0, ffn_checked=0, worst_l1=0.0)
+    cdfs = cdf if cdf is not None else {l: inputs.cdf_params(cfg, l) for l in layers}
+    stats = dict(copies=0, misses=0, ffn_checked=0, worst_l1=0.0, covered=0, tokens=0)
     try:
         for t in range(steps):
             logs = runner.step()
@@ -52,6 +53,9 @@ def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau
                 g = gating.gate_topk(h_post, wg, bias, cfg.k, mode, avail)
                 ledger.compare_rows(log.route_idx, g["route_idx"], g["margin"], f"route t{t} l{l}")
                 ledger.compare_rows(log.exec_idx, g["exec_idx"], g["margin"], f"exec t{t} l{l}")
+                for b in range(batch):
+                    stats["covered"] += set(log.route_idx[b]) <= set(lists[b])
+                stats["tokens"] += batch
                 if mode == native.MODE_EXACT:
                     want = sorted(set(int(e) for e in log.route_idx.ravel()) - R)
                     assert log.missing == want, (t, l, log.missing, want)
@@ -94,3 +98,17 @@ def test_decode_granite3b_batch8_stall_free_ordinal():
 def test_decode_olmoe_batch16_exact():
     cfg = configs.OLMOE
     check_decode(cfg, 16, native.MODE_EXACT, 3, [0, 9], ffn_every=2)
+
+
+def test_decode_granite1b_ordinal_fitted_model():
+    # per-layer models fitted on held-out tokens (training stage on the GPU kernels), then
+    # decoding with them; the oracle replays the same fitted parameters
+    from paper_2608_11688_amd import cdf_fit
+    cfg = configs.GRANITE_1B
+    layers = [0, 11, 23]
+    params, report = cdf_fit.fit_model(cfg, tokens=512, layers=layers)
+    st = check_decode(cfg, 1, native.MODE_EXACT, 8, layers, policy=native.SEL_ORDINAL_CDF,
+                      tau=0.9, cdf=params)
+    print(report, st)
+    # calibrated at tau = 0.9 on held-out tokens: most of these tokens are fully covered
+    assert st["covered"] >= 0.6 * st["tokens"]
