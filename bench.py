@@ -133,21 +133,26 @@ def copy_calibration(torch, native, cs, nbytes=256 << 20, reps=5):
 
 
 def measured_traffic(cfg, batch):
-    """HBM bytes per apex_moe_ffn call from the committed FETCH_SIZE / WRITE_SIZE record,
-    or None when that record is for another workload or the kernel source has changed
-    since the counters were taken."""
+    """HBM bytes per apex_moe_ffn call from the committed FETCH_SIZE / WRITE_SIZE records,
+    or None when no record is for this workload and batch, or the source of the kernels
+    it covers has changed since the counters were taken."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "moe_ffn_traffic.json")
     try:
-        rec = json.load(open(path))
-        src = open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()
+        records = json.load(open(path))["records"]
     except (OSError, KeyError, ValueError):
         return None
-    if hashlib.sha256(src).hexdigest() != rec.get("kernel_source_sha256"):
-        return None
-    if rec.get("workload") != cfg.name or rec.get("batch") != batch:
-        return None
-    return rec.get("traffic_bytes_per_call")
+    for rec in records:
+        if rec.get("workload") != cfg.name or rec.get("batch") != batch:
+            continue
+        try:
+            src = open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()
+        except (OSError, KeyError):
+            return None
+        if hashlib.sha256(src).hexdigest() != rec.get("kernel_source_sha256"):
+            return None
+        return rec.get("traffic_bytes_per_call")
+    return None
 
 
 def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=None):

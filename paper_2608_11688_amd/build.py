@@ -22,9 +22,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libapex.so")
 PLAN_LIB = os.path.join(PKG, "libapex_plan.so")
 
-HIP_SOURCES = ["errors.cpp", "residency.cpp", "decode.cpp", "route_gate.hip", "moe_ffn.hip",
-               "prefetch.hip",
-               "util.hip"]
+HIP_SOURCES = ["errors.cpp", "residency.cpp", "decode.cpp", "route_gate.hip", "moe_ffn.cpp",
+               "ffn_b1.hip", "ffn_gemm.hip", "prefetch.hip", "util.hip"]
 HOST_SOURCES = ["errors.cpp", "residency.cpp"]
 
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -1,200 +1,23 @@
-// Gated SwiGLU experts over HBM cache slots (apex_moe_ffn).
+// Expert FFN for two or more tokens (apex_moe_ffn, batch >= 2): a grouped GEMM on the
+// matrix cores.
 //
-// Both paths stream each executed expert's bf16 weights from HBM once per call and
-// need no atomics, so results are deterministic:
-//
-// Batch 1 (up_b1, down_b1): one token, k experts. up_b1 reads W1/W3 rows of an expert
-//   with all row loads issued before any arithmetic and writes h[j, i]; down_b1 owns one
-//   output row of y and sums g_j * (W2_j[row] . h[j]) over the k experts in one
-//   flattened dot, so the k experts share a single launch.
-// Batch >= 2 (group_pairs, up_gemm, down_gemm, combine_pairs): a grouped GEMM on the
-//   matrix cores. group_pairs converts x to bf16 and builds one table of the pairs
-//   sorted by expert; up_gemm and down_gemm stage 64-row weight tiles and 16*MT token
-//   rows through LDS and issue v_mfma_f32_16x16x32_bf16 on them; combine_pairs sums
-//   the gated per-pair outputs of every token in pair order.
-// Weights are read with 16-byte loads that cover consecutive 16-byte chunks of a row.
+// group_pairs converts x to bf16 and builds one table of the (token, position) pairs
+// sorted by expert; up_gemm and down_gemm stage 64-row weight tiles and 16*MT token rows
+// through LDS and issue v_mfma_f32_16x16x32_bf16 on them; combine_pairs sums the gated
+// per-pair outputs of every token in pair order.  Every executed expert's weights are
+// read once per call whatever the number of tokens routed to it, and no atomics are
+// used, so results are deterministic.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <cmath>
 
-#include "common.h"
+#include "ffn_device.h"
+#include "ffn_internal.h"
 
 namespace {
 
-constexpr int kWave = 64;
-
-__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-__device__ __forceinline__ float dot8(uint4 w, float4 a, float4 b, float acc) {
-    acc = fmaf(bf_lo(w.x), a.x, acc);
-    acc = fmaf(bf_hi(w.x), a.y, acc);
-    acc = fmaf(bf_lo(w.y), a.z, acc);
-    acc = fmaf(bf_hi(w.y), a.w, acc);
-    acc = fmaf(bf_lo(w.z), b.x, acc);
-    acc = fmaf(bf_hi(w.z), b.y, acc);
-    acc = fmaf(bf_lo(w.w), b.z, acc);
-    acc = fmaf(bf_hi(w.w), b.w, acc);
-    return acc;
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-    return v;
-}
-
-__device__ __forceinline__ float silu(float u) { return u / (1.f + expf(-u)); }
-
-// ---------------------------------------------------------------------------------
-// Batch-1 path.  One token, so no grouping: position j of exec_idx is expert j's pair.
-//
-// up_b1: grid (I / (WAVES * RW), k).  A wavefront owns RW rows of the expert at
-// position blockIdx.y and issues every 16-byte load of those rows (W1 and W3, NPL
-// chunks per lane) before the first multiply, so each lane keeps 2 * RW * NPL loads in
-// flight.  Writes h[j, i] = silu(W1[i] . x) * (W3[i] . x) * gate_j: the gate is folded
-// in here so the down projection is one long dot product per output row.
-template <int NPL, int RW, int WAVES>
-__global__ __launch_bounds__(WAVES *kWave) void up_b1(
-    const float *__restrict__ x, int d, int I, int E, int k,
-    const int32_t *__restrict__ exec_idx, const float *__restrict__ exec_gate,
-    const int32_t *__restrict__ slot_of_expert, const uint16_t *__restrict__ slots, int n_slots,
-    size_t slot_elems, float *__restrict__ h) {
-    const int j = blockIdx.y;
-    const int e = exec_idx[j];
-    const float g = exec_gate[j];
-    if (e < 0 || e >= E) return;
-    const int s = slot_of_expert[e];
-    if (s < 0 || s >= n_slots) return;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int i0 = (blockIdx.x * WAVES + wave) * RW;
-    if (i0 >= I) return;
-    const int nch = d / 8;
-    const uint4 *W = reinterpret_cast<const uint4 *>(slots + size_t(s) * slot_elems);
-    const float4 *x4 = reinterpret_cast<const float4 *>(x);
-
-    float u[RW], v[RW];   // lane partial sums over every block of the row
-#pragma unroll
-    for (int r = 0; r < RW; ++r) u[r] = v[r] = 0.f;
-    for (int cb = 0; cb < nch; cb += NPL * kWave) {
-        uint4 w1[RW][NPL], w3[RW][NPL];
-#pragma unroll
-        for (int r = 0; r < RW; ++r) {
-            const int i = (i0 + r < I) ? i0 + r : I - 1;
-            const uint4 *row = W + size_t(i) * 2 * nch;
-#pragma unroll
-            for (int n = 0; n < NPL; ++n) {
-                const int c = cb + lane + n * kWave;
-                if (c < nch) {
-                    w1[r][n] = row[c];
-                    w3[r][n] = row[nch + c];
-                }
-            }
-        }
-        float4 xa[NPL], xb[NPL];
-#pragma unroll
-        for (int n = 0; n < NPL; ++n) {
-            const int c = cb + lane + n * kWave;
-            if (c < nch) {
-                xa[n] = x4[2 * c];
-                xb[n] = x4[2 * c + 1];
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < RW; ++r)
-#pragma unroll
-            for (int n = 0; n < NPL; ++n) {
-                const int c = cb + lane + n * kWave;
-                if (c < nch) {
-                    u[r] = dot8(w1[r][n], xa[n], xb[n], u[r]);
-                    v[r] = dot8(w3[r][n], xa[n], xb[n], v[r]);
-                }
-            }
-    }
-    float hv = 0.f;
-#pragma unroll
-    for (int r = 0; r < RW; ++r) {
-        const float su = wave_sum(u[r]);
-        const float sv = wave_sum(v[r]);
-        if (lane == r) hv = silu(su) * sv * g;
-    }
-    if (lane < RW && i0 + lane < I) h[size_t(j) * I + i0 + lane] = hv;
-}
-
-// down_b1: grid d / (WAVES * RD).  A wavefront owns RD output rows; the gated h of
-// all valid positions is one vector of length (#valid) * I, so each row is a single dot
-// product over the concatenated W2 rows of the executed experts.  Lanes step through
-// (position, chunk) pairs UNR at a time with all loads issued before the multiplies.
-template <int RD, int WAVES, int UNR>
-__global__ __launch_bounds__(WAVES *kWave) void down_b1(
-    int d, int I, int E, int k, const int32_t *__restrict__ exec_idx,
-    const int32_t *__restrict__ slot_of_expert, const uint16_t *__restrict__ slots, int n_slots,
-    size_t slot_elems, const float *__restrict__ h, float *__restrict__ y, int accumulate) {
-    __shared__ int meta_pos[APEX_MAX_EXPERTS];
-    __shared__ const uint4 *meta_w2[APEX_MAX_EXPERTS];
-    __shared__ int n_valid;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int nch = I / 8;
-    if (wave == 0) {
-        const int e = lane < k ? exec_idx[lane] : -1;
-        const int s = (e >= 0 && e < E) ? slot_of_expert[e] : -1;
-        const bool ok = s >= 0 && s < n_slots;
-        const unsigned long long m = __ballot(ok);
-        if (ok) {
-            const int idx = __popcll(m & ((1ull << lane) - 1ull));
-            meta_pos[idx] = lane;
-            meta_w2[idx] = reinterpret_cast<const uint4 *>(slots + size_t(s) * slot_elems +
-                                                           size_t(2) * I * d);
-        }
-        if (lane == 0) n_valid = __popcll(m);
-    }
-    __syncthreads();
-    const int j0 = (blockIdx.x * WAVES + wave) * RD;
-    if (j0 >= d) return;
-    const int total = n_valid * nch;
-    float acc[RD];
-#pragma unroll
-    for (int r = 0; r < RD; ++r) acc[r] = 0.f;
-    // lane's first (position, chunk): t = lane
-    int item = 0, c = lane;
-    while (c >= nch && item < n_valid) { c -= nch; ++item; }
-    for (int t0 = lane; t0 < total; t0 += UNR * kWave) {
-        uint4 w[UNR][RD];
-        float4 ha[UNR], hb[UNR];
-        bool on[UNR];
-        int it = item, cc = c;
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            on[u] = t0 + u * kWave < total;
-            if (on[u]) {
-                const uint4 *w2 = meta_w2[it];
-                const float4 *hr = reinterpret_cast<const float4 *>(h + size_t(meta_pos[it]) * I);
-                ha[u] = hr[2 * cc];
-                hb[u] = hr[2 * cc + 1];
-#pragma unroll
-                for (int r = 0; r < RD; ++r) {
-                    const int jr = (j0 + r < d) ? j0 + r : d - 1;
-                    w[u][r] = w2[size_t(jr) * nch + cc];
-                }
-            }
-            cc += kWave;
-            while (cc >= nch) { cc -= nch; ++it; }
-        }
-        item = it;
-        c = cc;
-#pragma unroll
-        for (int u = 0; u < UNR; ++u)
-            if (on[u])
-#pragma unroll
-                for (int r = 0; r < RD; ++r) acc[r] = dot8(w[u][r], ha[u], hb[u], acc[r]);
-    }
-#pragma unroll
-    for (int r = 0; r < RD; ++r) {
-        const float s = wave_sum(acc[r]);
-        if (lane == r && j0 + r < d) y[j0 + r] = (accumulate ? y[j0 + r] : 0.f) + s;
-    }
-}
+using apex::ffn::kWave;
+using apex::ffn::silu;
 
 // ---------------------------------------------------------------------------------
 // Batched path (B >= 2): grouped GEMMs on the matrix cores.
@@ -497,98 +320,30 @@ __global__ __launch_bounds__(256) void combine_pairs(
     *dst = (accumulate ? *dst : 0.f) + s;
 }
 
-constexpr int kMfmaMinBatch = 2;
-
-size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
-
 }  // namespace
 
-// workspace: [GroupTable][h: B*k x I fp32 (bf16 on the batched path)]
-//            then, for B >= 2: [per-pair outputs: B*k x d fp32][bf16 activations: B x d]
-extern "C" size_t apex_moe_ffn_workspace_bytes(int B, int d, int I, int k) {
-    if (B <= 0 || k <= 0 || I <= 0 || d <= 0) return 256;
+namespace apex {
+
+// [GroupTable][h: B*k x I bf16][per-pair outputs: B*k x d fp32][x: B x d bf16]
+size_t ffn_grouped_workspace(int B, int d, int I, int k) {
     const size_t P = size_t(B) * k;
-    size_t n = align_up(sizeof(GroupTable), 256) + align_up(P * I * sizeof(float), 256);
-    if (B >= kMfmaMinBatch)
-        n += align_up(P * d * sizeof(float), 256) + align_up(size_t(B) * d * 2, 256);
-    return n;
+    return align_up(sizeof(GroupTable), 256) + align_up(P * I * 2, 256) +
+           align_up(P * d * sizeof(float), 256) + align_up(size_t(B) * d * 2, 256);
 }
 
-extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
-                                    const int32_t *exec_idx, const float *exec_gate,
-                                    const int32_t *slot_of_expert, const uint16_t *slots,
-                                    int n_slots, float *y, int accumulate, void *workspace,
-                                    size_t workspace_bytes, hipStream_t stream) {
-    const char *fn = "apex_moe_ffn";
-    APEX_REQUIRE(B >= 0, "%s: B=%d must be >= 0", fn, B);
-    APEX_REQUIRE(E >= 1, "%s: E=%d must be >= 1", fn, E);
-    if (E > APEX_MAX_EXPERTS)
-        return apex::fail(APEX_E_UNSUPPORTED, "%s: E=%d exceeds %d", fn, E, APEX_MAX_EXPERTS);
-    APEX_REQUIRE(k >= 1 && k <= E, "%s: k=%d out of [1, E=%d]", fn, k, E);
-    APEX_REQUIRE(d >= 8 && d % 8 == 0, "%s: d=%d must be a positive multiple of 8", fn, d);
-    APEX_REQUIRE(I >= 8 && I % 8 == 0, "%s: I=%d must be a positive multiple of 8", fn, I);
-    APEX_REQUIRE(n_slots >= 1, "%s: n_slots=%d must be >= 1", fn, n_slots);
-    if (size_t(B) * k > APEX_MAX_PAIRS)
-        return apex::fail(APEX_E_UNSUPPORTED, "%s: B*k=%d exceeds %d", fn, B * k, APEX_MAX_PAIRS);
-    if (B == 0) return APEX_OK;
-    APEX_REQUIRE(x && exec_idx && exec_gate && slot_of_expert && slots && y && workspace,
-                 "%s: NULL pointer", fn);
-    APEX_REQUIRE(apex::aligned16(x) && apex::aligned16(slots) && apex::aligned16(workspace) &&
-                     apex::aligned16(y),
-                 "%s: x, slots, y and workspace must be 16-byte aligned", fn);
-    const size_t need = apex_moe_ffn_workspace_bytes(B, d, I, k);
-    if (workspace_bytes < need)
-        return apex::fail(APEX_E_CAPACITY, "%s: workspace %zu < %zu bytes", fn, workspace_bytes,
-                          need);
-    // y rows are read back when accumulating
+apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
+                        const int32_t *exec_idx, const float *exec_gate,
+                        const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,
+                        float *y, int accumulate, void *workspace, hipStream_t stream) {
     const int P = B * k;
     const size_t slot_elems = size_t(3) * d * I;
+    const int max_act = P < E ? P : E;
     char *wsb = static_cast<char *>(workspace);
     GroupTable *G = reinterpret_cast<GroupTable *>(wsb);
-    float *h = reinterpret_cast<float *>(wsb + align_up(sizeof(GroupTable), 256));
-    const int max_act = P < E ? P : E;
-
-    if (B == 1) {
-        // h holds gated rows per position; tile shapes measured on MI355X (streaming rate
-        // of the two launches against the plain read rate at the same sizes)
-        const int npl = (d + 511) / 512;
-        if (d <= 2048) {
-            const dim3 gu(I / 4 + (I % 4 != 0), k);
-            if (npl <= 1)
-                hipLaunchKernelGGL((up_b1<1, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                                   exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-            else if (npl == 2)
-                hipLaunchKernelGGL((up_b1<2, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                                   exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-            else if (npl == 3)
-                hipLaunchKernelGGL((up_b1<3, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                                   exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-            else
-                hipLaunchKernelGGL((up_b1<4, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                                   exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-            APEX_HIP(hipGetLastError());
-            hipLaunchKernelGGL((down_b1<1, 1, 8>), dim3(d), dim3(64), 0, stream, d, I, E, k,
-                               exec_idx, slot_of_expert, slots, n_slots, slot_elems, h, y,
-                               accumulate);
-        } else {
-            const dim3 gu(I / 8 + (I % 8 != 0), k);
-            hipLaunchKernelGGL((up_b1<4, 2, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-            APEX_HIP(hipGetLastError());
-            hipLaunchKernelGGL((down_b1<4, 4, 8>), dim3(d / 16 + (d % 16 != 0)), dim3(256), 0,
-                               stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
-                               slot_elems, h, y, accumulate);
-        }
-        APEX_HIP(hipGetLastError());
-        return APEX_OK;
-    }
-
-    // B >= 2: grouped GEMM on the matrix cores
-    char *after_h = wsb + align_up(sizeof(GroupTable), 256) +
-                    align_up(size_t(P) * I * sizeof(float), 256);
+    __bf16 *hb = reinterpret_cast<__bf16 *>(wsb + align_up(sizeof(GroupTable), 256));
+    char *after_h = reinterpret_cast<char *>(hb) + align_up(size_t(P) * I * 2, 256);
     float *ypair = reinterpret_cast<float *>(after_h);
     __bf16 *xb = reinterpret_cast<__bf16 *>(after_h + align_up(size_t(P) * d * sizeof(float), 256));
-    __bf16 *hb = reinterpret_cast<__bf16 *>(h);
     const size_t n8 = size_t(B) * d / 8;
     const unsigned conv_blocks = unsigned(std::min<size_t>(64, (n8 + kGroupThreads - 1) / kGroupThreads));
     hipLaunchKernelGGL(group_pairs, dim3(conv_blocks), dim3(kGroupThreads), 0, stream,
@@ -622,4 +377,4 @@ extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, 
     return APEX_OK;
 }
 
-
+}  // namespace apex

@@ -1,0 +1,31 @@
+// Launchers of the two expert-FFN paths behind apex_moe_ffn.  Arguments are checked by
+// the entry point before either is called; both enqueue on `stream` and return
+// APEX_E_HIP if a launch fails.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "common.h"
+
+namespace apex {
+
+// One token: up_b1 then down_b1.  `h` is k x I fp32 scratch.
+size_t ffn_b1_workspace(int d, int I, int k);
+apex_status ffn_b1(const float *x, int d, int I, int E, int k, const int32_t *exec_idx,
+                   const float *exec_gate, const int32_t *slot_of_expert, const uint16_t *slots,
+                   int n_slots, float *h, float *y, int accumulate, hipStream_t stream);
+
+// Two or more tokens: grouped GEMMs on the matrix cores.  `workspace` is 256-byte
+// aligned and holds ffn_grouped_workspace(B, d, I, k) bytes.
+size_t ffn_grouped_workspace(int B, int d, int I, int k);
+apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
+                        const int32_t *exec_idx, const float *exec_gate,
+                        const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,
+                        float *y, int accumulate, void *workspace, hipStream_t stream);
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace apex

@@ -155,5 +155,6 @@ def test_entry_points_validate_before_enqueue(hip_lib):
 def test_workspace_size():
     small = native.apex_moe_ffn_workspace_bytes(1, 1024, 512, 8)
     assert small >= 8 * 512 * 4 and small % 256 == 0
-    big = native.apex_moe_ffn_workspace_bytes(64, 2048, 1024, 8)   # batched path: + outputs
-    assert big >= 512 * (1024 + 2048) * 4 and big % 256 == 0
+    big = native.apex_moe_ffn_workspace_bytes(64, 2048, 1024, 8)   # batched path
+    # bf16 h and fp32 per-pair outputs for 512 pairs, bf16 activations
+    assert big >= 512 * (1024 * 2 + 2048 * 4) + 64 * 2048 * 2 and big % 256 == 0
