@@ -1,12 +1,20 @@
 // Expert FFN for two or more tokens (apex_moe_ffn, batch >= 2): a grouped GEMM on the
 // matrix cores.
 //
-// group_pairs converts x to bf16 and builds one table of the (token, position) pairs
-// sorted by expert; up_gemm and down_gemm stage 64-row weight tiles and 16*MT token rows
-// through LDS and issue v_mfma_f32_16x16x32_bf16 on them; combine_pairs sums the gated
-// per-pair outputs of every token in pair order.  Every executed expert's weights are
-// read once per call whatever the number of tokens routed to it, and no atomics are
-// used, so results are deterministic.
+// up_gemm and down_gemm take tokens as the M dimension (tiles of 16, padded), weight
+// rows as N and the hidden / intermediate dimension as K, with v_mfma_f32_16x16x32_bf16
+// (activations rounded to bf16, fp32 accumulation).  A workgroup owns 64 weight rows of
+// one expert (blockIdx.y is the expert id; experts without a slot or without tokens exit
+// at once) and finds that expert's (token, position) pairs itself from exec_idx, in pair
+// order.  When a projection has too few row tiles to keep the chip's loads in flight, its
+// K range is split over blockIdx.z and each split writes fp32 partial sums:
+//   * up_gemm with one split writes h = bf16(silu(W1 x) * (W3 x)) per pair; with several
+//     it writes the partial W1 x and W3 x, and down_gemm forms h from their sums while
+//     it stages its activations;
+//   * down_gemm writes per-split, per-pair outputs; combine_pairs adds the splits and the
+//     gated positions of each token in a fixed order.
+// Every executed expert's weights are read once per call whatever the number of tokens
+// routed to it, and no atomics are used, so results are deterministic.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -19,124 +27,106 @@ namespace {
 using apex::ffn::kWave;
 using apex::ffn::silu;
 
-// ---------------------------------------------------------------------------------
-// Batched path (B >= 2): grouped GEMMs on the matrix cores.
-//
-// group_pairs (one workgroup) writes the (expert, token) grouping once per call; the
-// GEMM kernels take tokens as the M dimension (tiles of 16, padded), weight rows as N
-// and the hidden / intermediate dimension as K, with v_mfma_f32_16x16x32_bf16
-// (activations rounded to bf16, fp32 accumulation).  Every expert's weights are read
-// once per call whatever the number of tokens routed to it.  Per-pair outputs go to
-// the workspace and a combine kernel applies the gates in a fixed order.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-struct GroupTable {          // lives at the start of the workspace
-    int n_act;
-    int n_items;
-    int act_e[APEX_MAX_EXPERTS];
-    int act_start[APEX_MAX_EXPERTS + 1];
-    int item[APEX_MAX_PAIRS];   // pair indices sorted by (expert, pair)
-};
-
-constexpr int kGroupThreads = 1024;
-
-// Every workgroup rounds a slice of the activations to bf16 (xb [B, d], 8 values per
-// thread per step) for the matrix cores; workgroup 0 also builds the grouping.
-__global__ __launch_bounds__(kGroupThreads) void group_pairs(
-    const int32_t *__restrict__ exec_idx, const int32_t *__restrict__ slot_of_expert, int P, int E,
-    int n_slots, GroupTable *__restrict__ G, const float *__restrict__ x, int B, int d,
-    __bf16 *__restrict__ xb) {
-    const size_t n8 = size_t(B) * d / 8;
-    for (size_t i = size_t(blockIdx.x) * kGroupThreads + threadIdx.x; i < n8;
-         i += size_t(gridDim.x) * kGroupThreads) {
-        const float4 p = reinterpret_cast<const float4 *>(x)[2 * i];
-        const float4 q = reinterpret_cast<const float4 *>(x)[2 * i + 1];
-        bf16x8 v;
-        v[0] = (__bf16)p.x; v[1] = (__bf16)p.y; v[2] = (__bf16)p.z; v[3] = (__bf16)p.w;
-        v[4] = (__bf16)q.x; v[5] = (__bf16)q.y; v[6] = (__bf16)q.z; v[7] = (__bf16)q.w;
-        reinterpret_cast<bf16x8 *>(xb)[i] = v;
-    }
-    if (blockIdx.x != 0) return;
-    constexpr int kW = kGroupThreads / kWave;
-    __shared__ int cnt[kW][APEX_MAX_EXPERTS];
-    __shared__ int wave_off[kW][APEX_MAX_EXPERTS];
-    __shared__ int start[APEX_MAX_EXPERTS + 1];
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    for (int base = 0; base < P; base += kGroupThreads) {
-        // pairs [base, base + 1024) this round; P <= 1024 so there is one round
-        const int p = base + threadIdx.x;
-        int e = -1;
-        if (p < P) {
-            const int x = exec_idx[p];
-            if (x >= 0 && x < E) {
-                const int s = slot_of_expert[x];
-                if (s >= 0 && s < n_slots) e = x;
-            }
-        }
-        int local = 0;
-        for (int ex = 0; ex < E; ++ex) {
-            const unsigned long long m = __ballot(e == ex);
-            if (e == ex) local = __popcll(m & ((1ull << lane) - 1ull));
-            if (lane == 0) cnt[wave][ex] = __popcll(m);
-        }
-        __syncthreads();
-        if (threadIdx.x < E) {
-            int run = 0;
-            for (int w = 0; w < kW; ++w) {
-                wave_off[w][threadIdx.x] = run;
-                run += cnt[w][threadIdx.x];
-            }
-            cnt[0][threadIdx.x] = run;   // total per expert (cnt[0] already consumed)
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            int run = 0, n_act = 0;
-            for (int ex = 0; ex < E; ++ex) {
-                start[ex] = run;
-                if (cnt[0][ex] > 0) {
-                    G->act_e[n_act] = ex;
-                    G->act_start[n_act] = run;
-                    ++n_act;
-                }
-                run += cnt[0][ex];
-            }
-            start[E] = run;
-            G->act_start[n_act] = run;
-            G->n_act = n_act;
-            G->n_items = run;
-        }
-        __syncthreads();
-        if (e >= 0) G->item[start[e] + wave_off[wave][e] + local] = p;
-    }
-}
+constexpr int kThreads = 256;
+constexpr int kRows = 64;          // weight rows per workgroup tile
+constexpr int kKB = 128;           // K per staged block
+constexpr int kLdsRow = kKB + 8;   // +16 B per row: the 16 rows of a fragment read hit distinct banks
+constexpr int kMaxSplit = 4;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// Grouped-GEMM mainloop shared by the gate/up and down projections.
-// A workgroup (4 wavefronts) owns a tile of 64 weight rows of NW weight matrices and up
-// to 16*MT tokens.  K advances in blocks of 128: every thread loads 16-byte pieces so
-// that each group of 16 threads reads 256 contiguous bytes of one weight row (whole
-// cache lines), the block goes to LDS, and while the matrix cores work on it the next
-// block is already loading into registers.  Wavefront w multiplies its 16 rows with
-// every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.
-constexpr int kKB = 128;
-constexpr int kLdsRow = kKB + 8;   // +16 B per row: the 16 rows of a fragment read hit distinct banks
+__device__ __forceinline__ uint4 pack_bf16(float a0, float a1, float a2, float a3, float a4,
+                                           float a5, float a6, float a7) {
+    bf16x8 v;
+    v[0] = (__bf16)a0; v[1] = (__bf16)a1; v[2] = (__bf16)a2; v[3] = (__bf16)a3;
+    v[4] = (__bf16)a4; v[5] = (__bf16)a5; v[6] = (__bf16)a6; v[7] = (__bf16)a7;
+    return __builtin_bit_cast(uint4, v);
+}
 
-// One K block of the tile into registers.  Every address is valid (rows and K are
-// clamped); pieces outside the tile are zeroed after the load instead of branching,
-// so all 4*NW + MT loads issue back to back.
 // Component-wise select: a select of the whole vector struct is lowered through
 // private memory by the compiler.
 __device__ __forceinline__ uint4 keep_if(uint4 v, bool c) {
     return make_uint4(c ? v.x : 0u, c ? v.y : 0u, c ? v.z : 0u, c ? v.w : 0u);
 }
 
-template <int NW, int MT>
+// Activation sources: 8 consecutive K values of one row as bf16.
+struct ActF32 {          // fp32 rows (the FFN input x), rounded here
+    static __device__ __forceinline__ uint4 load(const void *row, int kc, size_t) {
+        const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(row) + kc);
+        const float4 a = p[0], b = p[1];
+        return pack_bf16(a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w);
+    }
+};
+struct ActBf16 {         // bf16 rows (h written by a one-split up_gemm)
+    static __device__ __forceinline__ uint4 load(const void *row, int kc, size_t) {
+        return *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(row) + kc);
+    }
+};
+template <int SU>
+struct ActSwiglu {       // h from SU split partials: u of split s at row + 2s*stride, v at +1
+    static __device__ __forceinline__ uint4 load(const void *row, int kc, size_t stride) {
+        const float *r = static_cast<const float *>(row) + kc;
+        float u[8], v[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) u[c] = v[c] = 0.f;
+#pragma unroll
+        for (int s = 0; s < SU; ++s) {
+            const float4 *pu = reinterpret_cast<const float4 *>(r + 2 * s * stride);
+            const float4 *pv = reinterpret_cast<const float4 *>(r + (2 * s + 1) * stride);
+            const float4 u0 = pu[0], u1 = pu[1], v0 = pv[0], v1 = pv[1];
+            u[0] += u0.x; u[1] += u0.y; u[2] += u0.z; u[3] += u0.w;
+            u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
+            v[0] += v0.x; v[1] += v0.y; v[2] += v0.z; v[3] += v0.w;
+            v[4] += v1.x; v[5] += v1.y; v[6] += v1.z; v[7] += v1.w;
+        }
+        return pack_bf16(silu(u[0]) * v[0], silu(u[1]) * v[1], silu(u[2]) * v[2],
+                         silu(u[3]) * v[3], silu(u[4]) * v[4], silu(u[5]) * v[5],
+                         silu(u[6]) * v[6], silu(u[7]) * v[7]);
+    }
+};
+
+// The pairs p < P with exec_idx[p] == e, in ascending order, into list[]; returns how
+// many.  256 threads; P <= 1024 (four rounds of wave ballots).
+__device__ int expert_pairs(const int32_t *__restrict__ exec_idx, int P, int e, int *list,
+                            int (*cnt)[4]) {
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    int ev[APEX_MAX_PAIRS / kThreads];
+#pragma unroll
+    for (int r = 0; r < APEX_MAX_PAIRS / kThreads; ++r) {
+        const int p = r * kThreads + t;
+        ev[r] = p < P ? exec_idx[p] : -1;
+    }
+    unsigned long long m[APEX_MAX_PAIRS / kThreads];
+#pragma unroll
+    for (int r = 0; r < APEX_MAX_PAIRS / kThreads; ++r) {
+        m[r] = __ballot(ev[r] == e);
+        if (lane == 0) cnt[r][wave] = __popcll(m[r]);
+    }
+    __syncthreads();
+    int base = 0;
+#pragma unroll
+    for (int r = 0; r < APEX_MAX_PAIRS / kThreads; ++r) {
+        int off = base;
+        for (int w = 0; w < wave; ++w) off += cnt[r][w];
+        if (ev[r] == e) list[off + __popcll(m[r] & ((1ull << lane) - 1ull))] = r * kThreads + t;
+        base += cnt[r][0] + cnt[r][1] + cnt[r][2] + cnt[r][3];
+    }
+    __syncthreads();
+    return base;
+}
+
+// One K block of the tile into registers.  Every weight address is valid (rows and K
+// are clamped) and pieces outside the tile are zeroed after the load instead of
+// branching, so the 4*NW weight loads issue back to back.
+template <int NW, int MT, class Act>
 __device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][4], uint4 (&xreg)[MT],
                                           const uint16_t *const (&wbase)[NW], size_t wstride,
-                                          int rows_valid, int K, const uint16_t *const (&xrow)[MT],
-                                          const bool (&xok)[MT], int k0, int r0, int seg) {
+                                          int rows_valid, int K, const void *const (&xrow)[MT],
+                                          const bool (&xok)[MT], size_t xstride, int k0, int r0,
+                                          int seg) {
     const int kk = k0 + 8 * seg;
     const bool in = kk < K;
     const int kc = in ? kk : K - 8;
@@ -149,19 +139,28 @@ __device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][4], uint4 (&xreg)[MT
             const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + kc);
             wreg[m][j] = keep_if(v, in && row < rows_valid);
         }
+    // activation rows past the expert's tokens (tile padding) are not loaded at all
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(xrow[j] + kc);
-        xreg[j] = keep_if(v, in && xok[j]);
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (in && xok[j]) v = Act::load(xrow[j], kc, xstride);
+        xreg[j] = v;
     }
 }
 
-template <int NW, int MT>
+// Grouped-GEMM mainloop shared by the gate/up and down projections.
+// A workgroup (4 wavefronts) owns a tile of 64 weight rows of NW weight matrices and up
+// to 16*MT tokens, over the K blocks [b_lo, b_hi).  Every thread loads 16-byte pieces so
+// that each group of 16 threads reads 256 contiguous bytes of one weight row (whole
+// cache lines), the block goes to LDS, and while the matrix cores work on it the next
+// block is already loading into registers.  Wavefront w multiplies its 16 rows with
+// every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.
+template <int NW, int MT, class Act>
 __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW], size_t wstride,
-                                              int rows_valid, int K,
-                                              const uint16_t *const (&xrow)[MT],
-                                              const bool (&xok)[MT], int n_tiles,
-                                              uint16_t (*Ws)[64][kLdsRow],
+                                              int rows_valid, int K, int b_lo, int b_hi,
+                                              const void *const (&xrow)[MT],
+                                              const bool (&xok)[MT], size_t xstride,
+                                              int n_tiles, uint16_t (*Ws)[kRows][kLdsRow],
                                               uint16_t (*Xs)[kLdsRow], floatx4 (&acc)[NW][MT]) {
     const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
     const int seg = t & 15, r0 = t >> 4;
@@ -170,12 +169,17 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW]
     for (int m = 0; m < NW; ++m)
 #pragma unroll
         for (int tt = 0; tt < MT; ++tt) acc[m][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const int nb = (K + kKB - 1) / kKB;
+    const int nb = b_hi - b_lo;
+    if (nb <= 0) return;
     // Workgroups start at different K blocks: tiles that run side by side then read
     // different offsets of their rows instead of all hitting the same DRAM channels.
     const int rot = int((blockIdx.x * 7u + blockIdx.y * 13u) % unsigned(nb));
-    const auto kblk = [nb, rot](int b) { const int q = b + rot; return (q >= nb ? q - nb : q) * kKB; };
-    gemm_load<NW, MT>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, kblk(0), r0, seg);
+    const auto kblk = [nb, rot, b_lo](int b) {
+        const int q = b + rot;
+        return (b_lo + (q >= nb ? q - nb : q)) * kKB;
+    };
+    gemm_load<NW, MT, Act>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, xstride,
+                           kblk(0), r0, seg);
     for (int b = 0; b < nb; ++b) {
         __syncthreads();   // the previous block's fragments have been read
 #pragma unroll
@@ -187,8 +191,8 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW]
         for (int j = 0; j < MT; ++j) *reinterpret_cast<uint4 *>(&Xs[r0 + 16 * j][8 * seg]) = xreg[j];
         __syncthreads();
         if (b + 1 < nb)
-            gemm_load<NW, MT>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok,
-                              kblk(b + 1), r0, seg);
+            gemm_load<NW, MT, Act>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, xstride,
+                                   kblk(b + 1), r0, seg);
 #pragma unroll
         for (int q = 0; q < kKB / 32; ++q) {
             const int kc = 32 * q + 8 * (lane >> 4);
@@ -209,82 +213,108 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW]
     }
 }
 
-// up_gemm: grid (ceil(I / 64), max active experts): 64 rows of W1 and W3 of one expert,
-// every token of the expert (16*MT per pass).
-// hb[pair, i] = bf16(silu(W1[i] . x_b) * (W3[i] . x_b)), ungated.
-template <int MT>
-__global__ __launch_bounds__(256) void up_gemm(
-    const __bf16 *__restrict__ xb, int d, int I, int k, const GroupTable *__restrict__ G,
-    const int32_t *__restrict__ slot_of_expert, const uint16_t *__restrict__ slots,
-    size_t slot_elems, __bf16 *__restrict__ hb) {
-    __shared__ uint16_t Ws[2][64][kLdsRow];
+__device__ __forceinline__ void split_range(int K, int splits, int z, int &b_lo, int &b_hi) {
+    const int nb = (K + kKB - 1) / kKB;
+    b_lo = z * nb / splits;
+    b_hi = (z + 1) * nb / splits;
+}
+
+// up_gemm: grid (ceil(I / 64), E, SU).  64 rows of W1 and W3 of expert blockIdx.y, every
+// token of the expert (16*MT per pass), K blocks of split blockIdx.z.
+// SU == 1: hb[pair, i] = bf16(silu(W1[i] . x_b) * (W3[i] . x_b)), ungated.
+// SU  > 1: uv[(2z) * P*I + pair*I + i] = W1[i] . x_b over the split, uv[(2z+1) ...] = W3.
+template <int MT, int SU>
+__global__ __launch_bounds__(kThreads) void up_gemm(
+    const float *__restrict__ x, int d, int I, int P, int k, const int32_t *__restrict__ exec_idx,
+    const int32_t *__restrict__ slot_of_expert, int n_slots, const uint16_t *__restrict__ slots,
+    size_t slot_elems, __bf16 *__restrict__ hb, float *__restrict__ uv) {
+    __shared__ uint16_t Ws[2][kRows][kLdsRow];
     __shared__ uint16_t Xs[16 * MT][kLdsRow];
-    const int a = blockIdx.y;
-    if (a >= G->n_act) return;
-    const int i0 = blockIdx.x * 64;
-    if (i0 >= I) return;
+    __shared__ int list[APEX_MAX_PAIRS];
+    __shared__ int cnt[APEX_MAX_PAIRS / kThreads][4];
+    const int e = blockIdx.y;
+    const int s = slot_of_expert[e];
+    if (s < 0 || s >= n_slots) return;
+    const int i0 = blockIdx.x * kRows;
+    const int n_e = expert_pairs(exec_idx, P, e, list, cnt);
+    if (n_e == 0) return;
+    int b_lo, b_hi;
+    split_range(d, gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int e = G->act_e[a];
-    const int beg = G->act_start[a], n_e = G->act_start[a + 1] - beg;
-    const uint16_t *W = slots + size_t(slot_of_expert[e]) * slot_elems + size_t(i0) * 2 * d;
+    const uint16_t *W = slots + size_t(s) * slot_elems + size_t(i0) * 2 * d;
     const uint16_t *const wbase[2] = {W, W + d};
-    const uint16_t *xs = reinterpret_cast<const uint16_t *>(xb);
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
-        const uint16_t *xrow[MT];
+        const void *xrow[MT];
         bool xok[MT];
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
             const int tok = t0 + (threadIdx.x >> 4) + 16 * j;
             xok[j] = tok < n_e;
-            xrow[j] = xs + size_t(G->item[beg + (xok[j] ? tok : 0)] / k) * d;
+            xrow[j] = x + size_t(list[xok[j] ? tok : 0] / k) * d;
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[2][MT];
-        gemm_mainloop<2, MT>(wbase, size_t(2) * d, I - i0, d, xrow, xok, n_tiles, Ws, Xs, acc);
+        gemm_mainloop<2, MT, ActF32>(wbase, size_t(2) * d, I - i0, d, b_lo, b_hi, xrow, xok, 0,
+                                     n_tiles, Ws, Xs, acc);
         const int i = i0 + 16 * wave + (lane & 15);
 #pragma unroll
         for (int tt = 0; tt < MT; ++tt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
-                if (tt < n_tiles && tok < n_e && i < I)
-                    hb[size_t(G->item[beg + tok]) * I + i] =
-                        (__bf16)(silu(acc[0][tt][r]) * acc[1][tt][r]);
+                if (tt < n_tiles && tok < n_e && i < I) {
+                    const size_t at = size_t(list[tok]) * I + i;
+                    if (SU == 1) {
+                        hb[at] = (__bf16)(silu(acc[0][tt][r]) * acc[1][tt][r]);
+                    } else {
+                        uv[size_t(2 * blockIdx.z) * P * I + at] = acc[0][tt][r];
+                        uv[size_t(2 * blockIdx.z + 1) * P * I + at] = acc[1][tt][r];
+                    }
+                }
             }
+        __syncthreads();   // LDS is reused by the next pass
     }
 }
 
-// down_gemm: grid (ceil(d / 64), max active experts): 64 rows j of W2 of one expert.
-// ypair[pair, j] = W2[j] . h[pair] for every token of the expert.
-template <int MT>
-__global__ __launch_bounds__(256) void down_gemm(
-    int d, int I, const GroupTable *__restrict__ G, const int32_t *__restrict__ slot_of_expert,
-    const uint16_t *__restrict__ slots, size_t slot_elems, const __bf16 *__restrict__ hb,
-    float *__restrict__ ypair) {
-    __shared__ uint16_t Ws[1][64][kLdsRow];
+// down_gemm: grid (ceil(d / 64), E, SD).  64 rows j of W2 of expert blockIdx.y, K (= I)
+// blocks of split blockIdx.z.  yp[z * P*d + pair*d + j] = W2[j] . h[pair] over the split.
+// The activations come from Act: bf16 h rows, or h formed from up_gemm's split partials.
+template <int MT, class Act>
+__global__ __launch_bounds__(kThreads) void down_gemm(
+    int d, int I, int P, const int32_t *__restrict__ exec_idx,
+    const int32_t *__restrict__ slot_of_expert, int n_slots, const uint16_t *__restrict__ slots,
+    size_t slot_elems, const void *__restrict__ act, size_t act_elem_bytes,
+    float *__restrict__ yp) {
+    __shared__ uint16_t Ws[1][kRows][kLdsRow];
     __shared__ uint16_t Xs[16 * MT][kLdsRow];
-    const int a = blockIdx.y;
-    if (a >= G->n_act) return;
-    const int j0 = blockIdx.x * 64;
-    if (j0 >= d) return;
+    __shared__ int list[APEX_MAX_PAIRS];
+    __shared__ int cnt[APEX_MAX_PAIRS / kThreads][4];
+    const int e = blockIdx.y;
+    const int s = slot_of_expert[e];
+    if (s < 0 || s >= n_slots) return;
+    const int j0 = blockIdx.x * kRows;
+    const int n_e = expert_pairs(exec_idx, P, e, list, cnt);
+    if (n_e == 0) return;
+    int b_lo, b_hi;
+    split_range(I, gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int e = G->act_e[a];
-    const int beg = G->act_start[a], n_e = G->act_start[a + 1] - beg;
-    const uint16_t *const wbase[1] = {slots + size_t(slot_of_expert[e]) * slot_elems +
-                                      size_t(2) * I * d + size_t(j0) * I};
-    const uint16_t *hs = reinterpret_cast<const uint16_t *>(hb);
+    const uint16_t *const wbase[1] = {slots + size_t(s) * slot_elems + size_t(2) * I * d +
+                                      size_t(j0) * I};
+    const char *ab = static_cast<const char *>(act);
+    float *out = yp + size_t(blockIdx.z) * P * d;
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
-        const uint16_t *hrow[MT];
+        const void *hrow[MT];
         bool hok[MT];
 #pragma unroll
         for (int j = 0; j < MT; ++j) {
             const int tok = t0 + (threadIdx.x >> 4) + 16 * j;
             hok[j] = tok < n_e;
-            hrow[j] = hs + size_t(G->item[beg + (hok[j] ? tok : 0)]) * I;
+            hrow[j] = ab + size_t(list[hok[j] ? tok : 0]) * I * act_elem_bytes;
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[1][MT];
-        gemm_mainloop<1, MT>(wbase, size_t(I), d - j0, I, hrow, hok, n_tiles, Ws, Xs, acc);
+        gemm_mainloop<1, MT, Act>(wbase, size_t(I), d - j0, I, b_lo, b_hi, hrow, hok,
+                                  size_t(P) * I, n_tiles, Ws, Xs, acc);
         const int j = j0 + 16 * wave + (lane & 15);
 #pragma unroll
         for (int tt = 0; tt < MT; ++tt)
@@ -292,21 +322,23 @@ __global__ __launch_bounds__(256) void down_gemm(
             for (int r = 0; r < 4; ++r) {
                 const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
                 if (tt < n_tiles && tok < n_e && j < d)
-                    ypair[size_t(G->item[beg + tok]) * d + j] = acc[0][tt][r];
+                    out[size_t(list[tok]) * d + j] = acc[0][tt][r];
             }
         __syncthreads();   // LDS is reused by the next pass
     }
 }
 
-// combine: y[b, j] (+)= sum over positions p of token b, in position order, of
-// gate[p] * ypair[p, j] for the pairs this pass executed.
-__global__ __launch_bounds__(256) void combine_pairs(
-    int B, int d, int E, int k, const int32_t *__restrict__ exec_idx,
+// combine: y[b, j] (+)= sum over positions q of token b, in position order, of
+// gate[q] * (sum over splits z, in order, of yp[z, pair, j]) for the pairs this pass
+// executed.
+__global__ __launch_bounds__(kThreads) void combine_pairs(
+    int B, int d, int E, int k, int SD, const int32_t *__restrict__ exec_idx,
     const float *__restrict__ exec_gate, const int32_t *__restrict__ slot_of_expert, int n_slots,
-    const float *__restrict__ ypair, float *__restrict__ y, int accumulate) {
+    const float *__restrict__ yp, float *__restrict__ y, int accumulate) {
     const int b = blockIdx.y;
-    const int j = blockIdx.x * 256 + threadIdx.x;
+    const int j = blockIdx.x * kThreads + threadIdx.x;
     if (b >= B || j >= d) return;
+    const size_t Pd = size_t(B) * k * d;
     float s = 0.f;
     for (int q = 0; q < k; ++q) {
         const int p = b * k + q;
@@ -314,21 +346,65 @@ __global__ __launch_bounds__(256) void combine_pairs(
         if (e < 0 || e >= E) continue;
         const int sl = slot_of_expert[e];
         if (sl < 0 || sl >= n_slots) continue;
-        s += exec_gate[p] * ypair[size_t(p) * d + j];
+        float v = 0.f;
+        for (int z = 0; z < SD; ++z) v += yp[z * Pd + size_t(p) * d + j];
+        s += exec_gate[p] * v;
     }
     float *dst = y + size_t(b) * d + j;
     *dst = (accumulate ? *dst : 0.f) + s;
+}
+
+// Splits for a projection with `tiles` row tiles per expert and K blocks `nb`: enough
+// workgroups for about four per compute unit over the experts that can run at once.
+int pick_splits(int tiles, int experts, int nb) {
+    constexpr int kTargetGroups = 1024;
+    const int groups = std::max(1, tiles * experts);
+    int s = (kTargetGroups + groups - 1) / groups;
+    s = std::min(s, kMaxSplit);
+    s = std::min(s, std::max(1, nb / 2));   // at least two K blocks per split
+    return std::max(s, 1);
+}
+
+struct Plan {
+    int MT, SU, SD;
+    size_t h_bytes, y_bytes;
+};
+
+Plan plan_for(int B, int d, int I, int k, int E, int n_slots) {
+    Plan pl;
+    // token tiles per pass: enough for the whole batch on one expert up to 64 tokens
+    pl.MT = B >= 48 ? 4 : (B >= 24 ? 2 : 1);
+    const int experts = std::min(std::min(E, B * k), n_slots);
+    const int nb_d = (d + kKB - 1) / kKB, nb_i = (I + kKB - 1) / kKB;
+    pl.SU = pl.MT == 1 ? pick_splits((I + kRows - 1) / kRows, experts, nb_d) : 1;
+    pl.SD = pick_splits((d + kRows - 1) / kRows, experts, nb_i);
+    const size_t P = size_t(B) * k;
+    pl.h_bytes = pl.SU == 1 ? P * I * 2 : size_t(2) * pl.SU * P * I * sizeof(float);
+    pl.y_bytes = size_t(pl.SD) * P * d * sizeof(float);
+    return pl;
+}
+
+template <int MT, int SU>
+void launch_up(dim3 g, hipStream_t st, const float *x, int d, int I, int P, int k,
+               const int32_t *exec_idx, const int32_t *soe, int n_slots, const uint16_t *slots,
+               size_t se, __bf16 *hb, float *uv) {
+    hipLaunchKernelGGL((up_gemm<MT, SU>), g, dim3(kThreads), 0, st, x, d, I, P, k, exec_idx, soe,
+                       n_slots, slots, se, hb, uv);
 }
 
 }  // namespace
 
 namespace apex {
 
-// [GroupTable][h: B*k x I bf16][per-pair outputs: B*k x d fp32][x: B x d bf16]
+// [h: bf16 B*k x I, or 2*SU fp32 partials][per-split, per-pair outputs: SD x B*k x d fp32]
 size_t ffn_grouped_workspace(int B, int d, int I, int k) {
-    const size_t P = size_t(B) * k;
-    return align_up(sizeof(GroupTable), 256) + align_up(P * I * 2, 256) +
-           align_up(P * d * sizeof(float), 256) + align_up(size_t(B) * d * 2, 256);
+    // the largest plan over the slot counts the call can be given
+    size_t worst = 0;
+    for (int experts = 1; experts <= APEX_MAX_EXPERTS; ++experts) {
+        const Plan pl = plan_for(B, d, I, k, APEX_MAX_EXPERTS, experts);
+        worst = std::max(worst, align_up(pl.h_bytes, 256) + align_up(pl.y_bytes, 256));
+    }
+    return worst;
 }
 
 apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
@@ -336,43 +412,50 @@ apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,
                         float *y, int accumulate, void *workspace, hipStream_t stream) {
     const int P = B * k;
-    const size_t slot_elems = size_t(3) * d * I;
-    const int max_act = P < E ? P : E;
+    const size_t se = size_t(3) * d * I;
+    const Plan pl = plan_for(B, d, I, k, E, n_slots);
     char *wsb = static_cast<char *>(workspace);
-    GroupTable *G = reinterpret_cast<GroupTable *>(wsb);
-    __bf16 *hb = reinterpret_cast<__bf16 *>(wsb + align_up(sizeof(GroupTable), 256));
-    char *after_h = reinterpret_cast<char *>(hb) + align_up(size_t(P) * I * 2, 256);
-    float *ypair = reinterpret_cast<float *>(after_h);
-    __bf16 *xb = reinterpret_cast<__bf16 *>(after_h + align_up(size_t(P) * d * sizeof(float), 256));
-    const size_t n8 = size_t(B) * d / 8;
-    const unsigned conv_blocks = unsigned(std::min<size_t>(64, (n8 + kGroupThreads - 1) / kGroupThreads));
-    hipLaunchKernelGGL(group_pairs, dim3(conv_blocks), dim3(kGroupThreads), 0, stream,
-                       exec_idx, slot_of_expert, P, E, n_slots, G, x, B, d, xb);
+    __bf16 *hb = reinterpret_cast<__bf16 *>(wsb);
+    float *uv = reinterpret_cast<float *>(wsb);
+    float *yp = reinterpret_cast<float *>(wsb + align_up(pl.h_bytes, 256));
+
+    const dim3 gu((I + kRows - 1) / kRows, E, pl.SU);
+    if (pl.MT == 4)
+        launch_up<4, 1>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
+    else if (pl.MT == 2)
+        launch_up<2, 1>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
+    else if (pl.SU == 1)
+        launch_up<1, 1>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
+    else if (pl.SU == 2)
+        launch_up<1, 2>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
+    else if (pl.SU == 3)
+        launch_up<1, 3>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
+    else
+        launch_up<1, 4>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
     APEX_HIP(hipGetLastError());
-    const dim3 gu((I + 63) / 64, max_act), gd((d + 63) / 64, max_act);
-    // token tiles per pass: enough for the whole batch on one expert up to 64 tokens
-    if (B >= 48) {
-        hipLaunchKernelGGL((up_gemm<4>), gu, dim3(256), 0, stream, xb, d, I, k, G,
-                           slot_of_expert, slots, slot_elems, hb);
-        APEX_HIP(hipGetLastError());
-        hipLaunchKernelGGL((down_gemm<4>), gd, dim3(256), 0, stream, d, I, G,
-                           slot_of_expert, slots, slot_elems, hb, ypair);
-    } else if (B >= 24) {
-        hipLaunchKernelGGL((up_gemm<2>), gu, dim3(256), 0, stream, xb, d, I, k, G,
-                           slot_of_expert, slots, slot_elems, hb);
-        APEX_HIP(hipGetLastError());
-        hipLaunchKernelGGL((down_gemm<2>), gd, dim3(256), 0, stream, d, I, G,
-                           slot_of_expert, slots, slot_elems, hb, ypair);
-    } else {
-        hipLaunchKernelGGL((up_gemm<1>), gu, dim3(256), 0, stream, xb, d, I, k, G,
-                           slot_of_expert, slots, slot_elems, hb);
-        APEX_HIP(hipGetLastError());
-        hipLaunchKernelGGL((down_gemm<1>), gd, dim3(256), 0, stream, d, I, G,
-                           slot_of_expert, slots, slot_elems, hb, ypair);
-    }
+
+    const dim3 gd((d + kRows - 1) / kRows, E, pl.SD);
+    const void *act = pl.SU == 1 ? static_cast<const void *>(hb) : static_cast<const void *>(uv);
+#define APEX_DOWN(MT_, ACT_, EB_)                                                           \
+    hipLaunchKernelGGL((down_gemm<MT_, ACT_>), gd, dim3(kThreads), 0, stream, d, I, P, exec_idx, \
+                       slot_of_expert, n_slots, slots, se, act, size_t(EB_), yp)
+    if (pl.MT == 4)
+        APEX_DOWN(4, ActBf16, 2);
+    else if (pl.MT == 2)
+        APEX_DOWN(2, ActBf16, 2);
+    else if (pl.SU == 1)
+        APEX_DOWN(1, ActBf16, 2);
+    else if (pl.SU == 2)
+        APEX_DOWN(1, ActSwiglu<2>, 4);
+    else if (pl.SU == 3)
+        APEX_DOWN(1, ActSwiglu<3>, 4);
+    else
+        APEX_DOWN(1, ActSwiglu<4>, 4);
+#undef APEX_DOWN
     APEX_HIP(hipGetLastError());
-    hipLaunchKernelGGL(combine_pairs, dim3((d + 255) / 256, B), dim3(256), 0, stream, B, d, E,
-                       k, exec_idx, exec_gate, slot_of_expert, n_slots, ypair, y, accumulate);
+    hipLaunchKernelGGL(combine_pairs, dim3((d + kThreads - 1) / kThreads, B), dim3(kThreads), 0,
+                       stream, B, d, E, k, pl.SD, exec_idx, exec_gate, slot_of_expert, n_slots, yp,
+                       y, accumulate);
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }

@@ -282,6 +282,10 @@ MFMA_SHAPES = [
     (shape("mfma_b48", 411, 512, 6, 2, I=256), 48),       # four token tiles per pass
     (shape("mfma_b16", 412, 1024, 32, 8, I=512), 16),     # one tile per pass
     (shape("mfma_b2", 415, 1024, 32, 8, I=512), 2),       # smallest batch on this path
+    # four experts, so both projections split K: up over 3 splits and down over 4, then
+    # up over 4 and down over 3; ragged K tails on both sides
+    (shape("mfma_split_a", 416, 776, 4, 2, I=1000), 4),
+    (shape("mfma_split_b", 417, 1000, 4, 2, I=776), 5),
 ]
 
 
