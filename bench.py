@@ -12,7 +12,7 @@ timeline with the attention-window stand-in subtracted (the MoE path's own cost
 including exposed stall); lower is better.
 
     python bench.py [--steps K] [--warmup W] [--config granite-1b-a400m] [--batch 1]
-                    [--mode exact|stall_free] [--policy cumprob|ordinal|static]
+                    [--mode exact|stall_free] [--policy cumprob|ordinal|static|none]
                     [--static-delta D] [--tau T] [--t-attn-us 10] [--no-cpu-baseline]
 
 With --policy ordinal, every layer's coverage model is first fitted on held-out tokens
@@ -45,7 +45,8 @@ def parse():
     p.add_argument("--batch", type=int, default=1)
     p.add_argument("--mode", default="exact", choices=["exact", "stall_free"])
     p.add_argument("--tau", type=float, default=None)
-    p.add_argument("--policy", default="cumprob", choices=["cumprob", "ordinal", "static"])
+    p.add_argument("--policy", default="cumprob",
+                   choices=["cumprob", "ordinal", "static", "none"])
     p.add_argument("--static-delta", type=int, default=0)
     p.add_argument("--cdf-tokens", type=int, default=1024,
                    help="held-out tokens per layer for the ordinal-model fit")
@@ -199,7 +200,7 @@ def main():
     mode = EXACT if args.mode == "exact" else STALL_FREE
     tau = cfg.tau if args.tau is None else args.tau
     policy = {"cumprob": native.SEL_CUMPROB, "ordinal": native.SEL_ORDINAL_CDF,
-              "static": native.SEL_STATIC}[args.policy]
+              "static": native.SEL_STATIC, "none": native.SEL_NONE}[args.policy]
     cdf, cdf_report = None, None
     if policy == native.SEL_ORDINAL_CDF:
         from paper_2608_11688_amd import cdf_fit
@@ -252,7 +253,7 @@ def main():
         "ffn_hbm_GBps": round(achieved, 1),
         "recall": round(s["recall"], 5),
         "full_coverage": round(s["full_coverage"], 5),
-        "mean_delta_hat": round(s["mean_delta_hat"], 4),
+        "mean_delta_hat": None if args.policy == "none" else round(s["mean_delta_hat"], 4),
         "cache_hit_rate": round(s["hit_rate"], 5),
         "copies_per_layer_step": round(s["copies_per_layer_step"], 4),
         "misses_per_layer_step": round(s["misses_per_layer_step"], 4),

@@ -59,7 +59,10 @@ typedef enum {
                                  sum to >= tau, clamped to [k, k_max]               */
     APEX_SEL_ORDINAL_CDF = 1, /* Eq. 8-9: delta_hat = min{delta : sigmoid(theta_delta
                                  - w.x) >= tau}, m = min(k + delta_hat, k_max)      */
-    APEX_SEL_STATIC = 2       /* m = min(k + static_delta, k_max) (static over-fetch) */
+    APEX_SEL_STATIC = 2,      /* m = min(k + static_delta, k_max) (static over-fetch) */
+    APEX_SEL_NONE = 3         /* no prefetch, the No-Prefetch baseline of Sec. V-A: m = 0
+                                 and pf_idx is all -1.  apex_decode_step does not run
+                                 the prefetch router at all under this policy.       */
 } apex_policy;
 
 /* Execution mode of apex_gate_topk (Sec. IV-E). */

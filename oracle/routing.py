@@ -12,6 +12,8 @@ Paper passages followed:
 * Cumulative-probability rule of the workload definitions: take experts in ranked
   order until their prefetch probabilities sum to at least tau, clamped to [k, k_max].
 * Static over-fetch baseline (Sec. V-A): delta fixed for every token.
+* No-Prefetch baseline (Sec. V-A): nothing is prefetched; every routed expert that is
+  not already resident is loaded after the gate.
 
 Readings (where the paper is silent): equal scores rank the lower expert id first;
 the ordinal model's input x is the prefetch probability vector sorted in descending
@@ -27,7 +29,7 @@ import numpy as np
 
 from .bf16 import bf16_to_f64
 
-CUMPROB, ORDINAL_CDF, STATIC = 0, 1, 2
+CUMPROB, ORDINAL_CDF, STATIC, NONE = 0, 1, 2, 3
 
 
 def router_logits(h: np.ndarray, w_bits: np.ndarray, bias=None) -> np.ndarray:
@@ -138,6 +140,8 @@ def prefetch_route(h_pre, w_pf_bits, b_pf, k, k_max, policy=CUMPROB, tau=0.9,
             m, _, mg = select_ordinal(q_ranked, cdf_w, cdf_theta, k, k_max, tau)
         elif policy == STATIC:
             m, mg = select_static(k, k_max, static_delta, E), math.inf
+        elif policy == NONE:
+            m, mg = 0, math.inf
         else:
             raise ValueError(f"unknown policy {policy}")
         # ordering and cut of the ranked prefix: logit gaps of adjacent entries

@@ -178,17 +178,26 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
     for (int l = 0; l < c.L; ++l) {
         const apex_decode_layer &Ly = dec->layers[l];
         // prefetch stage: router on the pre-attention state, then the attention window
-        st = apex_prefetch_route(h_pre[l], Ly.w_pf, Ly.b_pf, c.B, c.d, c.E, c.k, c.k_max,
-                                 c.policy, c.tau, c.static_delta, Ly.cdf_w, Ly.cdf_theta,
-                                 dec->pf_idx_h, dec->pf_count_h, nullptr, cs);
-        if (st != APEX_OK) return st;
-        APEX_HIP(hipEventRecord(dec->ev_route, cs));
+        // (the no-prefetch baseline has no router: its prefetched sets are empty)
+        const bool route = c.policy != APEX_SEL_NONE;
+        if (route) {
+            st = apex_prefetch_route(h_pre[l], Ly.w_pf, Ly.b_pf, c.B, c.d, c.E, c.k, c.k_max,
+                                     c.policy, c.tau, c.static_delta, Ly.cdf_w, Ly.cdf_theta,
+                                     dec->pf_idx_h, dec->pf_count_h, nullptr, cs);
+            if (st != APEX_OK) return st;
+            APEX_HIP(hipEventRecord(dec->ev_route, cs));
+        } else {
+            std::fill(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max, -1);
+            std::fill(dec->pf_count_h, dec->pf_count_h + c.B, 0);
+        }
         if (c.t_attn_us > 0) {
             st = apex_spin_us(c.t_attn_us, cs);
             if (st != APEX_OK) return st;
         }
-        st = poll(dec->ev_route);
-        if (st != APEX_OK) return st;
+        if (route) {
+            st = poll(dec->ev_route);
+            if (st != APEX_OK) return st;
+        }
         // earlier layers' gates precede this route on the stream: fold their statistics
         fold_pending(dec, stats);
         int n_copy = 0;

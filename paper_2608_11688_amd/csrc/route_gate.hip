@@ -151,8 +151,10 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
         const unsigned long long hit = __ballot(ok);
         const int delta_hat = hit ? __ffsll(static_cast<long long>(hit)) - 1 : E - k;
         m = min(k + delta_hat, k_max);
-    } else {
+    } else if (policy == APEX_SEL_STATIC) {
         m = min(k + static_delta, k_max);
+    } else {
+        m = 0;   // APEX_SEL_NONE
     }
     if (lane < k_max) pf_idx[size_t(b) * k_max + lane] = lane < m ? sorted_id[lane] : -1;
     if (lane == 0) pf_count[b] = m;
@@ -241,9 +243,10 @@ extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w
     if (st != APEX_OK) return st;
     APEX_REQUIRE(k_max >= k && k_max <= E, "%s: k_max=%d out of [k=%d, E=%d]", fn, k_max, k, E);
     APEX_REQUIRE(policy == APEX_SEL_CUMPROB || policy == APEX_SEL_ORDINAL_CDF ||
-                     policy == APEX_SEL_STATIC,
+                     policy == APEX_SEL_STATIC || policy == APEX_SEL_NONE,
                  "%s: unknown policy %d", fn, policy);
-    APEX_REQUIRE(policy == APEX_SEL_STATIC || (tau >= 0.f && tau <= 1.f),
+    APEX_REQUIRE(policy == APEX_SEL_STATIC || policy == APEX_SEL_NONE ||
+                     (tau >= 0.f && tau <= 1.f),
                  "%s: tau=%g out of [0, 1]", fn, double(tau));
     APEX_REQUIRE(policy != APEX_SEL_STATIC || static_delta >= 0, "%s: static_delta=%d < 0", fn,
                  static_delta);

@@ -21,7 +21,7 @@ LIB_PATH = os.path.join(PKG, "libapex.so")
 PLAN_LIB_PATH = os.path.join(PKG, "libapex_plan.so")
 
 APEX_OK, APEX_E_INVAL, APEX_E_UNSUPPORTED, APEX_E_HIP, APEX_E_CAPACITY = 0, -1, -2, -3, -4
-SEL_CUMPROB, SEL_ORDINAL_CDF, SEL_STATIC = 0, 1, 2
+SEL_CUMPROB, SEL_ORDINAL_CDF, SEL_STATIC, SEL_NONE = 0, 1, 2, 3
 MODE_EXACT, MODE_STALL_FREE = 0, 1
 MAX_EXPERTS = 64
 MAX_PAIRS = 1024

@@ -83,6 +83,17 @@ def test_decode_tiny_all_steps(mode):
     assert st["copies"] > 0
 
 
+@pytest.mark.parametrize("mode", [native.MODE_EXACT, native.MODE_STALL_FREE])
+def test_decode_no_prefetch_baseline(mode):
+    # nothing is prefetched: the cache keeps its initial experts, exact mode loads every
+    # other routed expert after the gate, stall-free mode runs on the initial experts
+    cfg = configs.GRANITE_1B
+    st = check_decode(cfg, 1, mode, 6, [0, 13], policy=native.SEL_NONE)
+    assert st["copies"] == 0 and st["covered"] == 0
+    if mode == native.MODE_EXACT:
+        assert st["misses"] > 0
+
+
 def test_decode_granite1b_exact():
     cfg = configs.GRANITE_1B
     st = check_decode(cfg, 1, native.MODE_EXACT, 4, list(range(cfg.L)), ffn_every=3)

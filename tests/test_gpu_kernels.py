@@ -84,6 +84,7 @@ def test_route_configs_all_policies(torch, name):
                 ledger=ledger)
     check_route(torch, cfg, h, native.SEL_STATIC, 0.0, sd=2, ledger=ledger)
     check_route(torch, cfg, h, native.SEL_STATIC, 0.0, sd=0, ledger=ledger)
+    check_route(torch, cfg, h, native.SEL_NONE, 0.0, ledger=ledger)
     print(name, ledger)
 
 

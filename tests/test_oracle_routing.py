@@ -14,6 +14,7 @@ import pytest
 import scipy.special
 
 from oracle import routing
+from paper_2608_11688_amd import configs, inputs
 from paper_2608_11688_amd.inputs import to_bf16_bits
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -195,3 +196,27 @@ def test_overhead_table_parameter_counts():
         per_hidden_w = L * (d * N + d + (N - k + 1))
         assert round(per_expert_w / 1e6, 2) == row["printed_millions"]
         assert round(per_hidden_w / 1e6, 2) != row["printed_millions"]
+
+
+def test_no_prefetch_policy_selects_nothing():
+    cfg = configs.GRANITE_1B
+    h = inputs.hidden_states(cfg, 0, 4, 1)[0][0]
+    wg, wpf, bias = inputs.router_weights(cfg, 0)
+    r = routing.prefetch_route(h, wpf, bias, cfg.k, cfg.k_max, routing.NONE)
+    assert (r["pf_count"] == 0).all() and (r["pf_idx"] == -1).all()
+    # the ranked list is still reported
+    assert sorted(r["ranked"][0].tolist()) == list(range(cfg.E))
+
+
+def test_no_prefetch_decode_keeps_the_initial_cache():
+    from oracle import decode, gating
+    cfg = configs.TINY
+    seen = []
+    for t, l, out in decode.run(cfg, 1, 12, mode=gating.EXACT, policy=routing.NONE,
+                                run_ffn=False):
+        assert out["copies"] == []
+        assert sorted(out["resident"]) == list(range(cfg.C))
+        routed = set(int(e) for e in out["gate"]["route_idx"][0])
+        assert sorted(out["misses"]) == sorted(routed - set(range(cfg.C)))
+        seen.append(len(out["misses"]))
+    assert sum(seen) > 0
