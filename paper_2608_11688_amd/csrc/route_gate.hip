@@ -2,7 +2,8 @@
 //
 // One workgroup of 16 wavefronts per token.  Every wavefront streams whole rows of the
 // bf16 router matrix with 16-byte loads (up to 4 experts at a time, sharing each read of
-// the hidden state) and reduces its dot products with cross-lane shuffles.  Softmax,
+// the hidden state, all loads of a row issued together up to d = 2048) and reduces its
+// dot products with cross-lane shuffles.  Softmax,
 // ranking and the selection rules then run in wavefront 0 with one lane per expert
 // (E <= 64), exchanging values through registers (readlane, shuffles, ballots).
 #include <hip/hip_runtime.h>
@@ -16,7 +17,6 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kExpertsPerPass = 4;
 constexpr int kMaxD = 65536;
 
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -47,33 +47,46 @@ __device__ __forceinline__ float wave_max(float v) {
 }
 
 // z[e] = W[e, :] . h (+ bias[e]) for all experts, into LDS.  All threads call it.
-// The hidden state is read straight from global memory (every wavefront reads the same
-// chunks, so after the first they hit the vector cache); no load waits on another.
+// Wavefront w takes experts w, w + 16, ... (EPP of them).  A pass covers NC 16-byte
+// chunks per lane (64 * NC * 8 elements of d), and every load of a pass, weights and
+// hidden state, is issued before the first multiply, so d <= 512 * NC costs one memory
+// round trip.  The hidden state is read straight from global memory (every wavefront
+// reads the same chunks, so after the first they hit the vector cache).
+template <int NC, int EPP>
 __device__ void token_logits(const float *__restrict__ h, const uint16_t *__restrict__ W,
                              const float *__restrict__ bias, int d, int E, float *z_lds) {
     const float4 *h4 = reinterpret_cast<const float4 *>(h);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int nch = d / 8;
-    for (int e0 = wave; e0 < E; e0 += kWaves * kExpertsPerPass) {
-        float acc[kExpertsPerPass] = {0.f, 0.f, 0.f, 0.f};
-        const uint4 *rows[kExpertsPerPass];
+    for (int e0 = wave; e0 < E; e0 += kWaves * EPP) {
+        float acc[EPP];
+        const uint4 *rows[EPP];
 #pragma unroll
-        for (int u = 0; u < kExpertsPerPass; ++u) {
+        for (int u = 0; u < EPP; ++u) {
+            acc[u] = 0.f;
             const int e = e0 + u * kWaves;
             rows[u] = reinterpret_cast<const uint4 *>(W + size_t(e < E ? e : 0) * d);
         }
-        for (int c = lane; c < nch; c += kWave) {
-            uint4 w[kExpertsPerPass];
+        for (int c0 = 0; c0 < nch; c0 += kWave * NC) {
+            uint4 w[EPP][NC];
+            float4 a[NC], b[NC];
 #pragma unroll
-            for (int u = 0; u < kExpertsPerPass; ++u)
-                if (e0 + u * kWaves < E) w[u] = rows[u][c];
-            const float4 a = h4[2 * c], b = h4[2 * c + 1];
+            for (int n = 0; n < NC; ++n) {
+                const int c = min(c0 + lane + n * kWave, nch - 1);
+                a[n] = h4[2 * c];
+                b[n] = h4[2 * c + 1];
 #pragma unroll
-            for (int u = 0; u < kExpertsPerPass; ++u)
-                if (e0 + u * kWaves < E) acc[u] = dot8(w[u], a, b, acc[u]);
+                for (int u = 0; u < EPP; ++u) w[u][n] = rows[u][c];   // rows past E repeat row 0
+            }
+#pragma unroll
+            for (int n = 0; n < NC; ++n)
+                if (c0 + lane + n * kWave < nch)
+#pragma unroll
+                    for (int u = 0; u < EPP; ++u)
+                        if (e0 + u * kWaves < E) acc[u] = dot8(w[u][n], a[n], b[n], acc[u]);
         }
 #pragma unroll
-        for (int u = 0; u < kExpertsPerPass; ++u) {
+        for (int u = 0; u < EPP; ++u) {
             const int e = e0 + u * kWaves;
             const float s = wave_sum(acc[u]);
             if (lane == 0 && e < E) z_lds[e] = s + (bias ? bias[e] : 0.f);
@@ -102,6 +115,7 @@ __device__ __forceinline__ float logit_of(float tau) {
     return logf(tau / (1.f - tau));
 }
 
+template <int NC, int EPP>
 __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     const float *__restrict__ h_pre, const uint16_t *__restrict__ w_pf,
     const float *__restrict__ b_pf, int d, int E, int k, int k_max, int policy, float tau,
@@ -112,7 +126,7 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     __shared__ int sorted_id[APEX_MAX_EXPERTS];
 
     const int b = blockIdx.x;
-    token_logits(h_pre + size_t(b) * d, w_pf, b_pf, d, E, z_lds);
+    token_logits<NC, EPP>(h_pre + size_t(b) * d, w_pf, b_pf, d, E, z_lds);
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     if (wave != 0) return;   // selection is one wavefront's work; no barriers follow
@@ -161,6 +175,7 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     if (pf_prob && live) pf_prob[size_t(b) * E + lane] = q;
 }
 
+template <int NC, int EPP>
 __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     const float *__restrict__ h_post, const uint16_t *__restrict__ w_g,
     const float *__restrict__ b_g, int d, int E, int k, int mode,
@@ -170,7 +185,7 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     __shared__ float z_lds[APEX_MAX_EXPERTS];
 
     const int b = blockIdx.x;
-    token_logits(h_post + size_t(b) * d, w_g, b_g, d, E, z_lds);
+    token_logits<NC, EPP>(h_post + size_t(b) * d, w_g, b_g, d, E, z_lds);
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     if (wave != 0) return;
@@ -214,6 +229,21 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     if (gate_prob && live) gate_prob[size_t(b) * E + lane] = p / psum;
 }
 
+// Shape of token_logits: experts per wavefront (1, 2 or 4 for E <= 16, 32, 64) and
+// 16-byte chunks per lane per pass (1, 2 or 4; one pass up to d = 2048), with the
+// staged loads of a pass, (EPP + 2) * NC * 4 registers, kept within the 128 registers a
+// lane has in a 1024-thread workgroup.
+struct LogitShape {
+    int nc, epp;
+};
+LogitShape logit_shape(int d, int E) {
+    const int nch = d / 8;
+    const int epp = E <= kWaves ? 1 : (E <= 2 * kWaves ? 2 : 4);
+    int nc = nch <= kWave ? 1 : (nch <= 2 * kWave ? 2 : 4);
+    if (epp == 4 && nc == 4) nc = 2;
+    return {nc, epp};
+}
+
 apex_status check_router_args(const char *fn, const float *h, const uint16_t *w, int B, int d,
                               int E, int k) {
     APEX_REQUIRE(B >= 0, "%s: B=%d must be >= 0", fn, B);
@@ -254,9 +284,24 @@ extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w
                  "%s: ORDINAL_CDF needs cdf_w and cdf_theta", fn);
     if (B == 0) return APEX_OK;
     APEX_REQUIRE(pf_idx && pf_count, "%s: NULL output pointer", fn);
-    hipLaunchKernelGGL(prefetch_route_kernel, dim3(B), dim3(kThreads), 0,
-                       stream, h_pre, w_pf, b_pf, d, E, k, k_max, policy, tau, static_delta,
-                       cdf_w, cdf_theta, pf_idx, pf_count, pf_prob);
+#define APEX_ROUTE(NC_, EPP_)                                                              \
+    hipLaunchKernelGGL((prefetch_route_kernel<NC_, EPP_>), dim3(B), dim3(kThreads), 0, stream,  \
+                       h_pre, w_pf, b_pf, d, E, k, k_max, policy, tau, static_delta, cdf_w,    \
+                       cdf_theta, pf_idx, pf_count, pf_prob)
+    const LogitShape sh = logit_shape(d, E);
+    if (sh.epp == 1) {
+        if (sh.nc == 1) APEX_ROUTE(1, 1);
+        else if (sh.nc == 2) APEX_ROUTE(2, 1);
+        else APEX_ROUTE(4, 1);
+    } else if (sh.epp == 2) {
+        if (sh.nc == 1) APEX_ROUTE(1, 2);
+        else if (sh.nc == 2) APEX_ROUTE(2, 2);
+        else APEX_ROUTE(4, 2);
+    } else {
+        if (sh.nc == 1) APEX_ROUTE(1, 4);
+        else APEX_ROUTE(2, 4);
+    }
+#undef APEX_ROUTE
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }
@@ -278,9 +323,24 @@ extern "C" apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, 
     }
     if (B == 0) return APEX_OK;
     APEX_REQUIRE(route_idx && route_gate && exec_idx && exec_gate, "%s: NULL output pointer", fn);
-    hipLaunchKernelGGL(gate_topk_kernel, dim3(B), dim3(kThreads), 0,
-                       stream, h_post, w_g, b_g, d, E, k, mode, avail, avail_stride, route_idx,
-                       route_gate, exec_idx, exec_gate, gate_prob);
+#define APEX_GATE(NC_, EPP_)                                                               \
+    hipLaunchKernelGGL((gate_topk_kernel<NC_, EPP_>), dim3(B), dim3(kThreads), 0, stream,       \
+                       h_post, w_g, b_g, d, E, k, mode, avail, avail_stride, route_idx,        \
+                       route_gate, exec_idx, exec_gate, gate_prob)
+    const LogitShape sh = logit_shape(d, E);
+    if (sh.epp == 1) {
+        if (sh.nc == 1) APEX_GATE(1, 1);
+        else if (sh.nc == 2) APEX_GATE(2, 1);
+        else APEX_GATE(4, 1);
+    } else if (sh.epp == 2) {
+        if (sh.nc == 1) APEX_GATE(1, 2);
+        else if (sh.nc == 2) APEX_GATE(2, 2);
+        else APEX_GATE(4, 2);
+    } else {
+        if (sh.nc == 1) APEX_GATE(1, 4);
+        else APEX_GATE(2, 4);
+    }
+#undef APEX_GATE
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }

@@ -123,3 +123,23 @@ def test_decode_granite1b_ordinal_fitted_model():
     print(report, st)
     # calibrated at tau = 0.9 on held-out tokens: most of these tokens are fully covered
     assert st["covered"] >= 0.6 * st["tokens"]
+
+
+def test_decode_every_expert_resident():
+    # C = E: the cache holds every expert from the start, so nothing is ever copied or
+    # missed, and stall-free mode executes exactly the routed sets
+    cfg = configs.MoEConfig("all_resident", 420, L=2, d=256, E=8, k=2, I=128, C=8, k_max=8,
+                            tau=0.9, steps=12)
+    for mode in (native.MODE_EXACT, native.MODE_STALL_FREE):
+        st = check_decode(cfg, 2, mode, 12, [0, 1])
+        assert st["copies"] == 0 and st["misses"] == 0
+
+
+def test_decode_every_expert_routed():
+    # k = E: every token routes to every expert; the prefetched set is the whole list
+    # (m is clamped to k = k_max = E), so every token is fully covered
+    cfg = configs.MoEConfig("all_routed", 421, L=1, d=264, E=4, k=4, I=136, C=4, k_max=4,
+                            tau=0.5, steps=10)
+    for mode in (native.MODE_EXACT, native.MODE_STALL_FREE):
+        st = check_decode(cfg, 3, mode, 10, [0])
+        assert st["covered"] == st["tokens"] and st["copies"] == 0
