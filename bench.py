@@ -13,7 +13,8 @@ including exposed stall); lower is better.
 
     python bench.py [--steps K] [--warmup W] [--config granite-1b-a400m] [--batch 1]
                     [--mode exact|stall_free] [--policy cumprob|ordinal|static|none]
-                    [--static-delta D] [--tau T] [--t-attn-us 10] [--no-cpu-baseline]
+                    [--static-delta D] [--tau T] [--weights bf16|fp8] [--t-attn-us 10]
+                    [--no-cpu-baseline]
 
 With --policy ordinal, every layer's coverage model is first fitted on held-out tokens
 (the method's training stage, outside the timed region).
@@ -33,7 +34,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 FFN_KERNELS = {True: "apex_moe_ffn (up_b1 + down_b1)",
-               False: "apex_moe_ffn (group_pairs + up_gemm + down_gemm + combine_pairs)"}
+               False: "apex_moe_ffn (up_gemm + down_gemm + combine_pairs)"}
 
 
 def parse():
@@ -48,6 +49,8 @@ def parse():
     p.add_argument("--policy", default="cumprob",
                    choices=["cumprob", "ordinal", "static", "none"])
     p.add_argument("--static-delta", type=int, default=0)
+    p.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
+                   help="expert weight format (fp8: E4M3 with fp32 row scales)")
     p.add_argument("--cdf-tokens", type=int, default=1024,
                    help="held-out tokens per layer for the ordinal-model fit")
     p.add_argument("--t-attn-us", type=float, default=10.0)
@@ -97,12 +100,13 @@ def ffn_roofline_leg(torch, native, runner, reps=8, seed=123):
     y = torch.empty((B, cfg.d), dtype=torch.float32, device="cuda")
     e0, e1 = native.apex_event_create(True), native.apex_event_create(True)
     torch.cuda.synchronize()
+    ffn = native.apex_moe_ffn_fp8 if runner.weights == "fp8" else native.apex_moe_ffn
     native.apex_spin_us(min(5000.0 + 50.0 * n, 1e6), cs)
     native.apex_event_record(e0, cs)
     for i in range(n):
         b, idx, gate, _ = plan[i % len(plan)]
-        native.apex_moe_ffn(b["h_post"][0], B, cfg.d, cfg.I, cfg.E, k, idx, gate, b["slot_dev"],
-                            b["slots"], cfg.C, y, 0, runner.ws, runner.ws_bytes, cs)
+        ffn(b["h_post"][0], B, cfg.d, cfg.I, cfg.E, k, idx, gate, b["slot_dev"], b["slots"],
+            cfg.C, y, 0, runner.ws, runner.ws_bytes, cs)
     native.apex_event_record(e1, cs)
     native.apex_event_synchronize(e1)
     ms = native.apex_event_elapsed_ms(e0, e1) / n
@@ -133,7 +137,7 @@ def copy_calibration(torch, native, cs, nbytes=256 << 20, reps=5):
                 GBps_read_plus_write=round(2 * nbytes / (ms * 1e-3) / 1e9, 1))
 
 
-def measured_traffic(cfg, batch):
+def measured_traffic(cfg, batch, weights="bf16"):
     """HBM bytes per apex_moe_ffn call from the committed FETCH_SIZE / WRITE_SIZE records,
     or None when no record is for this workload and batch, or the source of the kernels
     it covers has changed since the counters were taken."""
@@ -144,7 +148,8 @@ def measured_traffic(cfg, batch):
     except (OSError, KeyError, ValueError):
         return None
     for rec in records:
-        if rec.get("workload") != cfg.name or rec.get("batch") != batch:
+        if (rec.get("workload") != cfg.name or rec.get("batch") != batch or
+                rec.get("weights", "bf16") != weights):
             continue
         try:
             src = open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()
@@ -156,7 +161,8 @@ def measured_traffic(cfg, batch):
     return None
 
 
-def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=None):
+def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=None,
+                 weights="bf16"):
     """The oracle, as it stands, on the first layer-steps of the same workload."""
     from oracle import decode
     try:
@@ -168,7 +174,7 @@ def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=
     layers = list(range(min(cfg.L, 4)))
     steps = 64
     gen = decode.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers, policy=policy,
-                     static_delta=static_delta, cdf=cdf)
+                     static_delta=static_delta, cdf=cdf, weights=weights)
     # timed as the oracle runs: its seeded input generation is inside the sample
     n, elapsed = 0, 0.0
     it = iter(gen)
@@ -208,7 +214,7 @@ def main():
     total = args.warmup + args.steps
     runner = DecodeRunner(cfg, batch=args.batch, mode=mode, tau=tau, steps=max(total, 1),
                           t_attn_us=args.t_attn_us, policy=policy,
-                          static_delta=args.static_delta, cdf=cdf)
+                          static_delta=args.static_delta, cdf=cdf, weights=args.weights)
     h2d_peak = pinned_h2d_peak(torch)
 
     for _ in range(args.warmup):
@@ -243,11 +249,13 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 weights, fp32 accumulate",
+        "dtype": ("fp8 e4m3 weights with fp32 row scales, fp32 accumulate"
+                  if args.weights == "fp8" else "bf16 weights, fp32 accumulate"),
         "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) bf16 experts)",
         "config": {"workload": cfg.name, "layers": L, "d": cfg.d, "E": cfg.E, "k": cfg.k,
                    "I": cfg.I, "C": cfg.C, "k_max": cfg.k_max, "tau": tau, "batch": B,
-                   "mode": args.mode, "policy": args.policy, "t_attn_us": args.t_attn_us},
+                   "mode": args.mode, "policy": args.policy, "weights": args.weights,
+                   "t_attn_us": args.t_attn_us},
         "us_per_layer_step_incl_attn_window": round(us_layer_step, 3),
         "ffn_us": round(leg_ms * 1e3, 3),
         "ffn_hbm_GBps": round(achieved, 1),
@@ -263,7 +271,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": FFN_KERNELS[B == 1],
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": measured_traffic(cfg, B),
+                     "traffic": measured_traffic(cfg, B, args.weights),
                      "bytes_per_launch": leg_bytes, "launches": leg_n},
     }
     if args.policy == "static":
@@ -273,7 +281,7 @@ def main():
     runner.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, B, mode, tau, args.cpu_budget_s, policy,
-                                           args.static_delta, cdf)
+                                           args.static_delta, cdf, args.weights)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define APEX_ABI_VERSION 1
+#define APEX_ABI_VERSION 2
 #define APEX_MAX_EXPERTS 64
 #define APEX_MAX_PAIRS 1024     /* B * k limit of apex_moe_ffn */
 
@@ -64,6 +64,12 @@ typedef enum {
                                  and pf_idx is all -1.  apex_decode_step does not run
                                  the prefetch router at all under this policy.       */
 } apex_policy;
+
+/* Expert weight format: apex_pack_expert (bf16) or apex_pack_expert_fp8 (E4M3). */
+typedef enum {
+    APEX_WEIGHTS_BF16 = 0,
+    APEX_WEIGHTS_FP8_E4M3 = 1
+} apex_weights;
 
 /* Execution mode of apex_gate_topk (Sec. IV-E). */
 typedef enum {
@@ -144,6 +150,23 @@ apex_status apex_pack_expert(const uint16_t *w1, const uint16_t *w3, const uint1
                              int d, int I, uint16_t *out);
 
 /*
+ * Experts with 8-bit weights (the precision study of Sec. V-H: smaller experts move
+ * fewer bytes over the host link and out of HBM).  Weights are OCP E4M3 codes (1 sign,
+ * 4 exponent bits with bias 7, 3 mantissa bits; no infinities; largest value 448) with
+ * one fp32 scale per output row: row r of W1, W3 or W2 is s_r * q, where
+ * s_r = fp32(max |W[r, :]| / 448) and q rounds W[r, :] / s_r to the nearest code (ties
+ * to the even code, sign bit for negative values); an all-zero row has s_r = 0.
+ * apex_expert_bytes_fp8(d, I) = 3 d I + 4 (2 I + d) bytes:
+ *   rows i = 0..I-1 of [W1[i, 0:d] codes | W3[i, 0:d] codes], then W2 codes [d, I]
+ *   row-major, then the fp32 scales of W1's I rows, W3's I rows and W2's d rows.
+ * apex_pack_expert_fp8 quantises bf16 experts (w1, w3 [I, d], w2 [d, I]) into that
+ * layout (host memory to host memory); d and I must be multiples of 8.
+ */
+size_t apex_expert_bytes_fp8(int d, int I);
+apex_status apex_pack_expert_fp8(const uint16_t *w1, const uint16_t *w3, const uint16_t *w2,
+                                 int d, int I, void *out);
+
+/*
  * Gated SwiGLU experts (Sec. III-A weighted sum; Sec. IV-E aggregation with the
  * original router weights).  For every token b and position j with e = exec_idx[b, j]
  * in [0, E) and s = slot_of_expert[e] in [0, n_slots):
@@ -171,6 +194,18 @@ apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
                          const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,
                          float *y, int accumulate, void *workspace, size_t workspace_bytes,
                          hipStream_t stream);
+
+/*
+ * apex_moe_ffn over experts packed by apex_pack_expert_fp8: slot s starts at byte
+ * s * apex_expert_bytes_fp8(d, I) of `slots` (16-byte aligned).  The same sum, with
+ * every weight taken as s_r * q exactly; the row scales multiply the fp32 dot products.
+ * Same arguments, workspace size (apex_moe_ffn_workspace_bytes) and error behaviour.
+ */
+apex_status apex_moe_ffn_fp8(const float *x, int B, int d, int I, int E, int k,
+                             const int32_t *exec_idx, const float *exec_gate,
+                             const int32_t *slot_of_expert, const void *slots, int n_slots,
+                             float *y, int accumulate, void *workspace,
+                             size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Cache plan of one layer for one decode step (pure host function, no HIP calls).
@@ -270,13 +305,14 @@ typedef struct {
     int mode;              /* apex_mode */
     double t_attn_us;      /* attention-window stand-in per layer, >= 0 */
     int n_scratch;         /* miss-scratch slots (EXACT), >= min(E, B*k) recommended */
+    int weights;           /* apex_weights: layout of host_experts, slots and scratch */
 } apex_decode_config;
 
 typedef struct {
     const uint16_t *w_pf, *w_g;            /* device bf16 [E, d] */
     const float *b_pf, *b_g;               /* device fp32 [E] or NULL */
     const float *cdf_w, *cdf_theta;        /* device (ORDINAL_CDF only) or NULL */
-    const uint16_t *host_experts;          /* pinned, apex_pack_expert layout, [E] experts */
+    const uint16_t *host_experts;          /* pinned, [E] experts in the layout of cfg.weights */
     uint16_t *slots;                       /* device, [C] experts */
     int32_t *slot_of_expert_dev;           /* device int32 [E] (kept equal to the tables) */
     uint8_t *avail_dev;                    /* device uint8 [E] resident mask */

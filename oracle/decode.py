@@ -23,13 +23,14 @@ from .residency import Residency
 
 
 class LayerState:
-    def __init__(self, cfg, layer, seed=0, policy=routing.CUMPROB, cdf=None):
+    def __init__(self, cfg, layer, seed=0, policy=routing.CUMPROB, cdf=None, weights="bf16"):
         self.cfg, self.layer = cfg, layer
         self.wg, self.wpf, self.bias = inputs.router_weights(cfg, layer, seed)
         self.res = Residency(cfg.E, cfg.C)
         self.seed = seed
         self.policy = policy
         self.cdf = cdf if cdf is not None else (None, None)
+        self.weights = weights
         self._bits = {}
 
     def expert_bits(self, e):
@@ -54,7 +55,8 @@ def layer_step(st: LayerState, t, h_pre, h_post, mode, tau, static_delta=0, run_
             misses |= set(int(e) for e in g["route_idx"][b]) - R
     y = None
     if run_ffn:
-        y = ffn.moe_ffn(h_post, g["exec_idx"], g["exec_gate"], st.expert_bits)
+        y = ffn.moe_ffn(h_post, g["exec_idx"], g["exec_gate"], st.expert_bits,
+                        weights=st.weights)
     m = dict(
         overlap=[metrics.overlap(g["route_idx"][b], pf_lists[b], cfg.k) for b in range(B)],
         coverage=[metrics.full_coverage(g["route_idx"][b], pf_lists[b]) for b in range(B)],
@@ -67,14 +69,15 @@ def layer_step(st: LayerState, t, h_pre, h_post, mode, tau, static_delta=0, run_
 
 
 def run(cfg, batch, steps, mode=gating.EXACT, tau=None, seed=0, layers=None, run_ffn=True,
-        policy=routing.CUMPROB, static_delta=0, cdf=None):
+        policy=routing.CUMPROB, static_delta=0, cdf=None, weights="bf16"):
     """Replay ``steps`` decode steps of ``batch`` tokens; yields (t, layer, result).
 
-    cdf: {layer: (w, theta)} ordinal-model parameters when policy is ORDINAL_CDF.
+    cdf: {layer: (w, theta)} ordinal-model parameters when policy is ORDINAL_CDF;
+    weights: "bf16" or "fp8" expert weights (see ``ffn``).
     """
     tau = cfg.tau if tau is None else tau
     layers = range(cfg.L) if layers is None else layers
-    states = {l: LayerState(cfg, l, seed, policy, None if cdf is None else cdf[l])
+    states = {l: LayerState(cfg, l, seed, policy, None if cdf is None else cdf[l], weights)
               for l in layers}
     hs = {l: inputs.hidden_states(cfg, l, batch, steps, seed) for l in layers}
     for t in range(steps):

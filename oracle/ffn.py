@@ -7,11 +7,16 @@ experts process the token independently and their outputs are combined by a weig
 sum) and Sec. IV-E (the final aggregation uses the original router weights).
 Reading: the expert FFN is SwiGLU without biases, FFN(x) = W2 (silu(W1 x) * (W3 x)),
 silu(u) = u / (1 + exp(-u)), as the workload definitions state.
+
+With weights="fp8" every expert matrix is first quantised row by row to E4M3 with an
+fp32 scale per row (``fp8``, the reading taken for the precision study of Sec. V-H) and
+the FFN runs on the dequantised values s_r * q, in float64.
 """
 from __future__ import annotations
 
 import numpy as np
 
+from . import fp8
 from .bf16 import bf16_to_f64
 
 
@@ -27,13 +32,16 @@ def swiglu_expert(x, w1, w3, w2):
     return w2 @ (silu(u) * v)
 
 
-def moe_ffn(x, exec_idx, exec_gate, expert_bits, skip=None):
+def moe_ffn(x, exec_idx, exec_gate, expert_bits, skip=None, weights="bf16"):
     """y[b] = sum_j g[b, j] FFN_{e[b, j]}(x[b]) over the executed experts.
 
     x: [B, d]; exec_idx int [B, k] (-1 = unused position); exec_gate [B, k];
     expert_bits(e) -> (W1 bits [I,d], W3 bits [I,d], W2 bits [d,I]);
-    skip: optional set of expert ids left out (a pass that only covers some experts).
+    skip: optional set of expert ids left out (a pass that only covers some experts);
+    weights: "bf16" (the weights as given) or "fp8" (quantised per row first).
     """
+    if weights not in ("bf16", "fp8"):
+        raise ValueError(f"unknown weight format {weights}")
     x = np.atleast_2d(np.asarray(x, dtype=np.float64))
     B, d = x.shape
     y = np.zeros((B, d))
@@ -44,7 +52,10 @@ def moe_ffn(x, exec_idx, exec_gate, expert_bits, skip=None):
             if e < 0 or (skip is not None and e in skip):
                 continue
             if e not in cache:
-                cache[e] = tuple(bf16_to_f64(w) for w in expert_bits(e))
+                ws = tuple(bf16_to_f64(w) for w in expert_bits(e))
+                if weights == "fp8":
+                    ws = tuple(fp8.dequantize_rows(*fp8.quantize_rows(w)) for w in ws)
+                cache[e] = ws
             w1, w3, w2 = cache[e]
             y[b] += float(exec_gate[b, j]) * swiglu_expert(x[b], w1, w3, w2)
     return y

@@ -22,9 +22,9 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libapex.so")
 PLAN_LIB = os.path.join(PKG, "libapex_plan.so")
 
-HIP_SOURCES = ["errors.cpp", "residency.cpp", "decode.cpp", "route_gate.hip", "moe_ffn.cpp",
-               "ffn_b1.hip", "ffn_gemm.hip", "prefetch.hip", "util.hip"]
-HOST_SOURCES = ["errors.cpp", "residency.cpp"]
+HIP_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "decode.cpp", "route_gate.hip",
+               "moe_ffn.cpp", "ffn_b1.hip", "ffn_gemm.hip", "prefetch.hip", "util.hip"]
+HOST_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp"]
 
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
                # keep the compiler from forming packed fp32 instructions

@@ -86,6 +86,19 @@ void fold(apex_decode *dec, const apex_decode::Pending &p, apex_decode_stats *st
     st->misses += p.misses;
 }
 
+// One expert-FFN pass of the executed sets over the given slot pool.
+apex_status ffn(apex_decode *dec, const float *x, const int32_t *slot_of_expert,
+                const uint16_t *slots, int n_slots, float *y, int accumulate) {
+    const apex_decode_config &c = dec->cfg;
+    if (c.weights == APEX_WEIGHTS_FP8_E4M3)
+        return apex_moe_ffn_fp8(x, c.B, c.d, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate,
+                                slot_of_expert, slots, n_slots, y, accumulate, dec->ws,
+                                dec->ws_bytes, dec->compute);
+    return apex_moe_ffn(x, c.B, c.d, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate,
+                        slot_of_expert, slots, n_slots, y, accumulate, dec->ws, dec->ws_bytes,
+                        dec->compute);
+}
+
 void fold_pending(apex_decode *dec, apex_decode_stats *st) {
     for (const auto &p : dec->pending) fold(dec, p, st);
     dec->pending.clear();
@@ -108,6 +121,10 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
                  "%s: need 1 <= k <= k_max <= C <= E (k=%d k_max=%d C=%d E=%d)", fn, c.k,
                  c.k_max, c.C, c.E);
     APEX_REQUIRE(c.t_attn_us >= 0.0 && c.t_attn_us <= 1e6, "%s: t_attn_us=%g", fn, c.t_attn_us);
+    APEX_REQUIRE(c.weights == APEX_WEIGHTS_BF16 || c.weights == APEX_WEIGHTS_FP8_E4M3,
+                 "%s: unknown weight format %d", fn, c.weights);
+    APEX_REQUIRE(c.weights != APEX_WEIGHTS_FP8_E4M3 || (c.d % 16 == 0 && c.I % 16 == 0),
+                 "%s: E4M3 experts need d and I multiples of 16 (d=%d I=%d)", fn, c.d, c.I);
     APEX_REQUIRE(c.mode == APEX_MODE_EXACT || c.mode == APEX_MODE_STALL_FREE, "%s: mode %d", fn,
                  c.mode);
     APEX_REQUIRE(c.mode != APEX_MODE_EXACT || (scratch && miss_table_dev && c.n_scratch >= 1),
@@ -130,7 +147,8 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     dec->ws_bytes = workspace_bytes;
     dec->compute = compute;
     dec->side = side;
-    dec->expert_bytes = apex_expert_bytes(c.d, c.I);
+    dec->expert_bytes = c.weights == APEX_WEIGHTS_FP8_E4M3 ? apex_expert_bytes_fp8(c.d, c.I)
+                                                           : apex_expert_bytes(c.d, c.I);
     auto cleanup = [&](apex_status st) {
         apex_decode_destroy(dec);
         return st;
@@ -236,9 +254,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         if (st != APEX_OK) return st;
         APEX_HIP(hipEventRecord(dec->gate_done[l], cs));
         APEX_HIP(hipStreamWaitEvent(cs, dec->ready[l], 0));
-        st = apex_moe_ffn(h_post[l], c.B, c.d, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate,
-                          Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], 0, dec->ws, dec->ws_bytes,
-                          cs);
+        st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], 0);
         if (st != APEX_OK) return st;
         int n_miss = 0;
         if (c.mode == APEX_MODE_EXACT) {
@@ -253,9 +269,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
             if (st != APEX_OK) return st;
             if (n_miss > 0) {
                 APEX_HIP(hipStreamWaitEvent(cs, dec->ready_miss, 0));
-                st = apex_moe_ffn(h_post[l], c.B, c.d, c.I, c.E, c.k, dec->exec_idx,
-                                  dec->exec_gate, dec->miss_table, dec->scratch, c.n_scratch,
-                                  y[l], 1, dec->ws, dec->ws_bytes, cs);
+                st = ffn(dec, h_post[l], dec->miss_table, dec->scratch, c.n_scratch, y[l], 1);
                 if (st != APEX_OK) return st;
                 APEX_HIP(hipEventRecord(dec->scratch_free, cs));
             }

@@ -1,5 +1,5 @@
-// Device helpers shared by the expert-FFN kernels: bf16 unpacking, an 8-wide dot
-// product against fp32 activations, a wavefront sum and SiLU.
+// Device helpers shared by the expert-FFN kernels: bf16 unpacking, 8-wide (bf16) and
+// 16-wide (E4M3) dot products against fp32 activations, a wavefront sum and SiLU.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -33,6 +33,22 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 __device__ __forceinline__ float silu(float u) { return u / (1.f + expf(-u)); }
+
+// 16 E4M3 codes (the little-endian bytes of w) times x[0..3] (16 fp32 values); the
+// hardware conversion is exact, the products accumulate in fp32.
+__device__ __forceinline__ float dot16_e4m3(uint4 w, const float4 (&x)[4], float acc) {
+    const uint32_t word[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8(int(word[q]), false);   // bytes 0, 1
+        const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8(int(word[q]), true);    // bytes 2, 3
+        acc = fmaf(lo[0], x[q].x, acc);
+        acc = fmaf(lo[1], x[q].y, acc);
+        acc = fmaf(hi[0], x[q].z, acc);
+        acc = fmaf(hi[1], x[q].w, acc);
+    }
+    return acc;
+}
 
 }  // namespace ffn
 }  // namespace apex

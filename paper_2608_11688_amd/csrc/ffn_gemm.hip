@@ -13,8 +13,11 @@
 //     it stages its activations;
 //   * down_gemm writes per-split, per-pair outputs; combine_pairs adds the splits and the
 //     gated positions of each token in a fixed order.
-// Every executed expert's weights are read once per call whatever the number of tokens
-// routed to it, and no atomics are used, so results are deterministic.
+// Slots hold bf16 weights (apex_pack_expert) or E4M3 codes with fp32 row scales
+// (apex_pack_expert_fp8); E4M3 tiles are widened to bf16 exactly as they go to LDS and
+// the row scales multiply the outputs.  Every executed expert's weights are read once
+// per call whatever the number of tokens routed to it, and no atomics are used, so
+// results are deterministic.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -88,6 +91,38 @@ struct ActSwiglu {       // h from SU split partials: u of split s at row + 2s*s
     }
 };
 
+// Weight formats of a slot.  One 16-byte load per thread covers kPerLoad consecutive K
+// values of one row; kThrPerRow threads cover a 128-wide K block of the row and
+// kRowsPerPass rows are loaded per pass of the workgroup.
+struct WBf16 {           // apex_pack_expert slots: bf16 weights
+    using T = uint16_t;
+    static constexpr bool kFp8 = false;
+    static constexpr int kPerLoad = 8, kThrPerRow = kKB / 8, kRowsPerPass = kThreads / kThrPerRow;
+    static constexpr int kLoads = kRows / kRowsPerPass;
+};
+struct WE4M3 {           // apex_pack_expert_fp8 slots: E4M3 codes, fp32 row scales after them
+    using T = uint8_t;
+    static constexpr bool kFp8 = true;
+    static constexpr int kPerLoad = 16, kThrPerRow = kKB / 16, kRowsPerPass = kThreads / kThrPerRow;
+    static constexpr int kLoads = kRows / kRowsPerPass;
+};
+
+// 16 E4M3 codes (little-endian bytes of v) as 16 bf16 values, exactly: every E4M3 value
+// is a bf16 value, so dropping the low half of the fp32 conversion loses nothing.
+__device__ __forceinline__ void widen_e4m3(uint4 v, uint4 &lo, uint4 &hi) {
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const auto a = __builtin_amdgcn_cvt_pk_f32_fp8(int(w[q]), false);   // bytes 0, 1
+        const auto b = __builtin_amdgcn_cvt_pk_f32_fp8(int(w[q]), true);    // bytes 2, 3
+        o[2 * q] = (__float_as_uint(a[0]) >> 16) | (__float_as_uint(a[1]) & 0xffff0000u);
+        o[2 * q + 1] = (__float_as_uint(b[0]) >> 16) | (__float_as_uint(b[1]) & 0xffff0000u);
+    }
+    lo = make_uint4(o[0], o[1], o[2], o[3]);
+    hi = make_uint4(o[4], o[5], o[6], o[7]);
+}
+
 // The pairs p < P with exec_idx[p] == e, in ascending order, into list[]; returns how
 // many.  256 threads; P <= 1024 (four rounds of wave ballots).
 __device__ int expert_pairs(const int32_t *__restrict__ exec_idx, int P, int e, int *list,
@@ -120,26 +155,32 @@ __device__ int expert_pairs(const int32_t *__restrict__ exec_idx, int P, int e, 
 
 // One K block of the tile into registers.  Every weight address is valid (rows and K
 // are clamped) and pieces outside the tile are zeroed after the load instead of
-// branching, so the 4*NW weight loads issue back to back.
-template <int NW, int MT, class Act>
-__device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][4], uint4 (&xreg)[MT],
-                                          const uint16_t *const (&wbase)[NW], size_t wstride,
-                                          int rows_valid, int K, const void *const (&xrow)[MT],
-                                          const bool (&xok)[MT], size_t xstride, int k0, int r0,
-                                          int seg) {
-    const int kk = k0 + 8 * seg;
-    const bool in = kk < K;
-    const int kc = in ? kk : K - 8;
+// branching, so the weight loads issue back to back.
+template <int NW, int MT, class Act, class WF>
+__device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][WF::kLoads], uint4 (&xreg)[MT],
+                                          const typename WF::T *const (&wbase)[NW],
+                                          size_t wstride, int rows_valid, int K,
+                                          const void *const (&xrow)[MT], const bool (&xok)[MT],
+                                          size_t xstride, int k0) {
+    const int t = threadIdx.x;
+    const int wseg = t % WF::kThrPerRow, wr0 = t / WF::kThrPerRow;
+    const int wk = k0 + WF::kPerLoad * wseg;
+    const bool win = wk < K;
+    const int wkc = win ? wk : K - WF::kPerLoad;
 #pragma unroll
     for (int m = 0; m < NW; ++m)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int row = r0 + 16 * j;
+        for (int j = 0; j < WF::kLoads; ++j) {
+            const int row = wr0 + WF::kRowsPerPass * j;
             const int rc = row < rows_valid ? row : rows_valid - 1;
-            const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + kc);
-            wreg[m][j] = keep_if(v, in && row < rows_valid);
+            const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + wkc);
+            wreg[m][j] = keep_if(v, win && row < rows_valid);
         }
     // activation rows past the expert's tokens (tile padding) are not loaded at all
+    const int seg = t & 15;
+    const int kk = k0 + 8 * seg;
+    const bool in = kk < K;
+    const int kc = in ? kk : K - 8;
 #pragma unroll
     for (int j = 0; j < MT; ++j) {
         uint4 v = make_uint4(0u, 0u, 0u, 0u);
@@ -155,8 +196,9 @@ __device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][4], uint4 (&xreg)[MT
 // cache lines), the block goes to LDS, and while the matrix cores work on it the next
 // block is already loading into registers.  Wavefront w multiplies its 16 rows with
 // every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.
-template <int NW, int MT, class Act>
-__device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW], size_t wstride,
+template <int NW, int MT, class Act, class WF>
+__device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbase)[NW],
+                                              size_t wstride,
                                               int rows_valid, int K, int b_lo, int b_hi,
                                               const void *const (&xrow)[MT],
                                               const bool (&xok)[MT], size_t xstride,
@@ -164,7 +206,8 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW]
                                               uint16_t (*Xs)[kLdsRow], floatx4 (&acc)[NW][MT]) {
     const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
     const int seg = t & 15, r0 = t >> 4;
-    uint4 wreg[NW][4], xreg[MT];
+    const int wseg = t % WF::kThrPerRow, wr0 = t / WF::kThrPerRow;
+    uint4 wreg[NW][WF::kLoads], xreg[MT];
 #pragma unroll
     for (int m = 0; m < NW; ++m)
 #pragma unroll
@@ -178,21 +221,30 @@ __device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW]
         const int q = b + rot;
         return (b_lo + (q >= nb ? q - nb : q)) * kKB;
     };
-    gemm_load<NW, MT, Act>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, xstride,
-                           kblk(0), r0, seg);
+    gemm_load<NW, MT, Act, WF>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, xstride,
+                               kblk(0));
     for (int b = 0; b < nb; ++b) {
         __syncthreads();   // the previous block's fragments have been read
 #pragma unroll
         for (int m = 0; m < NW; ++m)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                *reinterpret_cast<uint4 *>(&Ws[m][r0 + 16 * j][8 * seg]) = wreg[m][j];
+            for (int j = 0; j < WF::kLoads; ++j) {
+                uint16_t *dst = &Ws[m][wr0 + WF::kRowsPerPass * j][WF::kPerLoad * wseg];
+                if constexpr (WF::kFp8) {
+                    uint4 lo, hi;
+                    widen_e4m3(wreg[m][j], lo, hi);
+                    *reinterpret_cast<uint4 *>(dst) = lo;
+                    *reinterpret_cast<uint4 *>(dst + 8) = hi;
+                } else {
+                    *reinterpret_cast<uint4 *>(dst) = wreg[m][j];
+                }
+            }
 #pragma unroll
         for (int j = 0; j < MT; ++j) *reinterpret_cast<uint4 *>(&Xs[r0 + 16 * j][8 * seg]) = xreg[j];
         __syncthreads();
         if (b + 1 < nb)
-            gemm_load<NW, MT, Act>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, xstride,
-                                   kblk(b + 1), r0, seg);
+            gemm_load<NW, MT, Act, WF>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok,
+                                       xstride, kblk(b + 1));
 #pragma unroll
         for (int q = 0; q < kKB / 32; ++q) {
             const int kc = 32 * q + 8 * (lane >> 4);
@@ -219,15 +271,24 @@ __device__ __forceinline__ void split_range(int K, int splits, int z, int &b_lo,
     b_hi = (z + 1) * nb / splits;
 }
 
+// The fp32 row scales of an apex_pack_expert_fp8 slot: W1 rows, W3 rows, W2 rows.
+template <class WF>
+__device__ __forceinline__ const float *row_scales(const typename WF::T *slot, int d, int I) {
+    return reinterpret_cast<const float *>(slot + size_t(3) * I * d);
+}
+
 // up_gemm: grid (ceil(I / 64), E, SU).  64 rows of W1 and W3 of expert blockIdx.y, every
-// token of the expert (16*MT per pass), K blocks of split blockIdx.z.
+// token of the expert (16*MT per pass), K blocks of split blockIdx.z.  slot_stride is
+// the slot size in elements of WF::T.
 // SU == 1: hb[pair, i] = bf16(silu(W1[i] . x_b) * (W3[i] . x_b)), ungated.
 // SU  > 1: uv[(2z) * P*I + pair*I + i] = W1[i] . x_b over the split, uv[(2z+1) ...] = W3.
-template <int MT, int SU>
+// E4M3 slots: the dot products are multiplied by the rows' scales.
+template <int MT, int SU, class WF>
 __global__ __launch_bounds__(kThreads) void up_gemm(
     const float *__restrict__ x, int d, int I, int P, int k, const int32_t *__restrict__ exec_idx,
-    const int32_t *__restrict__ slot_of_expert, int n_slots, const uint16_t *__restrict__ slots,
-    size_t slot_elems, __bf16 *__restrict__ hb, float *__restrict__ uv) {
+    const int32_t *__restrict__ slot_of_expert, int n_slots,
+    const typename WF::T *__restrict__ slots, size_t slot_stride, __bf16 *__restrict__ hb,
+    float *__restrict__ uv) {
     __shared__ uint16_t Ws[2][kRows][kLdsRow];
     __shared__ uint16_t Xs[16 * MT][kLdsRow];
     __shared__ int list[APEX_MAX_PAIRS];
@@ -241,8 +302,9 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
     int b_lo, b_hi;
     split_range(d, gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const uint16_t *W = slots + size_t(s) * slot_elems + size_t(i0) * 2 * d;
-    const uint16_t *const wbase[2] = {W, W + d};
+    const typename WF::T *slot = slots + size_t(s) * slot_stride;
+    const typename WF::T *W = slot + size_t(i0) * 2 * d;
+    const typename WF::T *const wbase[2] = {W, W + d};
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
         const void *xrow[MT];
         bool xok[MT];
@@ -254,9 +316,15 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[2][MT];
-        gemm_mainloop<2, MT, ActF32>(wbase, size_t(2) * d, I - i0, d, b_lo, b_hi, xrow, xok, 0,
-                                     n_tiles, Ws, Xs, acc);
+        gemm_mainloop<2, MT, ActF32, WF>(wbase, size_t(2) * d, I - i0, d, b_lo, b_hi, xrow, xok,
+                                         0, n_tiles, Ws, Xs, acc);
         const int i = i0 + 16 * wave + (lane & 15);
+        float s1 = 1.f, s3 = 1.f;
+        if constexpr (WF::kFp8) {
+            const float *sc = row_scales<WF>(slot, d, I);
+            s1 = i < I ? sc[i] : 0.f;
+            s3 = i < I ? sc[I + i] : 0.f;
+        }
 #pragma unroll
         for (int tt = 0; tt < MT; ++tt)
 #pragma unroll
@@ -264,11 +332,12 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
                 const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
                 if (tt < n_tiles && tok < n_e && i < I) {
                     const size_t at = size_t(list[tok]) * I + i;
+                    const float u = s1 * acc[0][tt][r], v = s3 * acc[1][tt][r];
                     if (SU == 1) {
-                        hb[at] = (__bf16)(silu(acc[0][tt][r]) * acc[1][tt][r]);
+                        hb[at] = (__bf16)(silu(u) * v);
                     } else {
-                        uv[size_t(2 * blockIdx.z) * P * I + at] = acc[0][tt][r];
-                        uv[size_t(2 * blockIdx.z + 1) * P * I + at] = acc[1][tt][r];
+                        uv[size_t(2 * blockIdx.z) * P * I + at] = u;
+                        uv[size_t(2 * blockIdx.z + 1) * P * I + at] = v;
                     }
                 }
             }
@@ -279,12 +348,12 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
 // down_gemm: grid (ceil(d / 64), E, SD).  64 rows j of W2 of expert blockIdx.y, K (= I)
 // blocks of split blockIdx.z.  yp[z * P*d + pair*d + j] = W2[j] . h[pair] over the split.
 // The activations come from Act: bf16 h rows, or h formed from up_gemm's split partials.
-template <int MT, class Act>
+template <int MT, class Act, class WF>
 __global__ __launch_bounds__(kThreads) void down_gemm(
     int d, int I, int P, const int32_t *__restrict__ exec_idx,
-    const int32_t *__restrict__ slot_of_expert, int n_slots, const uint16_t *__restrict__ slots,
-    size_t slot_elems, const void *__restrict__ act, size_t act_elem_bytes,
-    float *__restrict__ yp) {
+    const int32_t *__restrict__ slot_of_expert, int n_slots,
+    const typename WF::T *__restrict__ slots, size_t slot_stride, const void *__restrict__ act,
+    size_t act_elem_bytes, float *__restrict__ yp) {
     __shared__ uint16_t Ws[1][kRows][kLdsRow];
     __shared__ uint16_t Xs[16 * MT][kLdsRow];
     __shared__ int list[APEX_MAX_PAIRS];
@@ -298,8 +367,8 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
     int b_lo, b_hi;
     split_range(I, gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const uint16_t *const wbase[1] = {slots + size_t(s) * slot_elems + size_t(2) * I * d +
-                                      size_t(j0) * I};
+    const typename WF::T *slot = slots + size_t(s) * slot_stride;
+    const typename WF::T *const wbase[1] = {slot + size_t(2) * I * d + size_t(j0) * I};
     const char *ab = static_cast<const char *>(act);
     float *out = yp + size_t(blockIdx.z) * P * d;
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
@@ -313,16 +382,18 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[1][MT];
-        gemm_mainloop<1, MT, Act>(wbase, size_t(I), d - j0, I, b_lo, b_hi, hrow, hok,
-                                  size_t(P) * I, n_tiles, Ws, Xs, acc);
+        gemm_mainloop<1, MT, Act, WF>(wbase, size_t(I), d - j0, I, b_lo, b_hi, hrow, hok,
+                                      size_t(P) * I, n_tiles, Ws, Xs, acc);
         const int j = j0 + 16 * wave + (lane & 15);
+        float s2 = 1.f;
+        if constexpr (WF::kFp8) s2 = j < d ? row_scales<WF>(slot, d, I)[2 * I + j] : 0.f;
 #pragma unroll
         for (int tt = 0; tt < MT; ++tt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
                 if (tt < n_tiles && tok < n_e && j < d)
-                    out[size_t(list[tok]) * d + j] = acc[0][tt][r];
+                    out[size_t(list[tok]) * d + j] = s2 * acc[0][tt][r];
             }
         __syncthreads();   // LDS is reused by the next pass
     }
@@ -384,12 +455,67 @@ Plan plan_for(int B, int d, int I, int k, int E, int n_slots) {
     return pl;
 }
 
-template <int MT, int SU>
+template <int MT, int SU, class WF>
 void launch_up(dim3 g, hipStream_t st, const float *x, int d, int I, int P, int k,
-               const int32_t *exec_idx, const int32_t *soe, int n_slots, const uint16_t *slots,
-               size_t se, __bf16 *hb, float *uv) {
-    hipLaunchKernelGGL((up_gemm<MT, SU>), g, dim3(kThreads), 0, st, x, d, I, P, k, exec_idx, soe,
-                       n_slots, slots, se, hb, uv);
+               const int32_t *exec_idx, const int32_t *soe, int n_slots,
+               const typename WF::T *slots, size_t stride, __bf16 *hb, float *uv) {
+    hipLaunchKernelGGL((up_gemm<MT, SU, WF>), g, dim3(kThreads), 0, st, x, d, I, P, k, exec_idx,
+                       soe, n_slots, slots, stride, hb, uv);
+}
+
+template <int MT, class Act, class WF>
+void launch_down(dim3 g, hipStream_t st, int d, int I, int P, const int32_t *exec_idx,
+                 const int32_t *soe, int n_slots, const typename WF::T *slots, size_t stride,
+                 const void *act, size_t act_bytes, float *yp) {
+    hipLaunchKernelGGL((down_gemm<MT, Act, WF>), g, dim3(kThreads), 0, st, d, I, P, exec_idx, soe,
+                       n_slots, slots, stride, act, act_bytes, yp);
+}
+
+// The launches of one call for slots of weight format WF.
+template <class WF>
+apex_status run_grouped(const Plan &pl, const float *x, int B, int d, int I, int E, int k,
+                        const int32_t *exec_idx, const float *exec_gate,
+                        const int32_t *soe, const typename WF::T *slots, size_t stride,
+                        int n_slots, float *y, int accumulate, char *wsb, hipStream_t stream) {
+    const int P = B * k;
+    __bf16 *hb = reinterpret_cast<__bf16 *>(wsb);
+    float *uv = reinterpret_cast<float *>(wsb);
+    float *yp = reinterpret_cast<float *>(wsb + apex::align_up(pl.h_bytes, 256));
+    const dim3 gu((I + kRows - 1) / kRows, E, pl.SU);
+    if (pl.MT == 4)
+        launch_up<4, 1, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else if (pl.MT == 2)
+        launch_up<2, 1, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else if (pl.SU == 1)
+        launch_up<1, 1, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else if (pl.SU == 2)
+        launch_up<1, 2, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else if (pl.SU == 3)
+        launch_up<1, 3, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else
+        launch_up<1, 4, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    APEX_HIP(hipGetLastError());
+
+    const dim3 gd((d + kRows - 1) / kRows, E, pl.SD);
+    const void *act = pl.SU == 1 ? static_cast<const void *>(hb) : static_cast<const void *>(uv);
+    if (pl.MT == 4)
+        launch_down<4, ActBf16, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 2, yp);
+    else if (pl.MT == 2)
+        launch_down<2, ActBf16, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 2, yp);
+    else if (pl.SU == 1)
+        launch_down<1, ActBf16, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 2, yp);
+    else if (pl.SU == 2)
+        launch_down<1, ActSwiglu<2>, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 4, yp);
+    else if (pl.SU == 3)
+        launch_down<1, ActSwiglu<3>, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 4, yp);
+    else
+        launch_down<1, ActSwiglu<4>, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 4, yp);
+    APEX_HIP(hipGetLastError());
+    hipLaunchKernelGGL(combine_pairs, dim3((d + kThreads - 1) / kThreads, B), dim3(kThreads), 0,
+                       stream, B, d, E, k, pl.SD, exec_idx, exec_gate, soe, n_slots, yp, y,
+                       accumulate);
+    APEX_HIP(hipGetLastError());
+    return APEX_OK;
 }
 
 }  // namespace
@@ -409,55 +535,19 @@ size_t ffn_grouped_workspace(int B, int d, int I, int k) {
 
 apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *exec_idx, const float *exec_gate,
-                        const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,
-                        float *y, int accumulate, void *workspace, hipStream_t stream) {
-    const int P = B * k;
-    const size_t se = size_t(3) * d * I;
+                        const int32_t *slot_of_expert, const void *slots, int n_slots,
+                        bool fp8, float *y, int accumulate, void *workspace,
+                        hipStream_t stream) {
     const Plan pl = plan_for(B, d, I, k, E, n_slots);
     char *wsb = static_cast<char *>(workspace);
-    __bf16 *hb = reinterpret_cast<__bf16 *>(wsb);
-    float *uv = reinterpret_cast<float *>(wsb);
-    float *yp = reinterpret_cast<float *>(wsb + align_up(pl.h_bytes, 256));
-
-    const dim3 gu((I + kRows - 1) / kRows, E, pl.SU);
-    if (pl.MT == 4)
-        launch_up<4, 1>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
-    else if (pl.MT == 2)
-        launch_up<2, 1>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
-    else if (pl.SU == 1)
-        launch_up<1, 1>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
-    else if (pl.SU == 2)
-        launch_up<1, 2>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
-    else if (pl.SU == 3)
-        launch_up<1, 3>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
-    else
-        launch_up<1, 4>(gu, stream, x, d, I, P, k, exec_idx, slot_of_expert, n_slots, slots, se, hb, uv);
-    APEX_HIP(hipGetLastError());
-
-    const dim3 gd((d + kRows - 1) / kRows, E, pl.SD);
-    const void *act = pl.SU == 1 ? static_cast<const void *>(hb) : static_cast<const void *>(uv);
-#define APEX_DOWN(MT_, ACT_, EB_)                                                           \
-    hipLaunchKernelGGL((down_gemm<MT_, ACT_>), gd, dim3(kThreads), 0, stream, d, I, P, exec_idx, \
-                       slot_of_expert, n_slots, slots, se, act, size_t(EB_), yp)
-    if (pl.MT == 4)
-        APEX_DOWN(4, ActBf16, 2);
-    else if (pl.MT == 2)
-        APEX_DOWN(2, ActBf16, 2);
-    else if (pl.SU == 1)
-        APEX_DOWN(1, ActBf16, 2);
-    else if (pl.SU == 2)
-        APEX_DOWN(1, ActSwiglu<2>, 4);
-    else if (pl.SU == 3)
-        APEX_DOWN(1, ActSwiglu<3>, 4);
-    else
-        APEX_DOWN(1, ActSwiglu<4>, 4);
-#undef APEX_DOWN
-    APEX_HIP(hipGetLastError());
-    hipLaunchKernelGGL(combine_pairs, dim3((d + kThreads - 1) / kThreads, B), dim3(kThreads), 0,
-                       stream, B, d, E, k, pl.SD, exec_idx, exec_gate, slot_of_expert, n_slots, yp,
-                       y, accumulate);
-    APEX_HIP(hipGetLastError());
-    return APEX_OK;
+    if (fp8)
+        return run_grouped<WE4M3>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                                  static_cast<const uint8_t *>(slots),
+                                  apex_expert_bytes_fp8(d, I), n_slots, y, accumulate, wsb,
+                                  stream);
+    return run_grouped<WBf16>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                              static_cast<const uint16_t *>(slots), size_t(3) * d * I, n_slots,
+                              y, accumulate, wsb, stream);
 }
 
 }  // namespace apex

@@ -18,13 +18,21 @@ apex_status ffn_b1(const float *x, int d, int I, int E, int k, const int32_t *ex
                    const float *exec_gate, const int32_t *slot_of_expert, const uint16_t *slots,
                    int n_slots, float *h, float *y, int accumulate, hipStream_t stream);
 
-// Two or more tokens: grouped GEMMs on the matrix cores.  `workspace` is 256-byte
-// aligned and holds ffn_grouped_workspace(B, d, I, k) bytes.
+// The same over apex_pack_expert_fp8 slots (d and I multiples of 16).
+apex_status ffn_b1_fp8(const float *x, int d, int I, int E, int k, const int32_t *exec_idx,
+                       const float *exec_gate, const int32_t *slot_of_expert,
+                       const uint8_t *slots, int n_slots, float *h, float *y, int accumulate,
+                       hipStream_t stream);
+
+// Two or more tokens: grouped GEMMs on the matrix cores, over bf16 slots or (fp8) E4M3
+// slots.  `workspace` is 256-byte aligned and holds ffn_grouped_workspace(B, d, I, k)
+// bytes.
 size_t ffn_grouped_workspace(int B, int d, int I, int k);
 apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *exec_idx, const float *exec_gate,
-                        const int32_t *slot_of_expert, const uint16_t *slots, int n_slots,
-                        float *y, int accumulate, void *workspace, hipStream_t stream);
+                        const int32_t *slot_of_expert, const void *slots, int n_slots,
+                        bool fp8, float *y, int accumulate, void *workspace,
+                        hipStream_t stream);
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

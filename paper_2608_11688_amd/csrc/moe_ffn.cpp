@@ -1,5 +1,5 @@
-// apex_moe_ffn: argument checks and the choice between the batch-1 path (ffn_b1.hip)
-// and the grouped matrix-core path (ffn_gemm.hip).
+// apex_moe_ffn and apex_moe_ffn_fp8: argument checks and the choice between the batch-1
+// path (ffn_b1.hip) and the grouped matrix-core path (ffn_gemm.hip).
 #include <hip/hip_runtime.h>
 
 #include "ffn_internal.h"
@@ -9,19 +9,23 @@ extern "C" size_t apex_moe_ffn_workspace_bytes(int B, int d, int I, int k) {
     return B == 1 ? apex::ffn_b1_workspace(d, I, k) : apex::ffn_grouped_workspace(B, d, I, k);
 }
 
-extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
-                                    const int32_t *exec_idx, const float *exec_gate,
-                                    const int32_t *slot_of_expert, const uint16_t *slots,
-                                    int n_slots, float *y, int accumulate, void *workspace,
-                                    size_t workspace_bytes, hipStream_t stream) {
-    const char *fn = "apex_moe_ffn";
+namespace {
+
+apex_status moe_ffn(const char *fn, bool fp8, const float *x, int B, int d, int I, int E, int k,
+                    const int32_t *exec_idx, const float *exec_gate,
+                    const int32_t *slot_of_expert, const void *slots, int n_slots, float *y,
+                    int accumulate, void *workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+    const int mult = fp8 ? 16 : 8;   // one 16-byte load holds 16 E4M3 or 8 bf16 weights
     APEX_REQUIRE(B >= 0, "%s: B=%d must be >= 0", fn, B);
     APEX_REQUIRE(E >= 1, "%s: E=%d must be >= 1", fn, E);
     if (E > APEX_MAX_EXPERTS)
         return apex::fail(APEX_E_UNSUPPORTED, "%s: E=%d exceeds %d", fn, E, APEX_MAX_EXPERTS);
     APEX_REQUIRE(k >= 1 && k <= E, "%s: k=%d out of [1, E=%d]", fn, k, E);
-    APEX_REQUIRE(d >= 8 && d % 8 == 0, "%s: d=%d must be a positive multiple of 8", fn, d);
-    APEX_REQUIRE(I >= 8 && I % 8 == 0, "%s: I=%d must be a positive multiple of 8", fn, I);
+    APEX_REQUIRE(d >= mult && d % mult == 0, "%s: d=%d must be a positive multiple of %d", fn,
+                 d, mult);
+    APEX_REQUIRE(I >= mult && I % mult == 0, "%s: I=%d must be a positive multiple of %d", fn,
+                 I, mult);
     APEX_REQUIRE(n_slots >= 1, "%s: n_slots=%d must be >= 1", fn, n_slots);
     if (size_t(B) * k > APEX_MAX_PAIRS)
         return apex::fail(APEX_E_UNSUPPORTED, "%s: B*k=%d exceeds %d", fn, B * k, APEX_MAX_PAIRS);
@@ -35,9 +39,37 @@ extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, 
     if (workspace_bytes < need)
         return apex::fail(APEX_E_CAPACITY, "%s: workspace %zu < %zu bytes", fn, workspace_bytes,
                           need);
-    if (B == 1)
-        return apex::ffn_b1(x, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots,
-                            static_cast<float *>(workspace), y, accumulate, stream);
+    if (B == 1) {
+        float *h = static_cast<float *>(workspace);
+        if (fp8)
+            return apex::ffn_b1_fp8(x, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                                    static_cast<const uint8_t *>(slots), n_slots, h, y,
+                                    accumulate, stream);
+        return apex::ffn_b1(x, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                            static_cast<const uint16_t *>(slots), n_slots, h, y, accumulate,
+                            stream);
+    }
     return apex::ffn_grouped(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots,
-                             n_slots, y, accumulate, workspace, stream);
+                             n_slots, fp8, y, accumulate, workspace, stream);
+}
+
+}  // namespace
+
+extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
+                                    const int32_t *exec_idx, const float *exec_gate,
+                                    const int32_t *slot_of_expert, const uint16_t *slots,
+                                    int n_slots, float *y, int accumulate, void *workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
+    return moe_ffn("apex_moe_ffn", false, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                   slots, n_slots, y, accumulate, workspace, workspace_bytes, stream);
+}
+
+extern "C" apex_status apex_moe_ffn_fp8(const float *x, int B, int d, int I, int E, int k,
+                                        const int32_t *exec_idx, const float *exec_gate,
+                                        const int32_t *slot_of_expert, const void *slots,
+                                        int n_slots, float *y, int accumulate, void *workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+    return moe_ffn("apex_moe_ffn_fp8", true, x, B, d, I, E, k, exec_idx, exec_gate,
+                   slot_of_expert, slots, n_slots, y, accumulate, workspace, workspace_bytes,
+                   stream);
 }

@@ -23,6 +23,8 @@ PLAN_LIB_PATH = os.path.join(PKG, "libapex_plan.so")
 APEX_OK, APEX_E_INVAL, APEX_E_UNSUPPORTED, APEX_E_HIP, APEX_E_CAPACITY = 0, -1, -2, -3, -4
 SEL_CUMPROB, SEL_ORDINAL_CDF, SEL_STATIC, SEL_NONE = 0, 1, 2, 3
 MODE_EXACT, MODE_STALL_FREE = 0, 1
+WEIGHTS_BF16, WEIGHTS_FP8_E4M3 = 0, 1
+ABI_VERSION = 2
 MAX_EXPERTS = 64
 MAX_PAIRS = 1024
 
@@ -44,7 +46,7 @@ I32, I64, F32, F64, SZ = C.c_int, C.c_int64, C.c_float, C.c_double, C.c_size_t
 class DecodeConfig(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("L", "B", "d", "E", "k", "I", "C", "k_max", "policy")] + [
         ("tau", C.c_float), ("static_delta", C.c_int), ("mode", C.c_int),
-        ("t_attn_us", C.c_double), ("n_scratch", C.c_int)]
+        ("t_attn_us", C.c_double), ("n_scratch", C.c_int), ("weights", C.c_int)]
 
 
 class DecodeLayer(C.Structure):
@@ -74,8 +76,11 @@ SIGNATURES = {
     "apex_gate_topk": (I32, [P, P, P, I32, I32, I32, I32, I32, P, I32, P, P, P, P, P, P]),
     "apex_expert_bytes": (SZ, [I32, I32]),
     "apex_pack_expert": (I32, [P, P, P, I32, I32, P]),
+    "apex_expert_bytes_fp8": (SZ, [I32, I32]),
+    "apex_pack_expert_fp8": (I32, [P, P, P, I32, I32, P]),
     "apex_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32, I32]),
     "apex_moe_ffn": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
+    "apex_moe_ffn_fp8": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_plan_residency": (I32, [I32, I32, P, P, I32, I32, I64, P, P, P, P, P]),
     "apex_expert_prefetch": (I32, [P, P, I32, I32, SZ, P, P, I32, I32, I64, P, P, P, P, P, P, P,
                                    P, P, P]),
@@ -97,7 +102,7 @@ SIGNATURES = {
 }
 
 HOST_ONLY = ("apex_abi_version", "apex_last_error", "apex_expert_bytes", "apex_pack_expert",
-             "apex_plan_residency")
+             "apex_expert_bytes_fp8", "apex_pack_expert_fp8", "apex_plan_residency")
 
 
 def header_functions(path=HEADER):
@@ -188,6 +193,14 @@ def apex_pack_expert(w1, w3, w2, d, I, out, L=None):
     _call("apex_pack_expert", ptr(w1), ptr(w3), ptr(w2), d, I, ptr(out), L=L)
 
 
+def apex_expert_bytes_fp8(d, I, L=None):
+    return (L or lib()).apex_expert_bytes_fp8(d, I)
+
+
+def apex_pack_expert_fp8(w1, w3, w2, d, I, out, L=None):
+    _call("apex_pack_expert_fp8", ptr(w1), ptr(w3), ptr(w2), d, I, ptr(out), L=L)
+
+
 def apex_moe_ffn_workspace_bytes(B, d, I, k):
     return lib().apex_moe_ffn_workspace_bytes(B, d, I, k)
 
@@ -195,6 +208,13 @@ def apex_moe_ffn_workspace_bytes(B, d, I, k):
 def apex_moe_ffn(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots, y,
                  accumulate, workspace, workspace_bytes, stream=None):
     _call("apex_moe_ffn", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
+          ptr(slot_of_expert), ptr(slots), n_slots, ptr(y), int(accumulate), ptr(workspace),
+          workspace_bytes, stream)
+
+
+def apex_moe_ffn_fp8(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots, y,
+                     accumulate, workspace, workspace_bytes, stream=None):
+    _call("apex_moe_ffn_fp8", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
           ptr(slot_of_expert), ptr(slots), n_slots, ptr(y), int(accumulate), ptr(workspace),
           workspace_bytes, stream)
 

@@ -44,7 +44,8 @@ class StepLog:
 class DecodeRunner:
     def __init__(self, cfg: configs.MoEConfig, batch=1, mode=EXACT, tau=None,
                  policy=native.SEL_CUMPROB, static_delta=0, seed=0, steps=None, t_attn_us=10.0,
-                 layers=None, n_scratch=None, record=False, cdf=None, gen_threads=16):
+                 layers=None, n_scratch=None, record=False, cdf=None, gen_threads=16,
+                 weights="bf16"):
         torch = _torch()
         self.torch = torch
         self.cfg, self.B, self.mode = cfg, batch, mode
@@ -58,7 +59,11 @@ class DecodeRunner:
         self.compute = torch.cuda.current_stream()
         self.side = torch.cuda.Stream()
         self.cs, self.ss = self.compute.cuda_stream, self.side.cuda_stream
-        self.S = native.apex_expert_bytes(cfg.d, cfg.I)
+        if weights not in ("bf16", "fp8"):
+            raise ValueError(f"weights must be 'bf16' or 'fp8', not {weights!r}")
+        self.weights = weights
+        self.S = (native.apex_expert_bytes_fp8(cfg.d, cfg.I) if weights == "fp8"
+                  else native.apex_expert_bytes(cfg.d, cfg.I))
         E, B, k = cfg.E, batch, cfg.k
         self.n_scratch = min(E, B * k) if n_scratch is None else n_scratch
         L = len(self.layers)
@@ -81,7 +86,9 @@ class DecodeRunner:
         dcfg = native.DecodeConfig(L=L, B=B, d=cfg.d, E=E, k=k, I=cfg.I, C=cfg.C,
                                    k_max=cfg.k_max, policy=policy, tau=self.tau,
                                    static_delta=static_delta, mode=mode, t_attn_us=t_attn_us,
-                                   n_scratch=self.n_scratch)
+                                   n_scratch=self.n_scratch,
+                                   weights=(native.WEIGHTS_FP8_E4M3 if weights == "fp8"
+                                            else native.WEIGHTS_BF16))
         descs = []
         for l in self.layers:
             b = self.bufs[l]
@@ -125,7 +132,9 @@ class DecodeRunner:
 
         def fill(e):
             w1, w3, w2 = inputs.expert_weights(cfg, l, e, self.seed)
-            native.apex_pack_expert(w1, w3, w2, cfg.d, cfg.I, hp + e * self.S)
+            pack = (native.apex_pack_expert_fp8 if self.weights == "fp8"
+                    else native.apex_pack_expert)
+            pack(w1, w3, w2, cfg.d, cfg.I, hp + e * self.S)
 
         list(pool.map(fill, range(cfg.E)))
         slots = torch.empty(cfg.C * S2, dtype=torch.int16, device=self.dev)

@@ -18,13 +18,13 @@ pytestmark = pytest.mark.gpu
 
 
 def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau=None,
-                 ffn_every=1, cdf=None):
+                 ffn_every=1, cdf=None, weights="bf16"):
     """cdf: {layer: (w, theta)} for the ORDINAL policy; seeded random models if None."""
     from paper_2608_11688_amd.runtime import DecodeRunner
     tau = cfg.tau if tau is None else tau
     tau32 = float(np.float32(tau))
     runner = DecodeRunner(cfg, batch=batch, mode=mode, tau=tau32, policy=policy, steps=steps,
-                          layers=layers, t_attn_us=2.0, record=True, cdf=cdf)
+                          layers=layers, t_attn_us=2.0, record=True, cdf=cdf, weights=weights)
     ledger = TieLedger()
     res = {l: Residency(cfg.E, cfg.C) for l in layers}
     routers = {l: inputs.router_weights(cfg, l) for l in layers}
@@ -66,7 +66,7 @@ def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau
                 if (t * len(layers) + layers.index(l)) % ffn_every == 0:
                     bits = lambda e, l=l: inputs.expert_weights(cfg, l, e)
                     y_ref = offn.moe_ffn(h_post, log.exec_idx, log.exec_gate.astype(np.float64),
-                                         bits)
+                                         bits, weights=weights)
                     _, l1 = ffn_close(log.y, y_ref, f"y t{t} l{l}")
                     stats["worst_l1"] = max(stats["worst_l1"], l1)
                     stats["ffn_checked"] += 1
@@ -143,3 +143,16 @@ def test_decode_every_expert_routed():
     for mode in (native.MODE_EXACT, native.MODE_STALL_FREE):
         st = check_decode(cfg, 3, mode, 10, [0])
         assert st["covered"] == st["tokens"] and st["copies"] == 0
+
+
+@pytest.mark.parametrize("mode", [native.MODE_EXACT, native.MODE_STALL_FREE])
+def test_decode_granite1b_fp8_experts(mode):
+    # E4M3 experts through prefetch, miss correction and both FFN passes
+    cfg = configs.GRANITE_1B
+    st = check_decode(cfg, 1, mode, 4, [0, 7, 23], weights="fp8")
+    assert st["copies"] > 0
+
+
+def test_decode_olmoe_batch16_fp8_experts():
+    cfg = configs.OLMOE
+    check_decode(cfg, 16, native.MODE_EXACT, 2, [3], ffn_every=1, weights="fp8")

@@ -200,11 +200,12 @@ def test_gate_fewer_available_than_k_and_none(torch):
 class FfnCase:
     """A slot pool holding some of the experts, and a batch routed over all of them."""
 
-    def __init__(self, torch, cfg, B, seed, resident_frac=1.0, n_slots_extra=0):
+    def __init__(self, torch, cfg, B, seed, resident_frac=1.0, n_slots_extra=0, weights="bf16"):
         rng = np.random.default_rng(seed)
-        self.cfg, self.B = cfg, B
+        self.cfg, self.B, self.weights = cfg, B, weights
         E, k = cfg.E, cfg.k
-        self.S = native.apex_expert_bytes(cfg.d, cfg.I)
+        fp8 = weights == "fp8"
+        self.S = (native.apex_expert_bytes_fp8 if fp8 else native.apex_expert_bytes)(cfg.d, cfg.I)
         self.x = rng.standard_normal((B, cfg.d)).astype(np.float32)
         self.exec_idx = np.stack([rng.choice(E, k, replace=False) for _ in range(B)]).astype(np.int32)
         if B > 1:
@@ -220,12 +221,17 @@ class FfnCase:
         for e, s in zip(self.resident, slot_ids):
             self.table[e] = s
         self.bits = {}
-        pool = np.zeros(self.n_slots * self.S // 2, np.uint16)
+        if fp8:
+            pool = np.zeros(self.n_slots * self.S, np.uint8)
+            piece = lambda s: pool[s * self.S:(s + 1) * self.S]
+            pack = native.apex_pack_expert_fp8
+        else:
+            pool = np.zeros(self.n_slots * self.S // 2, np.uint16)
+            piece = lambda s: pool[s * self.S // 2:(s + 1) * self.S // 2]
+            pack = native.apex_pack_expert
         for e in self.resident:
             self.bits[e] = inputs.expert_weights(cfg, 0, e)
-            s = int(self.table[e])
-            native.apex_pack_expert(*self.bits[e], cfg.d, cfg.I,
-                                    pool[s * self.S // 2:(s + 1) * self.S // 2])
+            pack(*self.bits[e], cfg.d, cfg.I, piece(int(self.table[e])))
         self.pool = dev(torch, pool)
         self.torch = torch
 
@@ -236,9 +242,10 @@ class FfnCase:
         ws = torch.full((ws_bytes,), 0xAB, dtype=torch.uint8, device="cuda")
         y = dev(torch, y0) if y0 is not None else torch.full((B, cfg.d), float("nan"),
                                                               device="cuda")
-        native.apex_moe_ffn(dev(torch, self.x), B, cfg.d, cfg.I, cfg.E, cfg.k,
-                            dev(torch, self.exec_idx), dev(torch, self.gate), dev(torch, table),
-                            self.pool, self.n_slots, y, accumulate, ws, ws_bytes)
+        ffn = native.apex_moe_ffn_fp8 if self.weights == "fp8" else native.apex_moe_ffn
+        ffn(dev(torch, self.x), B, cfg.d, cfg.I, cfg.E, cfg.k, dev(torch, self.exec_idx),
+            dev(torch, self.gate), dev(torch, table), self.pool, self.n_slots, y, accumulate, ws,
+            ws_bytes)
         torch.cuda.synchronize()
         return y.cpu().numpy()
 
@@ -246,13 +253,14 @@ class FfnCase:
         """The oracle for a few tokens only (each output row depends on its token alone)."""
         skip = set(range(self.cfg.E)) - set(self.resident)
         return offn.moe_ffn(self.x[rows], self.exec_idx[rows],
-                            self.gate[rows].astype(np.float64), lambda e: self.bits[e], skip=skip)
+                            self.gate[rows].astype(np.float64), lambda e: self.bits[e], skip=skip,
+                            weights=self.weights)
 
     def oracle(self, only=None):
         keep = set(self.resident) if only is None else set(only)
         skip = set(range(self.cfg.E)) - keep
         return offn.moe_ffn(self.x, self.exec_idx, self.gate.astype(np.float64),
-                            lambda e: self.bits[e], skip=skip)
+                            lambda e: self.bits[e], skip=skip, weights=self.weights)
 
 
 FFN_SHAPES = [
@@ -352,6 +360,41 @@ def test_ffn_parity_mixtral_batched_sampled_tokens(torch, B):
     want = case.oracle_rows(rows)
     for i, r in enumerate(rows):
         print("mixtral", B, r, ffn_close(y[r:r + 1], want[i:i + 1], f"mixtral B{B} token {r}"))
+
+
+FP8_SHAPES = [
+    # E4M3 experts (apex_moe_ffn_fp8): d and I multiples of 16
+    (configs.GRANITE_1B, 1), (configs.GRANITE_3B, 1), (configs.OLMOE, 1), (configs.TINY, 1),
+    (configs.GRANITE_3B, 8), (configs.OLMOE, 16),
+    (shape("fp8_b48", 430, 512, 6, 2, I=256), 48),         # four token tiles per pass
+    (shape("fp8_split_a", 431, 784, 4, 2, I=1008), 4),     # up 3 splits, down 4; ragged K
+    (shape("fp8_split_b", 432, 1008, 4, 2, I=784), 5),     # up 4 splits, down 3
+    (shape("fp8_small", 433, 16, 3, 2, I=48), 3),          # one 16-byte chunk per row
+]
+
+
+@pytest.mark.parametrize("cfg,B", FP8_SHAPES, ids=[f"{c.name}-B{b}" for c, b in FP8_SHAPES])
+def test_ffn_fp8_parity(torch, cfg, B):
+    case = FfnCase(torch, cfg, B, seed=cfg.cfg_id * 7 + B, weights="fp8")
+    y = case.run()
+    print(cfg.name, B, ffn_close(y, case.oracle(), f"{cfg.name} B{B} fp8"))
+
+
+def test_ffn_fp8_mixtral_batch1_and_two_passes(torch):
+    # d = 4096 takes the wide batch-1 kernels; a second pass adds the other experts
+    cfg = configs.MIXTRAL
+    case = FfnCase(torch, cfg, 1, seed=50, weights="fp8")
+    print("mixtral fp8", ffn_close(case.run(), case.oracle(), "mixtral B1 fp8"))
+    cfg = shape("fp8_pass", 434, 512, 12, 4, I=256)
+    case = FfnCase(torch, cfg, 20, seed=51, n_slots_extra=2, weights="fp8")
+    res = case.resident
+    first, second = res[: len(res) // 2], res[len(res) // 2:]
+    t1, t2 = case.table.copy(), case.table.copy()
+    t1[second] = -1
+    t2[first] = -1
+    y1 = case.run(t1)
+    ffn_close(y1, case.oracle(only=first), "fp8 pass 1")
+    ffn_close(case.run(t2, y0=y1, accumulate=1), case.oracle(), "fp8 pass 1 + pass 2")
 
 
 def test_ffn_two_passes_equal_one(torch):

@@ -37,7 +37,8 @@ def test_libraries_export_every_declared_symbol(hip_lib, plan_lib):
         assert hasattr(hip_lib, name), name
     for name in native.HOST_ONLY:
         assert hasattr(plan_lib, name), name
-    assert native.abi_version(hip_lib) == 1 and native.abi_version(plan_lib) == 1
+    assert native.abi_version(hip_lib) == native.ABI_VERSION
+    assert native.abi_version(plan_lib) == native.ABI_VERSION
 
 
 @pytest.mark.parametrize("E,Cs,B,k_max,steps", [(8, 4, 1, 4, 60), (32, 16, 1, 16, 80),
@@ -158,3 +159,33 @@ def test_workspace_size():
     big = native.apex_moe_ffn_workspace_bytes(64, 2048, 1024, 8)   # batched path
     # bf16 h and fp32 per-pair outputs for 512 pairs, bf16 activations
     assert big >= 512 * (1024 * 2 + 2048 * 4) + 64 * 2048 * 2 and big % 256 == 0
+
+
+def test_pack_expert_fp8_matches_the_oracle_quantiser(plan_lib):
+    # the packed codes and scales equal the oracle's own E4M3 quantisation, byte for byte
+    from oracle import fp8
+    from oracle.bf16 import bf16_to_f64
+    d, I = 48, 32
+    rng = np.random.default_rng(41)
+    def bf16(a):
+        return (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    w1 = bf16(rng.standard_normal((I, d)) * 0.02)
+    w3 = bf16(rng.standard_normal((I, d)) * 3e-4)       # values reach the subnormal codes
+    w2 = bf16(rng.standard_normal((d, I)) * 0.02)
+    w1[5] = 0                                            # an all-zero row
+    w3[2, 3] = bf16([-1.0])[0]                           # a negative peak
+    nbytes = native.apex_expert_bytes_fp8(d, I, L=plan_lib)
+    assert nbytes == 3 * d * I + 4 * (2 * I + d)
+    out = np.zeros(nbytes, np.uint8)
+    native.apex_pack_expert_fp8(w1, w3, w2, d, I, out, L=plan_lib)
+    rows = out[:2 * I * d].reshape(I, 2 * d)
+    c2 = out[2 * I * d:3 * I * d].reshape(d, I)
+    sc = out[3 * I * d:].view(np.float32)
+    for mat, codes, scales in ((w1, rows[:, :d], sc[:I]), (w3, rows[:, d:], sc[I:2 * I]),
+                               (w2, c2, sc[2 * I:])):
+        want_codes, want_scales = fp8.quantize_rows(bf16_to_f64(mat))
+        assert np.array_equal(scales, want_scales)
+        assert np.array_equal(codes, want_codes)
+    assert sc[5] == 0 and not rows[5, :d].any()
+    with pytest.raises(native.ApexError):
+        native.apex_pack_expert_fp8(w1, w3, w2, 44, I, out, L=plan_lib)   # d not a multiple of 8
