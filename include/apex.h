@@ -175,8 +175,9 @@ apex_status apex_pack_expert_fp8(const uint16_t *w1, const uint16_t *w3, const u
  * Pairs whose expert has no slot are left out of this pass, which is how the miss
  * correction runs the missing experts in a second pass with accumulate = 1.
  * Each expert's weights are read from HBM once per call whatever the number of
- * tokens routed to it.  Arithmetic: fp32 accumulation of bf16 weights times fp32
- * activations.  Result is deterministic for given inputs.
+ * tokens routed to it.  Arithmetic: fp32 accumulation; at B = 1 the activations stay
+ * fp32, at B >= 2 the matrix cores take x and the intermediate h rounded to bf16.
+ * No atomics: the result is deterministic for given inputs.
  *   x               device fp32 [B, d]
  *   exec_idx        device int32 [B, k];  exec_gate device fp32 [B, k]
  *   slot_of_expert  device int32 [E]: slot index or -1

@@ -30,6 +30,20 @@ class MoEConfig:
     batches: Tuple[int, ...] = (1,)
     taus: Tuple[float, ...] = ()       # tau sweep, if any
     bias_skew: bool = False            # per-expert logit bias ~N(0,1) (Zipf-like load)
+    heads: int = 0                     # attention query heads (0: d / 64)
+    kv_heads: int = 0                  # attention key/value heads (0: as many as heads)
+
+    @property
+    def n_heads(self) -> int:
+        return self.heads or self.d // 64
+
+    @property
+    def n_kv_heads(self) -> int:
+        return self.kv_heads or self.n_heads
+
+    @property
+    def head_dim(self) -> int:
+        return self.d // self.n_heads
 
     @property
     def expert_bytes(self) -> int:
@@ -40,17 +54,20 @@ class MoEConfig:
         return n_experts * self.expert_bytes
 
 
+# Attention shapes (heads / key-value heads) follow the published model configurations;
+# they only shape the decode-attention window that the prefetch overlaps.
 TINY = MoEConfig("tiny", 0, L=1, d=256, E=8, k=2, I=512, C=4, k_max=4, tau=0.9,
-                 steps=64)
+                 steps=64, heads=4, kv_heads=2)
 GRANITE_1B = MoEConfig("granite-1b-a400m", 1, L=24, d=1024, E=32, k=8, I=512, C=16,
-                       k_max=16, tau=0.9, steps=256)
+                       k_max=16, tau=0.9, steps=256, heads=16, kv_heads=8)
 GRANITE_3B = MoEConfig("granite-3b-a800m", 2, L=32, d=1536, E=40, k=8, I=512, C=16,
                        k_max=16, tau=0.9, steps=256, batches=(1, 8),
-                       taus=(0.8, 0.9, 0.95, 0.99))
+                       taus=(0.8, 0.9, 0.95, 0.99), heads=24, kv_heads=8)
 OLMOE = MoEConfig("olmoe-1b-7b", 3, L=16, d=2048, E=64, k=8, I=1024, C=24, k_max=16,
-                  tau=0.9, steps=256, batches=(1, 16, 64), bias_skew=True)
+                  tau=0.9, steps=256, batches=(1, 16, 64), bias_skew=True, heads=16,
+                  kv_heads=16)
 MIXTRAL = MoEConfig("mixtral-8x7b", 4, L=8, d=4096, E=8, k=2, I=14336, C=4, k_max=4,
-                    tau=0.9, steps=128, batches=(1, 8, 32))
+                    tau=0.9, steps=128, batches=(1, 8, 32), heads=32, kv_heads=8)
 
 CONFIGS = {c.name: c for c in (TINY, GRANITE_1B, GRANITE_3B, OLMOE, MIXTRAL)}
 BY_ID = {c.cfg_id: c for c in CONFIGS.values()}

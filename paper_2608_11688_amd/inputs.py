@@ -29,7 +29,7 @@ from .configs import MoEConfig
 
 # stream tags
 TAG_H0, TAG_HZ, TAG_HPOST, TAG_WG, TAG_WPF, TAG_W1, TAG_W3, TAG_W2, TAG_BIAS, TAG_CDF, \
-    TAG_MISC = range(1, 12)
+    TAG_MISC, TAG_WQKV, TAG_WO, TAG_KCACHE, TAG_VCACHE = range(1, 16)
 
 AR_RHO = 0.7
 AR_SIGMA = 0.714
@@ -92,6 +92,33 @@ def expert_weights(cfg: MoEConfig, layer: int, expert: int, seed: int = 0):
         w *= np.float32(W_STD)
         out.append(to_bf16_bits(w))
     return tuple(out)
+
+
+def attention_weights(cfg: MoEConfig, layer: int, seed: int = 0):
+    """(W_qkv bits [(H + 2 G) * hd, d], W_o bits [d, H * hd]) of one decode-attention block.
+
+    Rows of W_qkv: the H query heads, then the G key heads, then the G value heads, hd rows
+    each.  Entries ~ N(0, 1/fan_in), so projections of unit-variance states have unit
+    variance.
+    """
+    H, G, hd, d = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.d
+    w_qkv = rng(seed, cfg.cfg_id, TAG_WQKV, layer).standard_normal(((H + 2 * G) * hd, d),
+                                                                   dtype=np.float32)
+    w_qkv *= np.float32(1.0 / np.sqrt(d))
+    w_o = rng(seed, cfg.cfg_id, TAG_WO, layer).standard_normal((d, H * hd), dtype=np.float32)
+    w_o *= np.float32(1.0 / np.sqrt(H * hd))
+    return to_bf16_bits(w_qkv), to_bf16_bits(w_o)
+
+
+def kv_cache(cfg: MoEConfig, layer: int, rows: int, ctx: int, seed: int = 0):
+    """(K bits, V bits), each [rows, G, ctx, hd] bf16, entries ~ N(0, 1): the cached keys
+    and values of `ctx` earlier tokens of every sequence."""
+    G, hd = cfg.n_kv_heads, cfg.head_dim
+    k = rng(seed, cfg.cfg_id, TAG_KCACHE, layer).standard_normal((rows, G, ctx, hd),
+                                                                 dtype=np.float32)
+    v = rng(seed, cfg.cfg_id, TAG_VCACHE, layer).standard_normal((rows, G, ctx, hd),
+                                                                 dtype=np.float32)
+    return to_bf16_bits(k), to_bf16_bits(v)
 
 
 def cdf_params(cfg: MoEConfig, layer: int, seed: int = 0):
