@@ -209,6 +209,30 @@ apex_status apex_moe_ffn_fp8(const float *x, int B, int d, int I, int E, int k,
                              size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Decode attention of one layer: the block that runs between the prefetch router and
+ * the gate, and whose duration the expert copies overlap (Sec. IV-A; Eq. 12).  The
+ * paper does not specify the block; this is grouped-query attention with H query
+ * heads, G key/value heads and head size hd (64 or 128; H a multiple of G with
+ * H / G in {1, 2, 3, 4, 8}).  For every token b:
+ *   [q; k; v] = W_qkv h[b]            (rows: H query heads, G key heads, G value heads,
+ *                                      hd rows each; W_qkv bf16 [(H + 2G) hd, d])
+ *   k and v are rounded to bf16 and written to position pos of the caches;
+ *   a_i = sum_{j <= pos} softmax_j(q_i . K_g[j] / sqrt(hd)) V_g[j],  g = i / (H / G);
+ *   o[b] = W_o [a_0; ...; a_{H-1}]    (W_o bf16 [d, H hd]).
+ * fp32 arithmetic, deterministic.
+ *   h          device fp32 [B, d]
+ *   k_cache, v_cache  device bf16 [B, G, ctx_max, hd]: positions 0..pos-1 are read,
+ *              position pos is written (0 <= pos < ctx_max)
+ *   o          device fp32 [B, d] out (overwritten)
+ *   workspace  device, >= apex_attention_workspace_bytes(B, H, G, hd, ctx_max) bytes
+ */
+size_t apex_attention_workspace_bytes(int B, int H, int G, int hd, int ctx_max);
+apex_status apex_attention_decode(const float *h, const uint16_t *w_qkv, const uint16_t *w_o,
+                                  int B, int d, int H, int G, int hd, uint16_t *k_cache,
+                                  uint16_t *v_cache, int ctx_max, int pos, float *o,
+                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Cache plan of one layer for one decode step (pure host function, no HIP calls).
  * The paper keeps a per-layer buffer that receives the prefetched set (Sec. V-C);
  * here each layer owns C persistent HBM slots.  Rule:

@@ -81,6 +81,9 @@ SIGNATURES = {
     "apex_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32, I32]),
     "apex_moe_ffn": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_fp8": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
+    "apex_attention_workspace_bytes": (SZ, [I32, I32, I32, I32, I32]),
+    "apex_attention_decode": (I32, [P, P, P, I32, I32, I32, I32, I32, P, P, I32, I32, P, P, SZ,
+                                    P]),
     "apex_plan_residency": (I32, [I32, I32, P, P, I32, I32, I64, P, P, P, P, P]),
     "apex_expert_prefetch": (I32, [P, P, I32, I32, SZ, P, P, I32, I32, I64, P, P, P, P, P, P, P,
                                    P, P, P]),
@@ -217,6 +220,16 @@ def apex_moe_ffn_fp8(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slot
     _call("apex_moe_ffn_fp8", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
           ptr(slot_of_expert), ptr(slots), n_slots, ptr(y), int(accumulate), ptr(workspace),
           workspace_bytes, stream)
+
+
+def apex_attention_workspace_bytes(B, H, G, hd, ctx_max):
+    return lib().apex_attention_workspace_bytes(B, H, G, hd, ctx_max)
+
+
+def apex_attention_decode(h, w_qkv, w_o, B, d, H, G, hd, k_cache, v_cache, ctx_max, pos, o,
+                          workspace, workspace_bytes, stream=None):
+    _call("apex_attention_decode", ptr(h), ptr(w_qkv), ptr(w_o), B, d, H, G, hd, ptr(k_cache),
+          ptr(v_cache), ctx_max, pos, ptr(o), ptr(workspace), workspace_bytes, stream)
 
 
 def apex_plan_residency(E, Cslots, pf_idx, pf_count, B, k_max, step, expert_of_slot, last_used,
