@@ -3,17 +3,20 @@
 
 One step = one decode token (batch B) through every MoE layer of the workload:
 prefetch router + adaptive K_p, cache plan + host-to-HBM expert copies on a side
-stream, attention-window stand-in, gate top-k (correctness-preserving mode by default),
+stream, the attention window (a spin of --t-attn-us, or with --window attention the
+layer's real decode attention), gate top-k (correctness-preserving mode by default),
 expert FFN over the HBM slots, miss correction.  Inputs (hidden states, routers, the
 HBM slot pools and the pinned host copy of every expert) are resident before timing.
 
 Prints one JSON line.  ``value`` is microseconds per token per MoE layer of the decode
-timeline with the attention-window stand-in subtracted (the MoE path's own cost
-including exposed stall); lower is better.
+timeline with the attention window subtracted (the spin's length, or the attention
+block's measured device time): the MoE path's own cost including exposed stall; lower
+is better.
 
     python bench.py [--steps K] [--warmup W] [--config granite-1b-a400m] [--batch 1]
                     [--mode exact|stall_free] [--policy cumprob|ordinal|static|none]
-                    [--static-delta D] [--tau T] [--weights bf16|fp8] [--t-attn-us 10]
+                    [--static-delta D] [--tau T] [--weights bf16|fp8]
+                    [--window spin|attention] [--t-attn-us 10] [--ctx 1024]
                     [--no-cpu-baseline]
 
 With --policy ordinal, every layer's coverage model is first fitted on held-out tokens
@@ -53,7 +56,12 @@ def parse():
                    help="expert weight format (fp8: E4M3 with fp32 row scales)")
     p.add_argument("--cdf-tokens", type=int, default=1024,
                    help="held-out tokens per layer for the ordinal-model fit")
-    p.add_argument("--t-attn-us", type=float, default=10.0)
+    p.add_argument("--t-attn-us", type=float, default=10.0,
+                   help="length of the spin that stands in for attention (--window spin)")
+    p.add_argument("--window", default="spin", choices=["spin", "attention"],
+                   help="attention window: a spin of --t-attn-us, or the layers' real decode "
+                        "attention over --ctx cached positions")
+    p.add_argument("--ctx", type=int, default=1024)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
     return p.parse_args()
@@ -115,6 +123,33 @@ def ffn_roofline_leg(torch, native, runner, reps=8, seed=123):
     nbytes = float(np.mean([plan[i % len(plan)][3] * runner.S + 2 * B * cfg.d * 4
                             for i in range(n)]))
     return ms, nbytes, n
+
+
+def attention_leg(torch, native, runner, reps=8):
+    """Device time of one layer's decode attention (apex_attention_decode) in the decode
+    launch configuration: calls cycling over the layers, queued behind a spin kernel,
+    one event pair around the batch.  Returns mean microseconds per call."""
+    cfg, B = runner.cfg, runner.B
+    H, G, hd = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
+    ws_bytes = native.apex_attention_workspace_bytes(B, H, G, hd, runner.ctx + 1)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    cs = runner.cs
+    n = reps * len(runner.layers)
+    e0, e1 = native.apex_event_create(True), native.apex_event_create(True)
+    torch.cuda.synchronize()
+    native.apex_spin_us(min(5000.0 + 30.0 * n, 1e6), cs)
+    native.apex_event_record(e0, cs)
+    for i in range(n):
+        b = runner.bufs[runner.layers[i % len(runner.layers)]]
+        native.apex_attention_decode(b["h_pre"][0], b["w_qkv"], b["w_o"], B, cfg.d, H, G, hd,
+                                     b["k_cache"], b["v_cache"], runner.ctx + 1, runner.ctx,
+                                     b["attn_out"], ws, ws_bytes, cs)
+    native.apex_event_record(e1, cs)
+    native.apex_event_synchronize(e1)
+    us = native.apex_event_elapsed_ms(e0, e1) * 1e3 / n
+    native.apex_event_destroy(e0)
+    native.apex_event_destroy(e1)
+    return us
 
 
 def copy_calibration(torch, native, cs, nbytes=256 << 20, reps=5):
@@ -214,7 +249,8 @@ def main():
     total = args.warmup + args.steps
     runner = DecodeRunner(cfg, batch=args.batch, mode=mode, tau=tau, steps=max(total, 1),
                           t_attn_us=args.t_attn_us, policy=policy,
-                          static_delta=args.static_delta, cdf=cdf, weights=args.weights)
+                          static_delta=args.static_delta, cdf=cdf, weights=args.weights,
+                          window=args.window, ctx=args.ctx)
     h2d_peak = pinned_h2d_peak(torch)
 
     for _ in range(args.warmup):
@@ -233,7 +269,9 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     L, B = len(runner.layers), args.batch
     us_layer_step = ms_per_step * 1e3 / L
-    value = (us_layer_step - args.t_attn_us) / B
+    attn_us = attention_leg(torch, native, runner) if args.window == "attention" else None
+    window_us = attn_us if attn_us is not None else args.t_attn_us
+    value = (us_layer_step - window_us) / B
     S = runner.S
     achieved = leg_bytes / (leg_ms * 1e-3) / 1e9
     s = runner.summary()
@@ -255,8 +293,9 @@ def main():
         "config": {"workload": cfg.name, "layers": L, "d": cfg.d, "E": cfg.E, "k": cfg.k,
                    "I": cfg.I, "C": cfg.C, "k_max": cfg.k_max, "tau": tau, "batch": B,
                    "mode": args.mode, "policy": args.policy, "weights": args.weights,
-                   "t_attn_us": args.t_attn_us},
+                   "window": args.window},
         "us_per_layer_step_incl_attn_window": round(us_layer_step, 3),
+        "attn_window_us": round(window_us, 3),
         "ffn_us": round(leg_ms * 1e3, 3),
         "ffn_hbm_GBps": round(achieved, 1),
         "recall": round(s["recall"], 5),
@@ -276,6 +315,10 @@ def main():
     }
     if args.policy == "static":
         out["config"]["static_delta"] = args.static_delta
+    if args.window == "attention":
+        out["config"].update(ctx=args.ctx, heads=cfg.n_heads, kv_heads=cfg.n_kv_heads)
+    else:
+        out["config"]["t_attn_us"] = args.t_attn_us
     if cdf_report is not None:
         out["ordinal_fit"] = cdf_report
     runner.close()

@@ -318,9 +318,15 @@ apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scr
  * Layers are processed in order on the compute stream, so a layer's router starts after
  * the previous layer's FFN, as in a model where each layer feeds the next.
  *
+ * With attn_heads > 0 the attention window is the layer's real decode attention
+ * (apex_attention_decode on h_pre, writing position attn_ctx of its caches) instead of
+ * the spin; its output goes to attn_out and does not feed the MoE input (layers draw
+ * their own hidden states).
+ *
  * apex_decode_create copies the configuration and the per-layer descriptors (the
  * buffers themselves stay caller-owned and must outlive the driver) and allocates the
- * driver's own events and pinned staging (setup time, not the hot path).
+ * driver's own events, pinned staging and attention workspace (setup time, not the hot
+ * path).
  */
 typedef struct {
     int L, B, d, E, k, I, C, k_max;
@@ -331,6 +337,9 @@ typedef struct {
     double t_attn_us;      /* attention-window stand-in per layer, >= 0 */
     int n_scratch;         /* miss-scratch slots (EXACT), >= min(E, B*k) recommended */
     int weights;           /* apex_weights: layout of host_experts, slots and scratch */
+    int attn_heads;        /* > 0: the attention window is apex_attention_decode with this */
+    int attn_kv_heads;     /*   many query / key-value heads over attn_ctx cached positions */
+    int attn_ctx;          /*   (caches hold attn_ctx + 1 positions); 0: spin t_attn_us  */
 } apex_decode_config;
 
 typedef struct {
@@ -343,6 +352,9 @@ typedef struct {
     uint8_t *avail_dev;                    /* device uint8 [E] resident mask */
     int32_t *expert_of_slot;               /* host int32 [C] in/out */
     int64_t *last_used;                    /* host int64 [E] in/out */
+    const uint16_t *w_qkv, *w_o;           /* attention window only: device bf16 weights, */
+    uint16_t *k_cache, *v_cache;           /*   caches [B, G, attn_ctx + 1, hd] and the    */
+    float *attn_out;                       /*   block's output [B, d]; NULL otherwise      */
 } apex_decode_layer;
 
 typedef struct {   /* counters the driver adds to at every layer-step */

@@ -1,7 +1,7 @@
 // Decode attention of one layer (apex_attention_decode): the block whose run time the
 // expert prefetch overlaps.
 //
-// Three launches per call:
+// Four launches per call:
 //   attn_qkv    grid (ceil(R / 4), B), R = (H + 2G) * hd: one wavefront per row of W_qkv,
 //               all loads of the row issued before the multiplies.  Query rows go to the
 //               workspace (fp32); key and value rows are rounded to bf16 and stored at
@@ -14,8 +14,9 @@
 //               are merged with the log-sum-exp rule, across the wavefront by shuffles
 //               and across wavefronts in LDS.  Output per (token, head, split):
 //               hd weighted sums, the maximum and the normaliser.
-//   attn_out    grid (ceil(d / 16), B): merges the splits of every head into the
-//               attention vector in LDS, then one wavefront per 4 rows of W_o.
+//   attn_merge  grid (H, B): the splits of one head merged (log-sum-exp rule) into the
+//               attention vector, all of its loads issued at once.
+//   attn_out    grid (ceil(d / 4), B): one wavefront per row of W_o.
 // fp32 arithmetic on bf16 weights and caches; no atomics, so results are deterministic.
 #include <hip/hip_runtime.h>
 
@@ -35,7 +36,8 @@ using apex::ffn::wave_sum;
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxGroup = 8;       // query heads per key/value head
-constexpr int kOutRows = 16;       // W_o rows per attn_out workgroup
+constexpr int kOutRows = kWaves;   // W_o rows per attn_out workgroup (one per wavefront)
+constexpr int kMaxSplits = kThreads;   // position splits (one merge thread each)
 
 __device__ __forceinline__ uint16_t bf16_bits(float v) {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
@@ -202,28 +204,62 @@ __global__ __launch_bounds__(kThreads) void attn_split(
     }
 }
 
-__global__ __launch_bounds__(kThreads) void attn_out(
-    const float *__restrict__ part, int S, const uint16_t *__restrict__ w_o, int d, int H,
-    int hd, float *__restrict__ o) {
+// attn_merge: grid (H, B).  The splits of one query head merged by the log-sum-exp
+// rule: every thread loads its share of the splits' values at once (S * hd / 256 of
+// them), then the partial sums meet in LDS.  a [B, H * hd] out.
+__global__ __launch_bounds__(kThreads) void attn_merge(const float *__restrict__ part, int S,
+                                                       int H, int hd, float *__restrict__ a) {
+    __shared__ float w[kMaxSplits];
+    __shared__ float red[kWaves];
+    __shared__ float num[kThreads];
+    const int head = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+    const int wave = t / kWave, lane = t % kWave;
+    const float *p = part + (size_t(b) * H + head) * S * (hd + 2);
+    // maximum over the splits
+    float m = t < S ? p[size_t(t) * (hd + 2) + hd] : -INFINITY;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+    if (lane == 0) red[wave] = m;
+    __syncthreads();
+    const float M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    __syncthreads();
+    // split weights exp(m_s - M) and the normaliser
+    float den = 0.f;
+    if (t < S) {
+        const float ms = p[size_t(t) * (hd + 2) + hd];
+        const float ws = ms == -INFINITY ? 0.f : expf(ms - M);
+        w[t] = ws;
+        den = ws * p[size_t(t) * (hd + 2) + hd + 1];
+    }
+    den = wave_sum(den);
+    if (lane == 0) red[wave] = den;
+    __syncthreads();
+    const float D = red[0] + red[1] + red[2] + red[3];
+    // weighted sums: thread t takes dimension t % hd of splits t / hd, t / hd + 256 / hd, ...
+    const int dim = t % hd, s0 = t / hd, step = kThreads / hd;
+    float acc = 0.f;
+#pragma unroll 8
+    for (int s = s0; s < S; s += step) acc = fmaf(w[s], p[size_t(s) * (hd + 2) + dim], acc);
+    num[t] = acc;
+    __syncthreads();
+    if (t < hd) {
+        float sum = 0.f;
+        for (int g = 0; g < step; ++g) sum += num[g * hd + t];
+        a[(size_t(b) * H + head) * hd + t] = sum / D;
+    }
+}
+
+// attn_out: grid (ceil(d / 4), B): o[b, r] = W_o[r] . a[b], one row per wavefront, a[b]
+// staged in LDS.
+__global__ __launch_bounds__(kThreads) void attn_out(const float *__restrict__ a,
+                                                     const uint16_t *__restrict__ w_o, int d,
+                                                     int H, int hd, float *__restrict__ o) {
     extern __shared__ float a_lds[];           // [H * hd]
     const int b = blockIdx.y;
     const int qrows = H * hd;
-    for (int idx = threadIdx.x; idx < qrows; idx += kThreads) {
-        const int head = idx / hd, dim = idx % hd;
-        const float *p = part + (size_t(b) * H + head) * S * (hd + 2);
-        float mm = -INFINITY;
-        for (int s = 0; s < S; ++s) mm = fmaxf(mm, p[s * (hd + 2) + hd]);
-        float num = 0.f, den = 0.f;
-        for (int s = 0; s < S; ++s) {
-            const float *ps = p + s * (hd + 2);
-            const float ms = ps[hd];
-            if (ms == -INFINITY) continue;
-            const float c = expf(ms - mm);
-            num = fmaf(c, ps[dim], num);
-            den = fmaf(c, ps[hd + 1], den);
-        }
-        a_lds[idx] = num / den;
-    }
+    for (int idx = threadIdx.x; idx < qrows / 4; idx += kThreads)
+        reinterpret_cast<float4 *>(a_lds)[idx] =
+            reinterpret_cast<const float4 *>(a + size_t(b) * qrows)[idx];
     __syncthreads();
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int nch = qrows / 8;
@@ -232,9 +268,9 @@ __global__ __launch_bounds__(kThreads) void attn_out(
         const uint4 *row = reinterpret_cast<const uint4 *>(w_o + size_t(r) * qrows);
         float acc = 0.f;
         for (int c = lane; c < nch; c += kWave) {
-            const float4 a = *reinterpret_cast<const float4 *>(&a_lds[8 * c]);
-            const float4 bb = *reinterpret_cast<const float4 *>(&a_lds[8 * c + 4]);
-            acc = dot8(row[c], a, bb, acc);
+            const float4 x0 = *reinterpret_cast<const float4 *>(&a_lds[8 * c]);
+            const float4 x1 = *reinterpret_cast<const float4 *>(&a_lds[8 * c + 4]);
+            acc = dot8(row[c], x0, x1, acc);
         }
         acc = wave_sum(acc);
         if (lane == 0) o[size_t(b) * d + r] = acc;
@@ -248,15 +284,13 @@ int pick_splits(int n_pos, int B, int G) {
     return std::max(1, std::min(want, most));
 }
 
-constexpr int kMaxSplits = 256;
-
 }  // namespace
 
 extern "C" size_t apex_attention_workspace_bytes(int B, int H, int G, int hd, int ctx_max) {
     if (B <= 0 || H <= 0 || G <= 0 || hd <= 0 || ctx_max <= 0) return 256;
-    const size_t qb = apex::align_up(size_t(B) * H * hd * sizeof(float), 256);
+    const size_t qb = apex::align_up(size_t(B) * H * hd * sizeof(float), 256);   // q, a
     const size_t pb = size_t(B) * H * kMaxSplits * (hd + 2) * sizeof(float);
-    return qb + apex::align_up(pb, 256);
+    return 2 * qb + apex::align_up(pb, 256);
 }
 
 extern "C" apex_status apex_attention_decode(const float *h, const uint16_t *w_qkv,
@@ -288,9 +322,10 @@ extern "C" apex_status apex_attention_decode(const float *h, const uint16_t *w_q
                           need);
     const int n_pos = pos + 1;
     const int S = std::min(pick_splits(n_pos, B, G), kMaxSplits);
+    const size_t qb = apex::align_up(size_t(B) * H * hd * sizeof(float), 256);
     float *q = static_cast<float *>(workspace);
-    float *part = reinterpret_cast<float *>(
-        static_cast<char *>(workspace) + apex::align_up(size_t(B) * H * hd * sizeof(float), 256));
+    float *a = reinterpret_cast<float *>(static_cast<char *>(workspace) + qb);
+    float *part = reinterpret_cast<float *>(static_cast<char *>(workspace) + 2 * qb);
 
     const int R = (H + 2 * G) * hd;
     const int nch = d / 8;
@@ -328,9 +363,11 @@ extern "C" apex_status apex_attention_decode(const float *h, const uint16_t *w_q
 #undef APEX_SPLIT_HD
 #undef APEX_SPLIT
     APEX_HIP(hipGetLastError());
+    hipLaunchKernelGGL(attn_merge, dim3(H, B), dim3(kThreads), 0, stream, part, S, H, hd, a);
+    APEX_HIP(hipGetLastError());
     const dim3 go((d + kOutRows - 1) / kOutRows, B);
-    hipLaunchKernelGGL(attn_out, go, dim3(kThreads), size_t(H) * hd * sizeof(float), stream, part,
-                       S, w_o, d, H, hd, o);
+    hipLaunchKernelGGL(attn_out, go, dim3(kThreads), size_t(H) * hd * sizeof(float), stream, a,
+                       w_o, d, H, hd, o);
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }

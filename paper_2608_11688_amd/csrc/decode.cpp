@@ -25,6 +25,9 @@ struct apex_decode {
     size_t ws_bytes = 0;
     hipStream_t compute = nullptr, side = nullptr;
     size_t expert_bytes = 0;
+    // attention window (attn_heads > 0)
+    void *attn_ws = nullptr;
+    size_t attn_ws_bytes = 0;
     // pinned staging
     int32_t *pf_idx_h = nullptr;      // [B][k_max]
     int32_t *pf_count_h = nullptr;    // [B]
@@ -130,11 +133,23 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     APEX_REQUIRE(c.mode != APEX_MODE_EXACT || (scratch && miss_table_dev && c.n_scratch >= 1),
                  "%s: EXACT mode needs a miss scratch pool", fn);
     APEX_REQUIRE(exec_idx_dev && exec_gate_dev && workspace, "%s: NULL buffer", fn);
+    const bool attn = c.attn_heads > 0;
+    if (attn) {
+        APEX_REQUIRE(c.attn_kv_heads >= 1 && c.attn_ctx >= 0 && c.d % c.attn_heads == 0,
+                     "%s: attention window: heads=%d kv_heads=%d ctx=%d d=%d", fn, c.attn_heads,
+                     c.attn_kv_heads, c.attn_ctx, c.d);
+        const int hd = c.d / c.attn_heads;
+        APEX_REQUIRE((hd == 64 || hd == 128) && c.attn_heads % c.attn_kv_heads == 0,
+                     "%s: attention window: head size %d, heads %d, kv heads %d", fn, hd,
+                     c.attn_heads, c.attn_kv_heads);
+    }
     for (int l = 0; l < c.L; ++l) {
         const apex_decode_layer &y = layers[l];
         APEX_REQUIRE(y.w_pf && y.w_g && y.host_experts && y.slots && y.slot_of_expert_dev &&
                          y.expert_of_slot && y.last_used,
                      "%s: layer %d has a NULL buffer", fn, l);
+        APEX_REQUIRE(!attn || (y.w_qkv && y.w_o && y.k_cache && y.v_cache && y.attn_out),
+                     "%s: layer %d has no attention buffers", fn, l);
     }
     auto *dec = new apex_decode();
     dec->cfg = c;
@@ -179,6 +194,14 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
         if (mk(&dec->ready[l]) != hipSuccess || mk(&dec->readers_done[l]) != hipSuccess ||
             mk(&dec->gate_done[l]) != hipSuccess)
             return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
+    if (attn) {
+        dec->attn_ws_bytes = apex_attention_workspace_bytes(c.B, c.attn_heads, c.attn_kv_heads,
+                                                            c.d / c.attn_heads, c.attn_ctx + 1);
+        e = hipMalloc(&dec->attn_ws, dec->attn_ws_bytes);
+        if (e != hipSuccess)
+            return cleanup(apex::fail(APEX_E_HIP, "%s: hipMalloc failed: %s", fn,
+                                      hipGetErrorString(e)));
+    }
     *out = dec;
     return APEX_OK;
 }
@@ -208,7 +231,13 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
             std::fill(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max, -1);
             std::fill(dec->pf_count_h, dec->pf_count_h + c.B, 0);
         }
-        if (c.t_attn_us > 0) {
+        if (c.attn_heads > 0) {
+            st = apex_attention_decode(h_pre[l], Ly.w_qkv, Ly.w_o, c.B, c.d, c.attn_heads,
+                                       c.attn_kv_heads, c.d / c.attn_heads, Ly.k_cache,
+                                       Ly.v_cache, c.attn_ctx + 1, c.attn_ctx, Ly.attn_out,
+                                       dec->attn_ws, dec->attn_ws_bytes, cs);
+            if (st != APEX_OK) return st;
+        } else if (c.t_attn_us > 0) {
             st = apex_spin_us(c.t_attn_us, cs);
             if (st != APEX_OK) return st;
         }
@@ -317,6 +346,7 @@ extern "C" apex_status apex_decode_destroy(apex_decode *dec) {
     for (void *p : {static_cast<void *>(dec->pf_idx_h), static_cast<void *>(dec->pf_count_h),
                     static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h)})
         if (p) (void)hipHostFree(p);
+    if (dec->attn_ws) (void)hipFree(dec->attn_ws);
     delete dec;
     return APEX_OK;
 }

@@ -121,6 +121,22 @@ def kv_cache(cfg: MoEConfig, layer: int, rows: int, ctx: int, seed: int = 0):
     return to_bf16_bits(k), to_bf16_bits(v)
 
 
+def kv_cache_device(torch, cfg: MoEConfig, layer: int, rows: int, ctx: int, seed: int = 0,
+                    device="cuda"):
+    """Like ``kv_cache`` but drawn on the device (torch's generator, seeded from the same
+    stream key), for caches too large to draw on the host: (K, V) int16 tensors holding
+    bf16 bits, [rows, G, ctx, hd] each."""
+    G, hd = cfg.n_kv_heads, cfg.head_dim
+    out = []
+    for tag in (TAG_KCACHE, TAG_VCACHE):
+        key = np.random.SeedSequence([int(seed), int(cfg.cfg_id), tag, int(layer)])
+        g = torch.Generator(device=device)
+        g.manual_seed(int(key.generate_state(1, np.uint64)[0] & 0x7FFFFFFFFFFFFFFF))
+        x = torch.randn((rows, G, ctx, hd), generator=g, device=device, dtype=torch.float32)
+        out.append(x.to(torch.bfloat16).view(torch.int16))
+    return tuple(out)
+
+
 def cdf_params(cfg: MoEConfig, layer: int, seed: int = 0):
     """Random ordinal-model parameters (w fp32 [E], theta fp32 [E-k+1], non-decreasing).
 

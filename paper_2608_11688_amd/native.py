@@ -46,13 +46,15 @@ I32, I64, F32, F64, SZ = C.c_int, C.c_int64, C.c_float, C.c_double, C.c_size_t
 class DecodeConfig(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("L", "B", "d", "E", "k", "I", "C", "k_max", "policy")] + [
         ("tau", C.c_float), ("static_delta", C.c_int), ("mode", C.c_int),
-        ("t_attn_us", C.c_double), ("n_scratch", C.c_int), ("weights", C.c_int)]
+        ("t_attn_us", C.c_double), ("n_scratch", C.c_int), ("weights", C.c_int),
+        ("attn_heads", C.c_int), ("attn_kv_heads", C.c_int), ("attn_ctx", C.c_int)]
 
 
 class DecodeLayer(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in (
         "w_pf", "w_g", "b_pf", "b_g", "cdf_w", "cdf_theta", "host_experts", "slots",
-        "slot_of_expert_dev", "avail_dev", "expert_of_slot", "last_used")]
+        "slot_of_expert_dev", "avail_dev", "expert_of_slot", "last_used", "w_qkv", "w_o",
+        "k_cache", "v_cache", "attn_out")]
 
 
 class DecodeStats(C.Structure):

@@ -45,7 +45,7 @@ class DecodeRunner:
     def __init__(self, cfg: configs.MoEConfig, batch=1, mode=EXACT, tau=None,
                  policy=native.SEL_CUMPROB, static_delta=0, seed=0, steps=None, t_attn_us=10.0,
                  layers=None, n_scratch=None, record=False, cdf=None, gen_threads=16,
-                 weights="bf16"):
+                 weights="bf16", window="spin", ctx=1024):
         torch = _torch()
         self.torch = torch
         self.cfg, self.B, self.mode = cfg, batch, mode
@@ -62,6 +62,9 @@ class DecodeRunner:
         if weights not in ("bf16", "fp8"):
             raise ValueError(f"weights must be 'bf16' or 'fp8', not {weights!r}")
         self.weights = weights
+        if window not in ("spin", "attention"):
+            raise ValueError(f"window must be 'spin' or 'attention', not {window!r}")
+        self.window, self.ctx = window, ctx
         self.S = (native.apex_expert_bytes_fp8(cfg.d, cfg.I) if weights == "fp8"
                   else native.apex_expert_bytes(cfg.d, cfg.I))
         E, B, k = cfg.E, batch, cfg.k
@@ -88,7 +91,9 @@ class DecodeRunner:
                                    static_delta=static_delta, mode=mode, t_attn_us=t_attn_us,
                                    n_scratch=self.n_scratch,
                                    weights=(native.WEIGHTS_FP8_E4M3 if weights == "fp8"
-                                            else native.WEIGHTS_BF16))
+                                            else native.WEIGHTS_BF16),
+                                   attn_heads=cfg.n_heads if window == "attention" else 0,
+                                   attn_kv_heads=cfg.n_kv_heads, attn_ctx=ctx)
         descs = []
         for l in self.layers:
             b = self.bufs[l]
@@ -98,7 +103,9 @@ class DecodeRunner:
                 cdf_w=p(b["cdf_w"]), cdf_theta=p(b["cdf_theta"]),
                 host_experts=p(b["host"]), slots=p(b["slots"]),
                 slot_of_expert_dev=p(b["slot_dev"]), avail_dev=p(b["avail_dev"]),
-                expert_of_slot=b["eos"].ctypes.data, last_used=b["last_used"].ctypes.data))
+                expert_of_slot=b["eos"].ctypes.data, last_used=b["last_used"].ctypes.data,
+                w_qkv=p(b.get("w_qkv")), w_o=p(b.get("w_o")), k_cache=p(b.get("k_cache")),
+                v_cache=p(b.get("v_cache")), attn_out=p(b.get("attn_out"))))
         self.dec, self._descs = native.apex_decode_create(
             dcfg, descs, self.scratch, self.miss_table, self.exec_idx, self.exec_gate, self.ws,
             self.ws_bytes, self.cs, self.ss)
@@ -151,6 +158,13 @@ class DecodeRunner:
                    slot_dev=to_dev(table), avail_dev=to_dev((table >= 0).astype(np.uint8)),
                    eos=eos, last_used=np.full(cfg.E, -1, np.int64), h_pre=to_dev(h_pre),
                    h_post=to_dev(h_post), cdf_w=None, cdf_theta=None)
+        if self.window == "attention":
+            w_qkv, w_o = inputs.attention_weights(cfg, l, self.seed)
+            out["w_qkv"] = to_dev(w_qkv.view(np.int16))
+            out["w_o"] = to_dev(w_o.view(np.int16))
+            out["k_cache"], out["v_cache"] = inputs.kv_cache_device(
+                torch, cfg, l, self.B, self.ctx + 1, self.seed, self.dev)
+            out["attn_out"] = torch.zeros((self.B, cfg.d), dtype=torch.float32, device=self.dev)
         if self.policy == native.SEL_ORDINAL_CDF:
             if cdf is None:
                 w, theta = inputs.cdf_params(cfg, l, self.seed)

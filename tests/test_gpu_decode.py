@@ -18,13 +18,14 @@ pytestmark = pytest.mark.gpu
 
 
 def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau=None,
-                 ffn_every=1, cdf=None, weights="bf16"):
+                 ffn_every=1, cdf=None, weights="bf16", window="spin"):
     """cdf: {layer: (w, theta)} for the ORDINAL policy; seeded random models if None."""
     from paper_2608_11688_amd.runtime import DecodeRunner
     tau = cfg.tau if tau is None else tau
     tau32 = float(np.float32(tau))
     runner = DecodeRunner(cfg, batch=batch, mode=mode, tau=tau32, policy=policy, steps=steps,
-                          layers=layers, t_attn_us=2.0, record=True, cdf=cdf, weights=weights)
+                          layers=layers, t_attn_us=2.0, record=True, cdf=cdf, weights=weights,
+                          window=window, ctx=128)
     ledger = TieLedger()
     res = {l: Residency(cfg.E, cfg.C) for l in layers}
     routers = {l: inputs.router_weights(cfg, l) for l in layers}
@@ -156,3 +157,33 @@ def test_decode_granite1b_fp8_experts(mode):
 def test_decode_olmoe_batch16_fp8_experts():
     cfg = configs.OLMOE
     check_decode(cfg, 16, native.MODE_EXACT, 2, [3], ffn_every=1, weights="fp8")
+
+
+def test_decode_with_attention_window():
+    # the window is the layers' real decode attention: the MoE path is unchanged, and every
+    # step's attention output matches the oracle's block on the same caches
+    from oracle import attention as oatt
+    from paper_2608_11688_amd.runtime import DecodeRunner
+    cfg = configs.GRANITE_1B
+    check_decode(cfg, 1, native.MODE_EXACT, 3, [0, 11], window="attention")
+    layers, steps, ctx, B = [2, 17], 3, 200, 2
+    H, G, hd = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
+    runner = DecodeRunner(cfg, batch=B, mode=native.MODE_STALL_FREE, steps=steps, layers=layers,
+                          record=True, window="attention", ctx=ctx)
+    try:
+        caches = {l: tuple(runner.bufs[l][n].cpu().numpy().view(np.uint16)
+                           for n in ("k_cache", "v_cache")) for l in layers}
+        weights = {l: inputs.attention_weights(cfg, l) for l in layers}
+        hs = {l: inputs.hidden_states(cfg, l, B, steps)[0] for l in layers}
+        worst = 0.0
+        for t in range(steps):
+            runner.step()
+            for l in layers:
+                got = runner.bufs[l]["attn_out"].cpu().numpy().astype(np.float64)
+                ref = oatt.attention_block(hs[l][t], *weights[l], *caches[l], H, G, hd, ctx)["o"]
+                err = np.abs(got - ref).max() / np.abs(ref).max()
+                assert err <= 1e-4, (t, l, err)
+                worst = max(worst, err)
+        print("attention window worst rel err", worst)
+    finally:
+        runner.close()
