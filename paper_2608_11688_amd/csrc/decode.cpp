@@ -133,6 +133,9 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     APEX_REQUIRE(c.mode != APEX_MODE_EXACT || (scratch && miss_table_dev && c.n_scratch >= 1),
                  "%s: EXACT mode needs a miss scratch pool", fn);
     APEX_REQUIRE(exec_idx_dev && exec_gate_dev && workspace, "%s: NULL buffer", fn);
+    if (workspace_bytes < apex_moe_ffn_workspace_bytes(c.B, c.d, c.I, c.k))
+        return apex::fail(APEX_E_CAPACITY, "%s: workspace %zu < %zu bytes", fn, workspace_bytes,
+                          apex_moe_ffn_workspace_bytes(c.B, c.d, c.I, c.k));
     const bool attn = c.attn_heads > 0;
     if (attn) {
         APEX_REQUIRE(c.attn_kv_heads >= 1 && c.attn_ctx >= 0 && c.d % c.attn_heads == 0,

@@ -102,11 +102,14 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1(
     int d, int I, int E, int k, const int32_t *__restrict__ exec_idx,
     const int32_t *__restrict__ slot_of_expert, const uint16_t *__restrict__ slots, int n_slots,
     size_t slot_elems, const float *__restrict__ h, float *__restrict__ y, int accumulate) {
+    // W2 of valid position idx starts at chunk meta_w2[idx] of the slot pool (offsets, not
+    // pointers, so that the loads stay global loads and do not wait on LDS traffic)
     __shared__ int meta_pos[APEX_MAX_EXPERTS];
-    __shared__ const uint4 *meta_w2[APEX_MAX_EXPERTS];
+    __shared__ size_t meta_w2[APEX_MAX_EXPERTS];
     __shared__ int n_valid;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int nch = I / 8;
+    const uint4 *pool = reinterpret_cast<const uint4 *>(slots);
     if (wave == 0) {
         const int e = lane < k ? exec_idx[lane] : -1;
         const int s = (e >= 0 && e < E) ? slot_of_expert[e] : -1;
@@ -115,8 +118,7 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1(
         if (ok) {
             const int idx = __popcll(m & ((1ull << lane) - 1ull));
             meta_pos[idx] = lane;
-            meta_w2[idx] = reinterpret_cast<const uint4 *>(slots + size_t(s) * slot_elems +
-                                                           size_t(2) * I * d);
+            meta_w2[idx] = (size_t(s) * slot_elems + size_t(2) * I * d) / 8;
         }
         if (lane == 0) n_valid = __popcll(m);
     }
@@ -139,7 +141,7 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1(
         for (int u = 0; u < UNR; ++u) {
             on[u] = t0 + u * kWave < total;
             if (on[u]) {
-                const uint4 *w2 = meta_w2[it];
+                const uint4 *w2 = pool + meta_w2[it];
                 const float4 *hr = reinterpret_cast<const float4 *>(h + size_t(meta_pos[it]) * I);
                 ha[u] = hr[2 * cc];
                 hb[u] = hr[2 * cc + 1];

@@ -92,12 +92,16 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1_e4m3(
     int d, int I, int E, int k, const int32_t *__restrict__ exec_idx,
     const int32_t *__restrict__ slot_of_expert, const uint8_t *__restrict__ slots, int n_slots,
     size_t slot_bytes, const float *__restrict__ h, float *__restrict__ y, int accumulate) {
+    // offsets into the slot pool (16-byte chunks for W2, floats for its row scales), not
+    // pointers, so that the loads stay global loads and do not wait on LDS traffic
     __shared__ int meta_pos[APEX_MAX_EXPERTS];
-    __shared__ const uint4 *meta_w2[APEX_MAX_EXPERTS];
-    __shared__ const float *meta_s2[APEX_MAX_EXPERTS];
+    __shared__ size_t meta_w2[APEX_MAX_EXPERTS];
+    __shared__ size_t meta_s2[APEX_MAX_EXPERTS];
     __shared__ int n_valid;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int nch = I / 16;
+    const uint4 *pool = reinterpret_cast<const uint4 *>(slots);
+    const float *pool_f = reinterpret_cast<const float *>(slots);
     if (wave == 0) {
         const int e = lane < k ? exec_idx[lane] : -1;
         const int s = (e >= 0 && e < E) ? slot_of_expert[e] : -1;
@@ -105,10 +109,10 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1_e4m3(
         const unsigned long long m = __ballot(ok);
         if (ok) {
             const int idx = __popcll(m & ((1ull << lane) - 1ull));
-            const uint8_t *slot = slots + size_t(s) * slot_bytes;
+            const size_t base = size_t(s) * slot_bytes;
             meta_pos[idx] = lane;
-            meta_w2[idx] = reinterpret_cast<const uint4 *>(slot + size_t(2) * I * d);
-            meta_s2[idx] = reinterpret_cast<const float *>(slot + size_t(3) * I * d) + 2 * I;
+            meta_w2[idx] = (base + size_t(2) * I * d) / 16;
+            meta_s2[idx] = (base + size_t(3) * I * d) / 4 + 2 * size_t(I);
         }
         if (lane == 0) n_valid = __popcll(m);
     }
@@ -131,8 +135,8 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1_e4m3(
         for (int u = 0; u < UNR; ++u) {
             on[u] = t0 + u * kWave < total;
             if (on[u]) {
-                const uint4 *w2 = meta_w2[it];
-                const float *s2 = meta_s2[it];
+                const uint4 *w2 = pool + meta_w2[it];
+                const float *s2 = pool_f + meta_s2[it];
                 const float4 *hr = reinterpret_cast<const float4 *>(h + size_t(meta_pos[it]) * I);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) hx[u][q] = hr[4 * cc + q];
