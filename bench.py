@@ -11,13 +11,14 @@ HBM slot pools and the pinned host copy of every expert) are resident before tim
 Prints one JSON line.  ``value`` is microseconds per token per MoE layer of the decode
 timeline with the attention window subtracted (the spin's length, or the attention
 block's measured device time): the MoE path's own cost including exposed stall; lower
-is better.
+is better.  The same timeline with every expert resident in HBM (no copies, no misses)
+is timed after it; the difference is the exposed stall.
 
     python bench.py [--steps K] [--warmup W] [--config granite-1b-a400m] [--batch 1]
                     [--mode exact|stall_free] [--policy cumprob|ordinal|static|none]
                     [--static-delta D] [--tau T] [--weights bf16|fp8]
                     [--window spin|attention] [--t-attn-us 10] [--ctx 1024]
-                    [--no-cpu-baseline]
+                    [--no-compute-only] [--no-cpu-baseline]
 
 With --policy ordinal, every layer's coverage model is first fitted on held-out tokens
 (the method's training stage, outside the timed region).
@@ -63,6 +64,8 @@ def parse():
                         "attention over --ctx cached positions")
     p.add_argument("--ctx", type=int, default=1024)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-compute-only", action="store_true",
+                   help="skip the all-resident run that the exposed stall is measured against")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
     return p.parse_args()
 
@@ -196,6 +199,44 @@ def measured_traffic(cfg, batch, weights="bf16"):
     return None
 
 
+def time_steps(torch, runner, steps, warmup):
+    """Runs warmup untimed steps, then times `steps` decode steps; ms per step."""
+    for _ in range(warmup):
+        runner.step()
+    runner.reset_metrics()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        runner.step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    runner.finish()
+    return (t1 - t0) * 1e3 / steps
+
+
+def compute_only_leg(torch, args, cfg, make_runner):
+    """The same decode with every expert resident in HBM (C = E): the same kernels, no
+    copies and no misses.  Returns ms per step."""
+    import dataclasses
+    runner = make_runner(dataclasses.replace(cfg, C=cfg.E, k_max=min(cfg.k_max, cfg.E)))
+    try:
+        return time_steps(torch, runner, args.steps, args.warmup)
+    finally:
+        runner.close()
+
+
+def delta_star_leg(cfg, tokens=256, max_layers=8):
+    """Mean delta* (Eq. 3: how deep in the prefetch ranking the deepest routed expert
+    sits, beyond k) over held-out tokens of up to `max_layers` evenly spaced layers,
+    from the router and gate kernels."""
+    from paper_2608_11688_amd import cdf_fit
+    layers = sorted(set(np.linspace(0, cfg.L - 1, min(cfg.L, max_layers)).astype(int).tolist()))
+    d = [cdf_fit.collect_samples(cfg, l, tokens)[1] for l in layers]
+    d = np.concatenate(d)
+    return dict(mean=round(float(d.mean()), 4), p90=int(np.percentile(d, 90)),
+                tokens=int(d.size), layers=layers)
+
+
 def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=None,
                  weights="bf16"):
     """The oracle, as it stands, on the first layer-steps of the same workload."""
@@ -247,26 +288,19 @@ def main():
         from paper_2608_11688_amd import cdf_fit
         cdf, cdf_report = cdf_fit.fit_model(cfg, tokens=args.cdf_tokens)
     total = args.warmup + args.steps
-    runner = DecodeRunner(cfg, batch=args.batch, mode=mode, tau=tau, steps=max(total, 1),
-                          t_attn_us=args.t_attn_us, policy=policy,
-                          static_delta=args.static_delta, cdf=cdf, weights=args.weights,
-                          window=args.window, ctx=args.ctx)
-    h2d_peak = pinned_h2d_peak(torch)
 
-    for _ in range(args.warmup):
-        runner.step()
-    runner.reset_metrics()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        runner.step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    runner.finish()
+    def make_runner(c):
+        return DecodeRunner(c, batch=args.batch, mode=mode, tau=tau, steps=max(total, 1),
+                            t_attn_us=args.t_attn_us, policy=policy,
+                            static_delta=args.static_delta, cdf=cdf, weights=args.weights,
+                            window=args.window, ctx=args.ctx)
+
+    runner = make_runner(cfg)
+    h2d_peak = pinned_h2d_peak(torch)
+    ms_per_step = time_steps(torch, runner, args.steps, args.warmup)
     leg_ms, leg_bytes, leg_n = ffn_roofline_leg(torch, native, runner)
     calib = copy_calibration(torch, native, runner.cs)
 
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
     L, B = len(runner.layers), args.batch
     us_layer_step = ms_per_step * 1e3 / L
     attn_us = attention_leg(torch, native, runner) if args.window == "attention" else None
@@ -276,6 +310,14 @@ def main():
     achieved = leg_bytes / (leg_ms * 1e-3) / 1e9
     s = runner.summary()
     copied_bytes_per_step = s["copies_per_layer_step"] * L * S
+    runner.close()
+    # exposed stall: this timeline against the same one with every expert resident
+    value_resident = stall = None
+    if not args.no_compute_only:
+        ms_res = compute_only_leg(torch, args, cfg, make_runner)
+        value_resident = (ms_res * 1e3 / L - window_us) / B
+        stall = value - value_resident
+    dstar = delta_star_leg(cfg)
     out = {
         "metric": "MoE-layer decode us/token + expert-weight HBM GB/s; prefetch recall vs oracle",
         "value": round(value, 3),
@@ -302,8 +344,14 @@ def main():
         "full_coverage": round(s["full_coverage"], 5),
         "mean_delta_hat": None if args.policy == "none" else round(s["mean_delta_hat"], 4),
         "cache_hit_rate": round(s["hit_rate"], 5),
+        "mean_delta_star": dstar["mean"],
+        "delta_star": dstar,
         "copies_per_layer_step": round(s["copies_per_layer_step"], 4),
+        "copied_MB_per_layer_step": round(s["copies_per_layer_step"] * S / 1e6, 3),
         "misses_per_layer_step": round(s["misses_per_layer_step"], 4),
+        "compute_only_us_per_token_layer": (None if value_resident is None
+                                            else round(value_resident, 3)),
+        "exposed_stall_us_per_token_layer": None if stall is None else round(stall, 3),
         "h2d_GBps_over_step": round(copied_bytes_per_step / (ms_per_step * 1e-3) / 1e9, 2),
         "h2d_pinned_peak_GBps": round(h2d_peak, 2),
         "hbm_copy_kernel": calib,
@@ -321,7 +369,6 @@ def main():
         out["config"]["t_attn_us"] = args.t_attn_us
     if cdf_report is not None:
         out["ordinal_fit"] = cdf_report
-    runner.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, B, mode, tau, args.cpu_budget_s, policy,
                                            args.static_delta, cdf, args.weights)
