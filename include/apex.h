@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define APEX_ABI_VERSION 2
+#define APEX_ABI_VERSION 3
 #define APEX_MAX_EXPERTS 64
 #define APEX_MAX_PAIRS 1024     /* B * k limit of apex_moe_ffn */
 
@@ -312,11 +312,18 @@ apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scr
  *   compute: apex_prefetch_route (K_p written to pinned host memory); attention-window
  *            stand-in (apex_spin_us, t_attn_us);
  *   host:    poll until the route is done; apex_expert_prefetch (copies on side);
- *   compute: apex_gate_topk; wait for the copies; apex_moe_ffn pass 1;
+ *   compute: apex_gate_topk; the shared experts, if any (apex_moe_ffn over the layer's
+ *            shared pool, every token, weight 1); wait for the copies; apex_moe_ffn
+ *            pass 1 (added to the shared experts' output);
  *   EXACT:   host waits for the gate, apex_expert_fetch_misses, and if any expert is
  *            missing: compute waits for it and runs apex_moe_ffn pass 2 (accumulate).
  * Layers are processed in order on the compute stream, so a layer's router starts after
  * the previous layer's FFN, as in a model where each layer feeds the next.
+ *
+ * Shared experts (n_shared > 0; DeepSeek-style, Sec. V-A) run for every token with
+ * weight 1 and stay out of the adaptive decision: they live in a resident pool per layer
+ * (shared_slots) and never enter the cache, the prefetch or the miss path.  They run
+ * while the routed experts' copies are still in flight.
  *
  * With attn_heads > 0 the attention window is the layer's real decode attention
  * (apex_attention_decode on h_pre, writing position attn_ctx of its caches) instead of
@@ -325,8 +332,10 @@ apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scr
  *
  * apex_decode_create copies the configuration and the per-layer descriptors (the
  * buffers themselves stay caller-owned and must outlive the driver) and allocates the
- * driver's own events, pinned staging and attention workspace (setup time, not the hot
- * path).
+ * driver's own events, pinned staging, attention workspace and shared-expert lists
+ * (setup time, not the hot path).  `workspace` must hold
+ * apex_moe_ffn_workspace_bytes for both the routed (I, k) and the shared (I_shared,
+ * n_shared) calls.
  */
 typedef struct {
     int L, B, d, E, k, I, C, k_max;
@@ -340,6 +349,8 @@ typedef struct {
     int attn_heads;        /* > 0: the attention window is apex_attention_decode with this */
     int attn_kv_heads;     /*   many query / key-value heads over attn_ctx cached positions */
     int attn_ctx;          /*   (caches hold attn_ctx + 1 positions); 0: spin t_attn_us  */
+    int n_shared;          /* shared experts per layer, 0..APEX_MAX_EXPERTS (0: none)     */
+    int I_shared;          /*   their intermediate size (same rules as I)                 */
 } apex_decode_config;
 
 typedef struct {
@@ -355,6 +366,8 @@ typedef struct {
     const uint16_t *w_qkv, *w_o;           /* attention window only: device bf16 weights, */
     uint16_t *k_cache, *v_cache;           /*   caches [B, G, attn_ctx + 1, hd] and the    */
     float *attn_out;                       /*   block's output [B, d]; NULL otherwise      */
+    const void *shared_slots;              /* n_shared > 0: device, [n_shared] experts of  */
+                                           /*   intermediate I_shared, cfg.weights layout  */
 } apex_decode_layer;
 
 typedef struct {   /* counters the driver adds to at every layer-step */

@@ -7,7 +7,8 @@ paper's two-stage runtime (Sec. IV-A and IV-D "Runtime Operation"):
   -> cache plan (copies of non-resident experts)
   -> original router on h_post -> K_r; executed set by mode (Sec. IV-E)
   -> correctness-preserving misses = K_r minus the resident set
-  -> gated SwiGLU experts on h_post.
+  -> gated SwiGLU experts on h_post, plus the workload's shared experts (Sec. V-A:
+     activated for every token, outside the adaptive decision), each with weight 1.
 
 The experts run on x = h_post and y is the MoE output alone (no residual, no norm);
 layers are not chained, each layer draws its own hidden-state stream.
@@ -38,6 +39,20 @@ class LayerState:
             self._bits[e] = inputs.expert_weights(self.cfg, self.layer, e, self.seed)
         return self._bits[e]
 
+    def shared_bits(self, s):
+        key = ("shared", s)
+        if key not in self._bits:
+            self._bits[key] = inputs.shared_expert_weights(self.cfg, self.layer, s, self.seed)
+        return self._bits[key]
+
+
+def shared_ffn(h_post, n_shared, shared_bits, weights="bf16"):
+    """Sum of the shared experts on every token: each with weight 1 (Sec. V-A)."""
+    h = np.atleast_2d(np.asarray(h_post, np.float64))
+    B = h.shape[0]
+    idx = np.tile(np.arange(n_shared), (B, 1))
+    return ffn.moe_ffn(h, idx, np.ones((B, n_shared)), shared_bits, weights=weights)
+
 
 def layer_step(st: LayerState, t, h_pre, h_post, mode, tau, static_delta=0, run_ffn=True):
     cfg = st.cfg
@@ -57,6 +72,8 @@ def layer_step(st: LayerState, t, h_pre, h_post, mode, tau, static_delta=0, run_
     if run_ffn:
         y = ffn.moe_ffn(h_post, g["exec_idx"], g["exec_gate"], st.expert_bits,
                         weights=st.weights)
+        if cfg.shared:
+            y = y + shared_ffn(h_post, cfg.shared, st.shared_bits, st.weights)
     m = dict(
         overlap=[metrics.overlap(g["route_idx"][b], pf_lists[b], cfg.k) for b in range(B)],
         coverage=[metrics.full_coverage(g["route_idx"][b], pf_lists[b]) for b in range(B)],

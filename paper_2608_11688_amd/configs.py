@@ -32,6 +32,8 @@ class MoEConfig:
     bias_skew: bool = False            # per-expert logit bias ~N(0,1) (Zipf-like load)
     heads: int = 0                     # attention query heads (0: d / 64)
     kv_heads: int = 0                  # attention key/value heads (0: as many as heads)
+    shared: int = 0                    # always-active shared experts per layer
+    I_shared: int = 0                  # their SwiGLU intermediate size (0: I)
 
     @property
     def n_heads(self) -> int:
@@ -44,6 +46,10 @@ class MoEConfig:
     @property
     def head_dim(self) -> int:
         return self.d // self.n_heads
+
+    @property
+    def shared_I(self) -> int:
+        return self.I_shared or self.I
 
     @property
     def expert_bytes(self) -> int:
@@ -69,7 +75,20 @@ OLMOE = MoEConfig("olmoe-1b-7b", 3, L=16, d=2048, E=64, k=8, I=1024, C=24, k_max
 MIXTRAL = MoEConfig("mixtral-8x7b", 4, L=8, d=4096, E=8, k=2, I=14336, C=4, k_max=4,
                     tau=0.9, steps=128, batches=(1, 8, 32), heads=32, kv_heads=8)
 
-CONFIGS = {c.name: c for c in (TINY, GRANITE_1B, GRANITE_3B, OLMOE, MIXTRAL)}
+# The paper's other two evaluated models (Sec. V-A).  d from the per-layer router sizes of
+# its overhead table (d N + 2N parameters per layer); I from the total and active
+# parameter counts in the model names, I = (P_total - P_active) / (L (N - k) 3 d), rounded
+# to a multiple of 64 (Phi: 7B and 2.4B over 32 layers; DeepSeek: 16B and 2.4B over its 26
+# MoE layers, the dense first layer left out).  DeepSeek's two shared experts run for
+# every token outside the adaptive decision.  Cache sizes and k_max follow the other
+# workloads (half of E at small E, C = 24 of 64 as OLMoE).
+PHI_7B = MoEConfig("phi-7b", 5, L=32, d=4096, E=16, k=2, I=832, C=8, k_max=6, tau=0.9,
+                   steps=256, batches=(1, 8), heads=32, kv_heads=8)
+DEEPSEEK_16B = MoEConfig("deepseek-16b", 6, L=26, d=2048, E=64, k=6, I=1472, C=24, k_max=16,
+                         tau=0.9, steps=256, batches=(1, 16), heads=16, kv_heads=16, shared=2)
+
+CONFIGS = {c.name: c for c in (TINY, GRANITE_1B, GRANITE_3B, OLMOE, MIXTRAL, PHI_7B,
+                               DEEPSEEK_16B)}
 BY_ID = {c.cfg_id: c for c in CONFIGS.values()}
 
 

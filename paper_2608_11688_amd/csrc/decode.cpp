@@ -28,6 +28,11 @@ struct apex_decode {
     // attention window (attn_heads > 0)
     void *attn_ws = nullptr;
     size_t attn_ws_bytes = 0;
+    // shared experts (n_shared > 0): every token runs shared expert s at position s with
+    // gate 1 over a pool whose slot s is expert s
+    int32_t *shared_idx = nullptr;     // device [B][n_shared]
+    float *shared_gate = nullptr;      // device [B][n_shared]
+    int32_t *shared_table = nullptr;   // device [n_shared]
     // pinned staging
     int32_t *pf_idx_h = nullptr;      // [B][k_max]
     int32_t *pf_count_h = nullptr;    // [B]
@@ -89,17 +94,25 @@ void fold(apex_decode *dec, const apex_decode::Pending &p, apex_decode_stats *st
     st->misses += p.misses;
 }
 
-// One expert-FFN pass of the executed sets over the given slot pool.
+// One expert-FFN pass in the layer's weight format.
+apex_status run_ffn(apex_decode *dec, const float *x, int I, int E, int k, const int32_t *idx,
+                    const float *gate, const int32_t *slot_of_expert, const void *slots,
+                    int n_slots, float *y, int accumulate) {
+    const apex_decode_config &c = dec->cfg;
+    if (c.weights == APEX_WEIGHTS_FP8_E4M3)
+        return apex_moe_ffn_fp8(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert, slots, n_slots,
+                                y, accumulate, dec->ws, dec->ws_bytes, dec->compute);
+    return apex_moe_ffn(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert,
+                        static_cast<const uint16_t *>(slots), n_slots, y, accumulate, dec->ws,
+                        dec->ws_bytes, dec->compute);
+}
+
+// The routed experts' executed sets over the given slot pool.
 apex_status ffn(apex_decode *dec, const float *x, const int32_t *slot_of_expert,
                 const uint16_t *slots, int n_slots, float *y, int accumulate) {
     const apex_decode_config &c = dec->cfg;
-    if (c.weights == APEX_WEIGHTS_FP8_E4M3)
-        return apex_moe_ffn_fp8(x, c.B, c.d, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate,
-                                slot_of_expert, slots, n_slots, y, accumulate, dec->ws,
-                                dec->ws_bytes, dec->compute);
-    return apex_moe_ffn(x, c.B, c.d, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate,
-                        slot_of_expert, slots, n_slots, y, accumulate, dec->ws, dec->ws_bytes,
-                        dec->compute);
+    return run_ffn(dec, x, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate, slot_of_expert, slots,
+                   n_slots, y, accumulate);
 }
 
 void fold_pending(apex_decode *dec, apex_decode_stats *st) {
@@ -133,9 +146,21 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     APEX_REQUIRE(c.mode != APEX_MODE_EXACT || (scratch && miss_table_dev && c.n_scratch >= 1),
                  "%s: EXACT mode needs a miss scratch pool", fn);
     APEX_REQUIRE(exec_idx_dev && exec_gate_dev && workspace, "%s: NULL buffer", fn);
-    if (workspace_bytes < apex_moe_ffn_workspace_bytes(c.B, c.d, c.I, c.k))
+    const int mult = c.weights == APEX_WEIGHTS_FP8_E4M3 ? 16 : 8;
+    APEX_REQUIRE(c.n_shared >= 0 && c.n_shared <= APEX_MAX_EXPERTS,
+                 "%s: n_shared=%d out of [0, %d]", fn, c.n_shared, APEX_MAX_EXPERTS);
+    APEX_REQUIRE(c.n_shared == 0 || (c.I_shared >= mult && c.I_shared % mult == 0),
+                 "%s: I_shared=%d must be a positive multiple of %d", fn, c.I_shared, mult);
+    if (size_t(c.B) * c.n_shared > APEX_MAX_PAIRS)
+        return apex::fail(APEX_E_UNSUPPORTED, "%s: B*n_shared=%d exceeds %d", fn,
+                          c.B * c.n_shared, APEX_MAX_PAIRS);
+    size_t ws_need = apex_moe_ffn_workspace_bytes(c.B, c.d, c.I, c.k);
+    if (c.n_shared > 0)
+        ws_need = std::max(ws_need, apex_moe_ffn_workspace_bytes(c.B, c.d, c.I_shared,
+                                                                 c.n_shared));
+    if (workspace_bytes < ws_need)
         return apex::fail(APEX_E_CAPACITY, "%s: workspace %zu < %zu bytes", fn, workspace_bytes,
-                          apex_moe_ffn_workspace_bytes(c.B, c.d, c.I, c.k));
+                          ws_need);
     const bool attn = c.attn_heads > 0;
     if (attn) {
         APEX_REQUIRE(c.attn_kv_heads >= 1 && c.attn_ctx >= 0 && c.d % c.attn_heads == 0,
@@ -151,6 +176,8 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
         APEX_REQUIRE(y.w_pf && y.w_g && y.host_experts && y.slots && y.slot_of_expert_dev &&
                          y.expert_of_slot && y.last_used,
                      "%s: layer %d has a NULL buffer", fn, l);
+        APEX_REQUIRE(c.n_shared == 0 || y.shared_slots,
+                     "%s: layer %d has no shared-expert pool", fn, l);
         APEX_REQUIRE(!attn || (y.w_qkv && y.w_o && y.k_cache && y.v_cache && y.attn_out),
                      "%s: layer %d has no attention buffers", fn, l);
     }
@@ -197,6 +224,27 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
         if (mk(&dec->ready[l]) != hipSuccess || mk(&dec->readers_done[l]) != hipSuccess ||
             mk(&dec->gate_done[l]) != hipSuccess)
             return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
+    if (c.n_shared > 0) {
+        const size_t pairs = size_t(c.B) * c.n_shared;
+        std::vector<int32_t> idx(pairs), table(c.n_shared);
+        std::vector<float> gate(pairs, 1.f);
+        for (size_t i = 0; i < pairs; ++i) idx[i] = int32_t(i % c.n_shared);
+        for (int s2 = 0; s2 < c.n_shared; ++s2) table[s2] = s2;
+        e = hipMalloc(reinterpret_cast<void **>(&dec->shared_idx), 4 * pairs);
+        if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&dec->shared_gate), 4 * pairs);
+        if (e == hipSuccess)
+            e = hipMalloc(reinterpret_cast<void **>(&dec->shared_table), 4 * size_t(c.n_shared));
+        if (e == hipSuccess)
+            e = hipMemcpy(dec->shared_idx, idx.data(), 4 * pairs, hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = hipMemcpy(dec->shared_gate, gate.data(), 4 * pairs, hipMemcpyHostToDevice);
+        if (e == hipSuccess)
+            e = hipMemcpy(dec->shared_table, table.data(), 4 * size_t(c.n_shared),
+                          hipMemcpyHostToDevice);
+        if (e != hipSuccess)
+            return cleanup(apex::fail(APEX_E_HIP, "%s: shared-expert lists: %s", fn,
+                                      hipGetErrorString(e)));
+    }
     if (attn) {
         dec->attn_ws_bytes = apex_attention_workspace_bytes(c.B, c.attn_heads, c.attn_kv_heads,
                                                             c.d / c.attn_heads, c.attn_ctx + 1);
@@ -285,8 +333,16 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
                             0, route_h, route_g, dec->exec_idx, dec->exec_gate, nullptr, cs);
         if (st != APEX_OK) return st;
         APEX_HIP(hipEventRecord(dec->gate_done[l], cs));
+        // shared experts first: they need no copy, so they run while the copies land
+        const bool shared = c.n_shared > 0;
+        if (shared) {
+            st = run_ffn(dec, h_post[l], c.I_shared, c.n_shared, c.n_shared, dec->shared_idx,
+                         dec->shared_gate, dec->shared_table, Ly.shared_slots, c.n_shared, y[l],
+                         0);
+            if (st != APEX_OK) return st;
+        }
         APEX_HIP(hipStreamWaitEvent(cs, dec->ready[l], 0));
-        st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], 0);
+        st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], shared ? 1 : 0);
         if (st != APEX_OK) return st;
         int n_miss = 0;
         if (c.mode == APEX_MODE_EXACT) {
@@ -350,6 +406,9 @@ extern "C" apex_status apex_decode_destroy(apex_decode *dec) {
                     static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h)})
         if (p) (void)hipHostFree(p);
     if (dec->attn_ws) (void)hipFree(dec->attn_ws);
+    for (void *p : {static_cast<void *>(dec->shared_idx), static_cast<void *>(dec->shared_gate),
+                    static_cast<void *>(dec->shared_table)})
+        if (p) (void)hipFree(p);
     delete dec;
     return APEX_OK;
 }

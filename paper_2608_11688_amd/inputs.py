@@ -83,15 +83,27 @@ def router_weights(cfg: MoEConfig, layer: int, seed: int = 0):
     return to_bf16_bits(base.astype(np.float32)), to_bf16_bits(w_pf.astype(np.float32)), bias
 
 
-def expert_weights(cfg: MoEConfig, layer: int, expert: int, seed: int = 0):
-    """(W1 bits [I,d], W3 bits [I,d], W2 bits [d,I]) of one SwiGLU expert."""
+def _swiglu_weights(cfg: MoEConfig, layer: int, index: int, I: int, seed: int):
     out = []
-    for tag, shape in ((TAG_W1, (cfg.I, cfg.d)), (TAG_W3, (cfg.I, cfg.d)), (TAG_W2, (cfg.d, cfg.I))):
-        g = rng(seed, cfg.cfg_id, tag, layer, expert)
+    for tag, shape in ((TAG_W1, (I, cfg.d)), (TAG_W3, (I, cfg.d)), (TAG_W2, (cfg.d, I))):
+        g = rng(seed, cfg.cfg_id, tag, layer, index)
         w = g.standard_normal(shape, dtype=np.float32)
         w *= np.float32(W_STD)
         out.append(to_bf16_bits(w))
     return tuple(out)
+
+
+def expert_weights(cfg: MoEConfig, layer: int, expert: int, seed: int = 0):
+    """(W1 bits [I,d], W3 bits [I,d], W2 bits [d,I]) of one routed SwiGLU expert."""
+    return _swiglu_weights(cfg, layer, expert, cfg.I, seed)
+
+
+def shared_expert_weights(cfg: MoEConfig, layer: int, s: int, seed: int = 0):
+    """The same for shared expert s < cfg.shared (its own streams: index E + s), with
+    intermediate size cfg.shared_I."""
+    if not 0 <= s < cfg.shared:
+        raise IndexError(f"{cfg.name} has {cfg.shared} shared experts")
+    return _swiglu_weights(cfg, layer, cfg.E + s, cfg.shared_I, seed)
 
 
 def attention_weights(cfg: MoEConfig, layer: int, seed: int = 0):

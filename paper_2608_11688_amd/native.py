@@ -24,7 +24,7 @@ APEX_OK, APEX_E_INVAL, APEX_E_UNSUPPORTED, APEX_E_HIP, APEX_E_CAPACITY = 0, -1, 
 SEL_CUMPROB, SEL_ORDINAL_CDF, SEL_STATIC, SEL_NONE = 0, 1, 2, 3
 MODE_EXACT, MODE_STALL_FREE = 0, 1
 WEIGHTS_BF16, WEIGHTS_FP8_E4M3 = 0, 1
-ABI_VERSION = 2
+ABI_VERSION = 3
 MAX_EXPERTS = 64
 MAX_PAIRS = 1024
 
@@ -47,14 +47,15 @@ class DecodeConfig(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("L", "B", "d", "E", "k", "I", "C", "k_max", "policy")] + [
         ("tau", C.c_float), ("static_delta", C.c_int), ("mode", C.c_int),
         ("t_attn_us", C.c_double), ("n_scratch", C.c_int), ("weights", C.c_int),
-        ("attn_heads", C.c_int), ("attn_kv_heads", C.c_int), ("attn_ctx", C.c_int)]
+        ("attn_heads", C.c_int), ("attn_kv_heads", C.c_int), ("attn_ctx", C.c_int),
+        ("n_shared", C.c_int), ("I_shared", C.c_int)]
 
 
 class DecodeLayer(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in (
         "w_pf", "w_g", "b_pf", "b_g", "cdf_w", "cdf_theta", "host_experts", "slots",
         "slot_of_expert_dev", "avail_dev", "expert_of_slot", "last_used", "w_qkv", "w_o",
-        "k_cache", "v_cache", "attn_out")]
+        "k_cache", "v_cache", "attn_out", "shared_slots")]
 
 
 class DecodeStats(C.Structure):

@@ -65,8 +65,7 @@ class DecodeRunner:
         if window not in ("spin", "attention"):
             raise ValueError(f"window must be 'spin' or 'attention', not {window!r}")
         self.window, self.ctx = window, ctx
-        self.S = (native.apex_expert_bytes_fp8(cfg.d, cfg.I) if weights == "fp8"
-                  else native.apex_expert_bytes(cfg.d, cfg.I))
+        self.S = self.expert_bytes(cfg.I)
         E, B, k = cfg.E, batch, cfg.k
         self.n_scratch = min(E, B * k) if n_scratch is None else n_scratch
         L = len(self.layers)
@@ -80,6 +79,9 @@ class DecodeRunner:
         self.exec_gate = torch.empty((B, k), dtype=torch.float32, device=self.dev)
         self.y = torch.zeros((L, B, cfg.d), dtype=torch.float32, device=self.dev)
         self.ws_bytes = native.apex_moe_ffn_workspace_bytes(B, cfg.d, cfg.I, k)
+        if cfg.shared:
+            self.ws_bytes = max(self.ws_bytes, native.apex_moe_ffn_workspace_bytes(
+                B, cfg.d, cfg.shared_I, cfg.shared))
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
         self.scratch = torch.empty(max(1, self.n_scratch) * self.S // 2, dtype=torch.int16,
                                    device=self.dev)
@@ -93,7 +95,8 @@ class DecodeRunner:
                                    weights=(native.WEIGHTS_FP8_E4M3 if weights == "fp8"
                                             else native.WEIGHTS_BF16),
                                    attn_heads=cfg.n_heads if window == "attention" else 0,
-                                   attn_kv_heads=cfg.n_kv_heads, attn_ctx=ctx)
+                                   attn_kv_heads=cfg.n_kv_heads, attn_ctx=ctx,
+                                   n_shared=cfg.shared, I_shared=cfg.shared_I)
         descs = []
         for l in self.layers:
             b = self.bufs[l]
@@ -105,7 +108,8 @@ class DecodeRunner:
                 slot_of_expert_dev=p(b["slot_dev"]), avail_dev=p(b["avail_dev"]),
                 expert_of_slot=b["eos"].ctypes.data, last_used=b["last_used"].ctypes.data,
                 w_qkv=p(b.get("w_qkv")), w_o=p(b.get("w_o")), k_cache=p(b.get("k_cache")),
-                v_cache=p(b.get("v_cache")), attn_out=p(b.get("attn_out"))))
+                v_cache=p(b.get("v_cache")), attn_out=p(b.get("attn_out")),
+                shared_slots=p(b.get("shared_slots"))))
         self.dec, self._descs = native.apex_decode_create(
             dcfg, descs, self.scratch, self.miss_table, self.exec_idx, self.exec_gate, self.ws,
             self.ws_bytes, self.cs, self.ss)
@@ -129,6 +133,18 @@ class DecodeRunner:
         self.t = 0
 
     # ------------------------------------------------------------------ setup
+    def expert_bytes(self, I):
+        """Bytes of one packed expert of intermediate size I in this runner's format."""
+        if self.weights == "fp8":
+            return native.apex_expert_bytes_fp8(self.cfg.d, I)
+        return native.apex_expert_bytes(self.cfg.d, I)
+
+    def pack(self, w1, w3, w2, d, I, out):
+        if self.weights == "fp8":
+            native.apex_pack_expert_fp8(w1, w3, w2, d, I, out)
+        else:
+            native.apex_pack_expert(w1, w3, w2, d, I, out)
+
     def _make_layer(self, l, pool, cdf):
         torch, cfg = self.torch, self.cfg
         wg, wpf, bias = inputs.router_weights(cfg, l, self.seed)
@@ -139,9 +155,7 @@ class DecodeRunner:
 
         def fill(e):
             w1, w3, w2 = inputs.expert_weights(cfg, l, e, self.seed)
-            pack = (native.apex_pack_expert_fp8 if self.weights == "fp8"
-                    else native.apex_pack_expert)
-            pack(w1, w3, w2, cfg.d, cfg.I, hp + e * self.S)
+            self.pack(w1, w3, w2, cfg.d, cfg.I, hp + e * self.S)
 
         list(pool.map(fill, range(cfg.E)))
         slots = torch.empty(cfg.C * S2, dtype=torch.int16, device=self.dev)
@@ -158,6 +172,14 @@ class DecodeRunner:
                    slot_dev=to_dev(table), avail_dev=to_dev((table >= 0).astype(np.uint8)),
                    eos=eos, last_used=np.full(cfg.E, -1, np.int64), h_pre=to_dev(h_pre),
                    h_post=to_dev(h_post), cdf_w=None, cdf_theta=None)
+        if cfg.shared:
+            # the shared experts: resident for the driver's life, never prefetched
+            S_sh = self.expert_bytes(cfg.shared_I)
+            sh = np.empty(cfg.shared * S_sh, np.uint8)
+            for s_ in range(cfg.shared):
+                w1, w3, w2 = inputs.shared_expert_weights(cfg, l, s_, self.seed)
+                self.pack(w1, w3, w2, cfg.d, cfg.shared_I, sh[s_ * S_sh:].ctypes.data)
+            out["shared_slots"] = to_dev(sh)
         if self.window == "attention":
             w_qkv, w_o = inputs.attention_weights(cfg, l, self.seed)
             out["w_qkv"] = to_dev(w_qkv.view(np.int16))

@@ -8,6 +8,7 @@ against the oracle's own separately.
 import numpy as np
 import pytest
 
+from oracle import decode as odecode
 from oracle import ffn as offn
 from oracle import gating, routing
 from oracle.residency import Residency
@@ -68,6 +69,9 @@ def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau
                     bits = lambda e, l=l: inputs.expert_weights(cfg, l, e)
                     y_ref = offn.moe_ffn(h_post, log.exec_idx, log.exec_gate.astype(np.float64),
                                          bits, weights=weights)
+                    if cfg.shared:
+                        sbits = lambda s, l=l: inputs.shared_expert_weights(cfg, l, s)
+                        y_ref = y_ref + odecode.shared_ffn(h_post, cfg.shared, sbits, weights)
                     _, l1 = ffn_close(log.y, y_ref, f"y t{t} l{l}")
                     stats["worst_l1"] = max(stats["worst_l1"], l1)
                     stats["ffn_checked"] += 1
@@ -187,3 +191,24 @@ def test_decode_with_attention_window():
         print("attention window worst rel err", worst)
     finally:
         runner.close()
+
+
+@pytest.mark.parametrize("batch,mode", [(1, native.MODE_EXACT), (16, native.MODE_STALL_FREE)])
+def test_decode_deepseek_shape_with_shared_experts(batch, mode):
+    # 64 routed experts (k = 6) plus two shared experts that every token runs with weight 1,
+    # before the routed experts' copies land; batch 16 takes the grouped path for both
+    cfg = configs.DEEPSEEK_16B
+    st = check_decode(cfg, batch, mode, 3, [0, 25])
+    assert st["ffn_checked"] > 0
+
+
+@pytest.mark.parametrize("batch,mode", [(1, native.MODE_EXACT), (8, native.MODE_STALL_FREE)])
+def test_decode_phi_shape(batch, mode):
+    cfg = configs.PHI_7B
+    st = check_decode(cfg, batch, mode, 3, [0, 31])
+    assert st["ffn_checked"] > 0
+
+
+def test_decode_deepseek_shape_fp8_shared_experts():
+    # the shared pool is packed in the layer's weight format as well
+    check_decode(configs.DEEPSEEK_16B, 1, native.MODE_EXACT, 2, [7], weights="fp8")

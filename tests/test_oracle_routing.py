@@ -198,6 +198,18 @@ def test_overhead_table_parameter_counts():
         assert round(per_hidden_w / 1e6, 2) != row["printed_millions"]
 
 
+def test_phi_and_deepseek_shapes_follow_the_overhead_table():
+    # the Phi-7B and DeepSeek-16B workloads take d, N, k and the MoE layer count of the
+    # overhead table's rows, and I from the total and active counts in the model names
+    g = {r["model"]: r for r in json.load(open(os.path.join(GOLDEN, "overhead_params.json")))["rows"]}
+    for cfg, row, total, active in ((configs.PHI_7B, g["Phi-7B"], 7.0e9, 2.4e9),
+                                    (configs.DEEPSEEK_16B, g["DeepSeek-16B"], 16.0e9, 2.4e9)):
+        assert (cfg.d, cfg.E, cfg.k, cfg.L) == (row["d"], row["N"], row["k"], row["layers"])
+        I = (total - active) / (cfg.L * (cfg.E - cfg.k) * 3 * cfg.d)
+        assert cfg.I == 64 * round(I / 64)
+    assert configs.DEEPSEEK_16B.shared == 2 and configs.PHI_7B.shared == 0
+
+
 def test_no_prefetch_policy_selects_nothing():
     cfg = configs.GRANITE_1B
     h = inputs.hidden_states(cfg, 0, 4, 1)[0][0]
