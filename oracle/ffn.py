@@ -10,13 +10,15 @@ silu(u) = u / (1 + exp(-u)), as the workload definitions state.
 
 With weights="fp8" every expert matrix is first quantised row by row to E4M3 with an
 fp32 scale per row (``fp8``, the reading taken for the precision study of Sec. V-H) and
-the FFN runs on the dequantised values s_r * q, in float64.
+the FFN runs on the dequantised values s_r * q, in float64.  With weights="mxfp4" every
+row is quantised in blocks of 32 along the reduction dimension to E2M1 codes with a
+power-of-two scale per block (``mxfp4``) and the FFN runs on 2^X * q.
 """
 from __future__ import annotations
 
 import numpy as np
 
-from . import fp8
+from . import fp8, mxfp4
 from .bf16 import bf16_to_f64
 
 
@@ -38,9 +40,10 @@ def moe_ffn(x, exec_idx, exec_gate, expert_bits, skip=None, weights="bf16"):
     x: [B, d]; exec_idx int [B, k] (-1 = unused position); exec_gate [B, k];
     expert_bits(e) -> (W1 bits [I,d], W3 bits [I,d], W2 bits [d,I]);
     skip: optional set of expert ids left out (a pass that only covers some experts);
-    weights: "bf16" (the weights as given) or "fp8" (quantised per row first).
+    weights: "bf16" (the weights as given), "fp8" (quantised per row first) or "mxfp4"
+    (quantised per block of 32 along each row first).
     """
-    if weights not in ("bf16", "fp8"):
+    if weights not in ("bf16", "fp8", "mxfp4"):
         raise ValueError(f"unknown weight format {weights}")
     x = np.atleast_2d(np.asarray(x, dtype=np.float64))
     B, d = x.shape
@@ -55,6 +58,8 @@ def moe_ffn(x, exec_idx, exec_gate, expert_bits, skip=None, weights="bf16"):
                 ws = tuple(bf16_to_f64(w) for w in expert_bits(e))
                 if weights == "fp8":
                     ws = tuple(fp8.dequantize_rows(*fp8.quantize_rows(w)) for w in ws)
+                elif weights == "mxfp4":
+                    ws = tuple(mxfp4.dequantize_blocks(*mxfp4.quantize_blocks(w)) for w in ws)
                 cache[e] = ws
             w1, w3, w2 = cache[e]
             y[b] += float(exec_gate[b, j]) * swiglu_expert(x[b], w1, w3, w2)
