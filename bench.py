@@ -16,7 +16,7 @@ is timed after it; the difference is the exposed stall.
 
     python bench.py [--steps K] [--warmup W] [--config granite-1b-a400m] [--batch 1]
                     [--mode exact|stall_free] [--policy cumprob|ordinal|static|none]
-                    [--static-delta D] [--tau T] [--weights bf16|fp8]
+                    [--static-delta D] [--tau T] [--weights bf16|fp8|mxfp4]
                     [--window spin|attention] [--t-attn-us 10] [--ctx 1024]
                     [--no-compute-only] [--no-cpu-baseline]
 
@@ -53,8 +53,9 @@ def parse():
     p.add_argument("--policy", default="cumprob",
                    choices=["cumprob", "ordinal", "static", "none"])
     p.add_argument("--static-delta", type=int, default=0)
-    p.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
-                   help="expert weight format (fp8: E4M3 with fp32 row scales)")
+    p.add_argument("--weights", default="bf16", choices=["bf16", "fp8", "mxfp4"],
+                   help="expert weight format (fp8: E4M3 with fp32 row scales; mxfp4: E2M1 "
+                        "with a power-of-two scale per block of 32)")
     p.add_argument("--cdf-tokens", type=int, default=1024,
                    help="held-out tokens per layer for the ordinal-model fit")
     p.add_argument("--t-attn-us", type=float, default=10.0,
@@ -111,7 +112,7 @@ def ffn_roofline_leg(torch, native, runner, reps=8, seed=123):
     y = torch.empty((B, cfg.d), dtype=torch.float32, device="cuda")
     e0, e1 = native.apex_event_create(True), native.apex_event_create(True)
     torch.cuda.synchronize()
-    ffn = native.apex_moe_ffn_fp8 if runner.weights == "fp8" else native.apex_moe_ffn
+    ffn = runner.moe_ffn
     native.apex_spin_us(min(5000.0 + 50.0 * n, 1e6), cs)
     native.apex_event_record(e0, cs)
     for i in range(n):
@@ -329,8 +330,9 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": ("fp8 e4m3 weights with fp32 row scales, fp32 accumulate"
-                  if args.weights == "fp8" else "bf16 weights, fp32 accumulate"),
+        "dtype": {"fp8": "fp8 e4m3 weights with fp32 row scales, fp32 accumulate",
+                  "mxfp4": "mxfp4 (e2m1, e8m0 block scales) weights, fp32 accumulate",
+                  "bf16": "bf16 weights, fp32 accumulate"}[args.weights],
         "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) bf16 experts)",
         "config": {"workload": cfg.name, "layers": L, "d": cfg.d, "E": cfg.E, "k": cfg.k,
                    "I": cfg.I, "C": cfg.C, "k_max": cfg.k_max, "tau": tau, "batch": B,

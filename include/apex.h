@@ -68,7 +68,8 @@ typedef enum {
 /* Expert weight format: apex_pack_expert (bf16) or apex_pack_expert_fp8 (E4M3). */
 typedef enum {
     APEX_WEIGHTS_BF16 = 0,
-    APEX_WEIGHTS_FP8_E4M3 = 1
+    APEX_WEIGHTS_FP8_E4M3 = 1,
+    APEX_WEIGHTS_MXFP4 = 2
 } apex_weights;
 
 /* Execution mode of apex_gate_topk (Sec. IV-E). */
@@ -167,6 +168,27 @@ apex_status apex_pack_expert_fp8(const uint16_t *w1, const uint16_t *w3, const u
                                  int d, int I, void *out);
 
 /*
+ * Experts with 4-bit weights (the precision study of Sec. V-H), in the OCP MXFP4 form:
+ * FP4 E2M1 codes (1 sign, 2 exponent bits with bias 1, 1 mantissa bit: magnitudes 0,
+ * 0.5, 1, 1.5, 2, 3, 4, 6), two per byte with element 2j in the low nibble of byte j,
+ * and one power-of-two scale 2^X per block of 32 consecutive values of a row (along the
+ * reduction dimension: d for W1 and W3, I for W2), stored as the byte X + 127.  For each
+ * block X = floor(log2 of its largest magnitude) - 2 and the codes round v / 2^X to the
+ * nearest E2M1 value (ties to the even code, magnitudes above 6 clamped to 6, sign bit
+ * for negative values); a block of zeros has X = -127 and codes 0.  The weights are
+ * 2^X * q exactly.
+ * apex_expert_bytes_mxfp4(d, I) = 3 d I / 2 + 3 d I / 32 bytes:
+ *   rows i = 0..I-1 of [W1[i, 0:d] codes | W3[i, 0:d] codes] (d/2 bytes each), then W2
+ *   codes [d, I/2 bytes] row-major, then the scale bytes of W1 [I, d/32], W3 [I, d/32]
+ *   and W2 [d, I/32].
+ * apex_pack_expert_mxfp4 quantises bf16 experts (w1, w3 [I, d], w2 [d, I]) into that
+ * layout (host memory to host memory); d and I must be multiples of 32.
+ */
+size_t apex_expert_bytes_mxfp4(int d, int I);
+apex_status apex_pack_expert_mxfp4(const uint16_t *w1, const uint16_t *w3, const uint16_t *w2,
+                                   int d, int I, void *out);
+
+/*
  * Gated SwiGLU experts (Sec. III-A weighted sum; Sec. IV-E aggregation with the
  * original router weights).  For every token b and position j with e = exec_idx[b, j]
  * in [0, E) and s = slot_of_expert[e] in [0, n_slots):
@@ -207,6 +229,19 @@ apex_status apex_moe_ffn_fp8(const float *x, int B, int d, int I, int E, int k,
                              const int32_t *slot_of_expert, const void *slots, int n_slots,
                              float *y, int accumulate, void *workspace,
                              size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * apex_moe_ffn over experts packed by apex_pack_expert_mxfp4: slot s starts at byte
+ * s * apex_expert_bytes_mxfp4(d, I) of `slots` (16-byte aligned); d and I multiples of
+ * 32.  The same sum with every weight taken as 2^X * q exactly (the block scales are
+ * applied as the codes are converted).  Same arguments, workspace size
+ * (apex_moe_ffn_workspace_bytes) and error behaviour.
+ */
+apex_status apex_moe_ffn_mxfp4(const float *x, int B, int d, int I, int E, int k,
+                               const int32_t *exec_idx, const float *exec_gate,
+                               const int32_t *slot_of_expert, const void *slots, int n_slots,
+                               float *y, int accumulate, void *workspace,
+                               size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Decode attention of one layer: the block that runs between the prefetch router and

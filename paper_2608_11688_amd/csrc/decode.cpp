@@ -102,6 +102,9 @@ apex_status run_ffn(apex_decode *dec, const float *x, int I, int E, int k, const
     if (c.weights == APEX_WEIGHTS_FP8_E4M3)
         return apex_moe_ffn_fp8(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert, slots, n_slots,
                                 y, accumulate, dec->ws, dec->ws_bytes, dec->compute);
+    if (c.weights == APEX_WEIGHTS_MXFP4)
+        return apex_moe_ffn_mxfp4(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert, slots,
+                                  n_slots, y, accumulate, dec->ws, dec->ws_bytes, dec->compute);
     return apex_moe_ffn(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert,
                         static_cast<const uint16_t *>(slots), n_slots, y, accumulate, dec->ws,
                         dec->ws_bytes, dec->compute);
@@ -137,16 +140,19 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
                  "%s: need 1 <= k <= k_max <= C <= E (k=%d k_max=%d C=%d E=%d)", fn, c.k,
                  c.k_max, c.C, c.E);
     APEX_REQUIRE(c.t_attn_us >= 0.0 && c.t_attn_us <= 1e6, "%s: t_attn_us=%g", fn, c.t_attn_us);
-    APEX_REQUIRE(c.weights == APEX_WEIGHTS_BF16 || c.weights == APEX_WEIGHTS_FP8_E4M3,
+    APEX_REQUIRE(c.weights == APEX_WEIGHTS_BF16 || c.weights == APEX_WEIGHTS_FP8_E4M3 ||
+                     c.weights == APEX_WEIGHTS_MXFP4,
                  "%s: unknown weight format %d", fn, c.weights);
-    APEX_REQUIRE(c.weights != APEX_WEIGHTS_FP8_E4M3 || (c.d % 16 == 0 && c.I % 16 == 0),
-                 "%s: E4M3 experts need d and I multiples of 16 (d=%d I=%d)", fn, c.d, c.I);
+    // one 16-byte load holds 8 bf16 or 16 E4M3 weights; MXFP4 rows are whole 32-value blocks
+    const int mult = c.weights == APEX_WEIGHTS_BF16 ? 8 : c.weights == APEX_WEIGHTS_FP8_E4M3 ? 16 : 32;
+    APEX_REQUIRE(c.d % mult == 0 && c.I % mult == 0,
+                 "%s: weight format %d needs d and I multiples of %d (d=%d I=%d)", fn, c.weights,
+                 mult, c.d, c.I);
     APEX_REQUIRE(c.mode == APEX_MODE_EXACT || c.mode == APEX_MODE_STALL_FREE, "%s: mode %d", fn,
                  c.mode);
     APEX_REQUIRE(c.mode != APEX_MODE_EXACT || (scratch && miss_table_dev && c.n_scratch >= 1),
                  "%s: EXACT mode needs a miss scratch pool", fn);
     APEX_REQUIRE(exec_idx_dev && exec_gate_dev && workspace, "%s: NULL buffer", fn);
-    const int mult = c.weights == APEX_WEIGHTS_FP8_E4M3 ? 16 : 8;
     APEX_REQUIRE(c.n_shared >= 0 && c.n_shared <= APEX_MAX_EXPERTS,
                  "%s: n_shared=%d out of [0, %d]", fn, c.n_shared, APEX_MAX_EXPERTS);
     APEX_REQUIRE(c.n_shared == 0 || (c.I_shared >= mult && c.I_shared % mult == 0),
@@ -193,6 +199,7 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     dec->compute = compute;
     dec->side = side;
     dec->expert_bytes = c.weights == APEX_WEIGHTS_FP8_E4M3 ? apex_expert_bytes_fp8(c.d, c.I)
+                        : c.weights == APEX_WEIGHTS_MXFP4  ? apex_expert_bytes_mxfp4(c.d, c.I)
                                                            : apex_expert_bytes(c.d, c.I);
     auto cleanup = [&](apex_status st) {
         apex_decode_destroy(dec);

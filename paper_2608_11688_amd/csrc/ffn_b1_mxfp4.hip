@@ -1,0 +1,209 @@
+// Expert FFN for one token over apex_pack_expert_mxfp4 slots (apex_moe_ffn_mxfp4, batch
+// 1): the two launches of ffn_b1.hip with 4-bit E2M1 weights and a power-of-two scale
+// per block of 32 values.  A lane's unit is 16 codes (8 bytes, half a block) and the
+// scale byte of its block; codes are widened and scaled exactly by the hardware
+// conversion, and the products accumulate in fp32.
+#include <hip/hip_runtime.h>
+
+#include "ffn_device.h"
+#include "ffn_internal.h"
+
+namespace {
+
+using apex::ffn::dot16_mxfp4;
+using apex::ffn::kWave;
+using apex::ffn::mx_scale;
+using apex::ffn::silu;
+using apex::ffn::wave_sum;
+
+// up_b1_mxfp4: grid (I / (WAVES * RW), k).  A wavefront owns RW rows of the expert at
+// position blockIdx.y; NPL counts 16-code units per lane (1024 values of a row per pass
+// of a wavefront).  All loads of a pass are issued before the first multiply.
+template <int NPL, int RW, int WAVES>
+__global__ __launch_bounds__(WAVES *kWave) void up_b1_mxfp4(
+    const float *__restrict__ x, int d, int I, int E, int k,
+    const int32_t *__restrict__ exec_idx, const float *__restrict__ exec_gate,
+    const int32_t *__restrict__ slot_of_expert, const uint8_t *__restrict__ slots, int n_slots,
+    size_t slot_bytes, float *__restrict__ h) {
+    const int j = blockIdx.y;
+    const int e = exec_idx[j];
+    const float g = exec_gate[j];
+    if (e < 0 || e >= E) return;
+    const int s = slot_of_expert[e];
+    if (s < 0 || s >= n_slots) return;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int i0 = (blockIdx.x * WAVES + wave) * RW;
+    if (i0 >= I) return;
+    const int nch = d / 16;                       // units per row of W1 (and of W3)
+    const int nsb = d / 32;                       // scale bytes per row
+    const uint8_t *slot = slots + size_t(s) * slot_bytes;
+    const uint2 *W = reinterpret_cast<const uint2 *>(slot);     // rows of 2 * nch units
+    const uint8_t *sc1 = slot + size_t(3) * I * d / 2;          // W1 scales [I][d/32]
+    const uint8_t *sc3 = sc1 + size_t(I) * nsb;                 // W3 scales
+    const float4 *x4 = reinterpret_cast<const float4 *>(x);
+
+    float u[RW], v[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) u[r] = v[r] = 0.f;
+    for (int cb = 0; cb < nch; cb += NPL * kWave) {
+        uint2 w1[RW][NPL], w3[RW][NPL];
+        uint32_t b1[RW][NPL], b3[RW][NPL];
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const int i = (i0 + r < I) ? i0 + r : I - 1;
+            const uint2 *row = W + size_t(i) * 2 * nch;
+#pragma unroll
+            for (int n = 0; n < NPL; ++n) {
+                const int c = cb + lane + n * kWave;
+                if (c < nch) {
+                    w1[r][n] = row[c];
+                    w3[r][n] = row[nch + c];
+                    b1[r][n] = sc1[size_t(i) * nsb + c / 2];
+                    b3[r][n] = sc3[size_t(i) * nsb + c / 2];
+                }
+            }
+        }
+        float4 xs[NPL][4];
+#pragma unroll
+        for (int n = 0; n < NPL; ++n) {
+            const int c = cb + lane + n * kWave;
+            if (c < nch)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) xs[n][q] = x4[4 * c + q];
+        }
+#pragma unroll
+        for (int r = 0; r < RW; ++r)
+#pragma unroll
+            for (int n = 0; n < NPL; ++n) {
+                const int c = cb + lane + n * kWave;
+                if (c < nch) {
+                    u[r] = dot16_mxfp4(w1[r][n], mx_scale(b1[r][n]), xs[n], u[r]);
+                    v[r] = dot16_mxfp4(w3[r][n], mx_scale(b3[r][n]), xs[n], v[r]);
+                }
+            }
+    }
+    float hv = 0.f;
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+        const float su = wave_sum(u[r]);
+        const float sv = wave_sum(v[r]);
+        if (lane == r) hv = silu(su) * sv * g;
+    }
+    if (lane < RW && i0 + lane < I) h[size_t(j) * I + i0 + lane] = hv;
+}
+
+// down_b1_mxfp4: grid d / (WAVES * RD).  A wavefront owns RD output rows; lanes step
+// through (valid position, unit) pairs UNR at a time, as down_b1 does.
+template <int RD, int WAVES, int UNR>
+__global__ __launch_bounds__(WAVES *kWave) void down_b1_mxfp4(
+    int d, int I, int E, int k, const int32_t *__restrict__ exec_idx,
+    const int32_t *__restrict__ slot_of_expert, const uint8_t *__restrict__ slots, int n_slots,
+    size_t slot_bytes, const float *__restrict__ h, float *__restrict__ y, int accumulate) {
+    // offsets into the slot pool (8-byte units of W2 codes, bytes of its scales)
+    __shared__ int meta_pos[APEX_MAX_EXPERTS];
+    __shared__ size_t meta_w2[APEX_MAX_EXPERTS];
+    __shared__ size_t meta_s2[APEX_MAX_EXPERTS];
+    __shared__ int n_valid;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int nch = I / 16, nsb = I / 32;
+    const uint2 *pool = reinterpret_cast<const uint2 *>(slots);
+    if (wave == 0) {
+        const int e = lane < k ? exec_idx[lane] : -1;
+        const int s = (e >= 0 && e < E) ? slot_of_expert[e] : -1;
+        const bool ok = s >= 0 && s < n_slots;
+        const unsigned long long m = __ballot(ok);
+        if (ok) {
+            const int idx = __popcll(m & ((1ull << lane) - 1ull));
+            const size_t base = size_t(s) * slot_bytes;
+            meta_pos[idx] = lane;
+            meta_w2[idx] = (base + size_t(I) * d) / 8;
+            meta_s2[idx] = base + size_t(3) * I * d / 2 + size_t(2) * I * (d / 32);
+        }
+        if (lane == 0) n_valid = __popcll(m);
+    }
+    __syncthreads();
+    const int j0 = (blockIdx.x * WAVES + wave) * RD;
+    if (j0 >= d) return;
+    const int total = n_valid * nch;
+    float acc[RD];
+#pragma unroll
+    for (int r = 0; r < RD; ++r) acc[r] = 0.f;
+    int item = 0, c = lane;
+    while (c >= nch && item < n_valid) { c -= nch; ++item; }
+    for (int t0 = lane; t0 < total; t0 += UNR * kWave) {
+        uint2 w[UNR][RD];
+        uint32_t sb[UNR][RD];
+        float4 hx[UNR][4];
+        bool on[UNR];
+        int it = item, cc = c;
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            on[u] = t0 + u * kWave < total;
+            if (on[u]) {
+                const uint2 *w2 = pool + meta_w2[it];
+                const uint8_t *s2 = slots + meta_s2[it];
+                const float4 *hr = reinterpret_cast<const float4 *>(h + size_t(meta_pos[it]) * I);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) hx[u][q] = hr[4 * cc + q];
+#pragma unroll
+                for (int r = 0; r < RD; ++r) {
+                    const int jr = (j0 + r < d) ? j0 + r : d - 1;
+                    w[u][r] = w2[size_t(jr) * nch + cc];
+                    sb[u][r] = s2[size_t(jr) * nsb + cc / 2];
+                }
+            }
+            cc += kWave;
+            while (cc >= nch) { cc -= nch; ++it; }
+        }
+        item = it;
+        c = cc;
+#pragma unroll
+        for (int u = 0; u < UNR; ++u)
+            if (on[u])
+#pragma unroll
+                for (int r = 0; r < RD; ++r)
+                    acc[r] = dot16_mxfp4(w[u][r], mx_scale(sb[u][r]), hx[u], acc[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < RD; ++r) {
+        const float s = wave_sum(acc[r]);
+        if (lane == r && j0 + r < d) y[j0 + r] = (accumulate ? y[j0 + r] : 0.f) + s;
+    }
+}
+
+}  // namespace
+
+namespace apex {
+
+apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32_t *exec_idx,
+                         const float *exec_gate, const int32_t *slot_of_expert,
+                         const uint8_t *slots, int n_slots, float *h, float *y, int accumulate,
+                         hipStream_t stream) {
+    const size_t slot_bytes = apex_expert_bytes_mxfp4(d, I);
+    const int npl = (d + 1023) / 1024;   // 16-code units per lane for a whole row
+    if (d <= 2048) {
+        const dim3 gu(I / 4 + (I % 4 != 0), k);
+        if (npl <= 1)
+            hipLaunchKernelGGL((up_b1_mxfp4<1, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
+                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_bytes, h);
+        else
+            hipLaunchKernelGGL((up_b1_mxfp4<2, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
+                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_bytes, h);
+        APEX_HIP(hipGetLastError());
+        hipLaunchKernelGGL((down_b1_mxfp4<1, 1, 8>), dim3(d), dim3(64), 0, stream, d, I, E, k,
+                           exec_idx, slot_of_expert, slots, n_slots, slot_bytes, h, y,
+                           accumulate);
+    } else {
+        const dim3 gu(I / 8 + (I % 8 != 0), k);
+        hipLaunchKernelGGL((up_b1_mxfp4<4, 2, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
+                           exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_bytes, h);
+        APEX_HIP(hipGetLastError());
+        hipLaunchKernelGGL((down_b1_mxfp4<4, 4, 4>), dim3(d / 16 + (d % 16 != 0)), dim3(256), 0,
+                           stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
+                           slot_bytes, h, y, accumulate);
+    }
+    APEX_HIP(hipGetLastError());
+    return APEX_OK;
+}
+
+}  // namespace apex

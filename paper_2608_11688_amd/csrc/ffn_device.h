@@ -1,5 +1,5 @@
 // Device helpers shared by the expert-FFN kernels: bf16 unpacking, 8-wide (bf16) and
-// 16-wide (E4M3) dot products against fp32 activations, a wavefront sum and SiLU.
+// 16-wide (E4M3, MXFP4) dot products against fp32 activations, a wavefront sum and SiLU.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -46,6 +46,35 @@ __device__ __forceinline__ float dot16_e4m3(uint4 w, const float4 (&x)[4], float
         acc = fmaf(lo[1], x[q].y, acc);
         acc = fmaf(hi[0], x[q].z, acc);
         acc = fmaf(hi[1], x[q].w, acc);
+    }
+    return acc;
+}
+
+// The fp32 value 2^(b - 127) of an MX scale byte b (b = 0 is the subnormal 2^-127).
+__device__ __forceinline__ float mx_scale(uint32_t b) {
+    return __uint_as_float(b ? b << 23 : 0x00400000u);
+}
+
+// 16 FP4 E2M1 codes (two per byte of w, the low nibble first) times x[0..3] (16 fp32
+// values), each code widened and multiplied by its block scale exactly in hardware.
+__device__ __forceinline__ float dot16_mxfp4(uint2 w, float scale, const float4 (&x)[4],
+                                             float acc) {
+    const uint32_t word[2] = {w.x, w.y};
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+        const auto p0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word[q], scale, 0);
+        const auto p1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word[q], scale, 1);
+        const auto p2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word[q], scale, 2);
+        const auto p3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(word[q], scale, 3);
+        const float4 a = x[2 * q], b = x[2 * q + 1];
+        acc = fmaf(p0[0], a.x, acc);
+        acc = fmaf(p0[1], a.y, acc);
+        acc = fmaf(p1[0], a.z, acc);
+        acc = fmaf(p1[1], a.w, acc);
+        acc = fmaf(p2[0], b.x, acc);
+        acc = fmaf(p2[1], b.y, acc);
+        acc = fmaf(p3[0], b.z, acc);
+        acc = fmaf(p3[1], b.w, acc);
     }
     return acc;
 }

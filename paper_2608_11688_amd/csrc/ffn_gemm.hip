@@ -13,14 +13,16 @@
 //     it stages its activations;
 //   * down_gemm writes per-split, per-pair outputs; combine_pairs adds the splits and the
 //     gated positions of each token in a fixed order.
-// Slots hold bf16 weights (apex_pack_expert) or E4M3 codes with fp32 row scales
-// (apex_pack_expert_fp8); E4M3 tiles are widened to bf16 exactly as they go to LDS and
-// the row scales multiply the outputs.  Every executed expert's weights are read once
+// Slots hold bf16 weights (apex_pack_expert), E4M3 codes with fp32 row scales
+// (apex_pack_expert_fp8) or MXFP4 codes with a power-of-two scale per block of 32
+// (apex_pack_expert_mxfp4).  E4M3 and MXFP4 tiles are widened to bf16 exactly as they go
+// to LDS (MXFP4 with its block scales applied); the E4M3 row scales multiply the outputs.  Every executed expert's weights are read once
 // per call whatever the number of tokens routed to it, and no atomics are used, so
 // results are deterministic.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "ffn_device.h"
 #include "ffn_internal.h"
@@ -94,16 +96,27 @@ struct ActSwiglu {       // h from SU split partials: u of split s at row + 2s*s
 // Weight formats of a slot.  One 16-byte load per thread covers kPerLoad consecutive K
 // values of one row; kThrPerRow threads cover a 128-wide K block of the row and
 // kRowsPerPass rows are loaded per pass of the workgroup.
+// kKPerElem: K values per element of T; kFp8: fp32 row scales after the codes;
+// kBlockScale: one scale byte per 32 K values of a row (kPerLoad is then one block).
 struct WBf16 {           // apex_pack_expert slots: bf16 weights
     using T = uint16_t;
-    static constexpr bool kFp8 = false;
+    static constexpr bool kFp8 = false, kBlockScale = false;
+    static constexpr int kKPerElem = 1;
     static constexpr int kPerLoad = 8, kThrPerRow = kKB / 8, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
 };
 struct WE4M3 {           // apex_pack_expert_fp8 slots: E4M3 codes, fp32 row scales after them
     using T = uint8_t;
-    static constexpr bool kFp8 = true;
+    static constexpr bool kFp8 = true, kBlockScale = false;
+    static constexpr int kKPerElem = 1;
     static constexpr int kPerLoad = 16, kThrPerRow = kKB / 16, kRowsPerPass = kThreads / kThrPerRow;
+    static constexpr int kLoads = kRows / kRowsPerPass;
+};
+struct WMxfp4 {          // apex_pack_expert_mxfp4 slots: two E2M1 codes per byte, block scales
+    using T = uint8_t;
+    static constexpr bool kFp8 = false, kBlockScale = true;
+    static constexpr int kKPerElem = 2;
+    static constexpr int kPerLoad = 32, kThrPerRow = kKB / 32, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
 };
 
@@ -121,6 +134,25 @@ __device__ __forceinline__ void widen_e4m3(uint4 v, uint4 &lo, uint4 &hi) {
     }
     lo = make_uint4(o[0], o[1], o[2], o[3]);
     hi = make_uint4(o[4], o[5], o[6], o[7]);
+}
+
+// 32 E2M1 codes (two per byte of v, the low nibble first) times their block's scale as
+// 32 bf16 values, exactly (an E2M1 value times a power of two is a bf16 value).
+__device__ __forceinline__ void widen_mxfp4(uint4 v, uint32_t scale_byte, uint4 (&out)[4]) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const float sc = apex::ffn::mx_scale(scale_byte);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const auto cvt = [&](auto sel) {   // byte sel of w[q]: elements 2 sel, 2 sel + 1
+            return __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w[q], sc, decltype(sel)::value));
+        };
+        out[q] = make_uint4(cvt(std::integral_constant<int, 0>{}),
+                            cvt(std::integral_constant<int, 1>{}),
+                            cvt(std::integral_constant<int, 2>{}),
+                            cvt(std::integral_constant<int, 3>{}));
+    }
 }
 
 // The pairs p < P with exec_idx[p] == e, in ascending order, into list[]; returns how
@@ -157,9 +189,11 @@ __device__ int expert_pairs(const int32_t *__restrict__ exec_idx, int P, int e, 
 // are clamped) and pieces outside the tile are zeroed after the load instead of
 // branching, so the weight loads issue back to back.
 template <int NW, int MT, class Act, class WF>
-__device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][WF::kLoads], uint4 (&xreg)[MT],
+__device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][WF::kLoads],
+                                          uint32_t (&sreg)[NW][WF::kLoads], uint4 (&xreg)[MT],
                                           const typename WF::T *const (&wbase)[NW],
-                                          size_t wstride, int rows_valid, int K,
+                                          size_t wstride, const uint8_t *const (&sbase)[NW],
+                                          size_t sstride, int rows_valid, int K,
                                           const void *const (&xrow)[MT], const bool (&xok)[MT],
                                           size_t xstride, int k0) {
     const int t = threadIdx.x;
@@ -173,8 +207,10 @@ __device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][WF::kLoads], uint4 (
         for (int j = 0; j < WF::kLoads; ++j) {
             const int row = wr0 + WF::kRowsPerPass * j;
             const int rc = row < rows_valid ? row : rows_valid - 1;
-            const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + wkc);
+            const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
+                                                             wkc / WF::kKPerElem);
             wreg[m][j] = keep_if(v, win && row < rows_valid);
+            if constexpr (WF::kBlockScale) sreg[m][j] = sbase[m][size_t(rc) * sstride + wkc / 32];
         }
     // activation rows past the expert's tokens (tile padding) are not loaded at all
     const int seg = t & 15;
@@ -198,7 +234,8 @@ __device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][WF::kLoads], uint4 (
 // every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.
 template <int NW, int MT, class Act, class WF>
 __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbase)[NW],
-                                              size_t wstride,
+                                              size_t wstride, const uint8_t *const (&sbase)[NW],
+                                              size_t sstride,
                                               int rows_valid, int K, int b_lo, int b_hi,
                                               const void *const (&xrow)[MT],
                                               const bool (&xok)[MT], size_t xstride,
@@ -208,6 +245,7 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
     const int seg = t & 15, r0 = t >> 4;
     const int wseg = t % WF::kThrPerRow, wr0 = t / WF::kThrPerRow;
     uint4 wreg[NW][WF::kLoads], xreg[MT];
+    uint32_t sreg[NW][WF::kLoads];
 #pragma unroll
     for (int m = 0; m < NW; ++m)
 #pragma unroll
@@ -221,8 +259,8 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
         const int q = b + rot;
         return (b_lo + (q >= nb ? q - nb : q)) * kKB;
     };
-    gemm_load<NW, MT, Act, WF>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok, xstride,
-                               kblk(0));
+    gemm_load<NW, MT, Act, WF>(wreg, sreg, xreg, wbase, wstride, sbase, sstride, rows_valid, K,
+                               xrow, xok, xstride, kblk(0));
     for (int b = 0; b < nb; ++b) {
         __syncthreads();   // the previous block's fragments have been read
 #pragma unroll
@@ -230,7 +268,12 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
 #pragma unroll
             for (int j = 0; j < WF::kLoads; ++j) {
                 uint16_t *dst = &Ws[m][wr0 + WF::kRowsPerPass * j][WF::kPerLoad * wseg];
-                if constexpr (WF::kFp8) {
+                if constexpr (WF::kBlockScale) {
+                    uint4 q[4];
+                    widen_mxfp4(wreg[m][j], sreg[m][j], q);
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) *reinterpret_cast<uint4 *>(dst + 8 * c) = q[c];
+                } else if constexpr (WF::kFp8) {
                     uint4 lo, hi;
                     widen_e4m3(wreg[m][j], lo, hi);
                     *reinterpret_cast<uint4 *>(dst) = lo;
@@ -243,8 +286,8 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
         for (int j = 0; j < MT; ++j) *reinterpret_cast<uint4 *>(&Xs[r0 + 16 * j][8 * seg]) = xreg[j];
         __syncthreads();
         if (b + 1 < nb)
-            gemm_load<NW, MT, Act, WF>(wreg, xreg, wbase, wstride, rows_valid, K, xrow, xok,
-                                       xstride, kblk(b + 1));
+            gemm_load<NW, MT, Act, WF>(wreg, sreg, xreg, wbase, wstride, sbase, sstride,
+                                       rows_valid, K, xrow, xok, xstride, kblk(b + 1));
 #pragma unroll
         for (int q = 0; q < kKB / 32; ++q) {
             const int kc = 32 * q + 8 * (lane >> 4);
@@ -303,8 +346,12 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
     split_range(d, gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const typename WF::T *slot = slots + size_t(s) * slot_stride;
-    const typename WF::T *W = slot + size_t(i0) * 2 * d;
-    const typename WF::T *const wbase[2] = {W, W + d};
+    const typename WF::T *W = slot + size_t(i0) * 2 * d / WF::kKPerElem;
+    const typename WF::T *const wbase[2] = {W, W + d / WF::kKPerElem};
+    // MXFP4 block scales of W1 and W3 rows i0.. (unused by the other formats)
+    const uint8_t *sc = reinterpret_cast<const uint8_t *>(slot) + size_t(3) * I * d / 2;
+    const uint8_t *const sbase[2] = {sc + size_t(i0) * (d / 32),
+                                     sc + size_t(I + i0) * (d / 32)};
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
         const void *xrow[MT];
         bool xok[MT];
@@ -316,8 +363,9 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[2][MT];
-        gemm_mainloop<2, MT, ActF32, WF>(wbase, size_t(2) * d, I - i0, d, b_lo, b_hi, xrow, xok,
-                                         0, n_tiles, Ws, Xs, acc);
+        gemm_mainloop<2, MT, ActF32, WF>(wbase, size_t(2) * d / WF::kKPerElem, sbase,
+                                         size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, 0,
+                                         n_tiles, Ws, Xs, acc);
         const int i = i0 + 16 * wave + (lane & 15);
         float s1 = 1.f, s3 = 1.f;
         if constexpr (WF::kFp8) {
@@ -368,7 +416,11 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
     split_range(I, gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const typename WF::T *slot = slots + size_t(s) * slot_stride;
-    const typename WF::T *const wbase[1] = {slot + size_t(2) * I * d + size_t(j0) * I};
+    const typename WF::T *const wbase[1] = {
+        slot + (size_t(2) * I * d + size_t(j0) * I) / WF::kKPerElem};
+    const uint8_t *const sbase[1] = {reinterpret_cast<const uint8_t *>(slot) +
+                                     size_t(3) * I * d / 2 + size_t(2) * I * (d / 32) +
+                                     size_t(j0) * (I / 32)};
     const char *ab = static_cast<const char *>(act);
     float *out = yp + size_t(blockIdx.z) * P * d;
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
@@ -382,8 +434,9 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[1][MT];
-        gemm_mainloop<1, MT, Act, WF>(wbase, size_t(I), d - j0, I, b_lo, b_hi, hrow, hok,
-                                      size_t(P) * I, n_tiles, Ws, Xs, acc);
+        gemm_mainloop<1, MT, Act, WF>(wbase, size_t(I) / WF::kKPerElem, sbase, size_t(I / 32),
+                                      d - j0, I, b_lo, b_hi, hrow, hok, size_t(P) * I, n_tiles,
+                                      Ws, Xs, acc);
         const int j = j0 + 16 * wave + (lane & 15);
         float s2 = 1.f;
         if constexpr (WF::kFp8) s2 = j < d ? row_scales<WF>(slot, d, I)[2 * I + j] : 0.f;
@@ -536,15 +589,20 @@ size_t ffn_grouped_workspace(int B, int d, int I, int k) {
 apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *exec_idx, const float *exec_gate,
                         const int32_t *slot_of_expert, const void *slots, int n_slots,
-                        bool fp8, float *y, int accumulate, void *workspace,
+                        WeightFormat fmt, float *y, int accumulate, void *workspace,
                         hipStream_t stream) {
     const Plan pl = plan_for(B, d, I, k, E, n_slots);
     char *wsb = static_cast<char *>(workspace);
-    if (fp8)
+    if (fmt == WeightFormat::kE4M3)
         return run_grouped<WE4M3>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
                                   static_cast<const uint8_t *>(slots),
                                   apex_expert_bytes_fp8(d, I), n_slots, y, accumulate, wsb,
                                   stream);
+    if (fmt == WeightFormat::kMxfp4)
+        return run_grouped<WMxfp4>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                                   static_cast<const uint8_t *>(slots),
+                                   apex_expert_bytes_mxfp4(d, I), n_slots, y, accumulate, wsb,
+                                   stream);
     return run_grouped<WBf16>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
                               static_cast<const uint16_t *>(slots), size_t(3) * d * I, n_slots,
                               y, accumulate, wsb, stream);

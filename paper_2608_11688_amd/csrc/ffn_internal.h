@@ -12,6 +12,9 @@
 
 namespace apex {
 
+// Expert weight formats of a slot pool.
+enum class WeightFormat { kBf16, kE4M3, kMxfp4 };
+
 // One token: up_b1 then down_b1.  `h` is k x I fp32 scratch.
 size_t ffn_b1_workspace(int d, int I, int k);
 apex_status ffn_b1(const float *x, int d, int I, int E, int k, const int32_t *exec_idx,
@@ -24,14 +27,19 @@ apex_status ffn_b1_fp8(const float *x, int d, int I, int E, int k, const int32_t
                        const uint8_t *slots, int n_slots, float *h, float *y, int accumulate,
                        hipStream_t stream);
 
-// Two or more tokens: grouped GEMMs on the matrix cores, over bf16 slots or (fp8) E4M3
-// slots.  `workspace` is 256-byte aligned and holds ffn_grouped_workspace(B, d, I, k)
+// The same over apex_pack_expert_mxfp4 slots (d and I multiples of 32).
+apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32_t *exec_idx,
+                         const float *exec_gate, const int32_t *slot_of_expert,
+                         const uint8_t *slots, int n_slots, float *h, float *y, int accumulate,
+                         hipStream_t stream);
+
+// Two or more tokens: grouped GEMMs on the matrix cores, over slots of format fmt.  `workspace` is 256-byte aligned and holds ffn_grouped_workspace(B, d, I, k)
 // bytes.
 size_t ffn_grouped_workspace(int B, int d, int I, int k);
 apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *exec_idx, const float *exec_gate,
                         const int32_t *slot_of_expert, const void *slots, int n_slots,
-                        bool fp8, float *y, int accumulate, void *workspace,
+                        WeightFormat fmt, float *y, int accumulate, void *workspace,
                         hipStream_t stream);
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }

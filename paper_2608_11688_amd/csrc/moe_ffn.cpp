@@ -1,5 +1,5 @@
-// apex_moe_ffn and apex_moe_ffn_fp8: argument checks and the choice between the batch-1
-// path (ffn_b1.hip) and the grouped matrix-core path (ffn_gemm.hip).
+// apex_moe_ffn, apex_moe_ffn_fp8 and apex_moe_ffn_mxfp4: argument checks and the choice
+// between the batch-1 paths (ffn_b1*.hip) and the grouped matrix-core path (ffn_gemm.hip).
 #include <hip/hip_runtime.h>
 
 #include "ffn_internal.h"
@@ -11,12 +11,14 @@ extern "C" size_t apex_moe_ffn_workspace_bytes(int B, int d, int I, int k) {
 
 namespace {
 
-apex_status moe_ffn(const char *fn, bool fp8, const float *x, int B, int d, int I, int E, int k,
+apex_status moe_ffn(const char *fn, apex::WeightFormat fmt, const float *x, int B, int d, int I,
+                    int E, int k,
                     const int32_t *exec_idx, const float *exec_gate,
                     const int32_t *slot_of_expert, const void *slots, int n_slots, float *y,
                     int accumulate, void *workspace, size_t workspace_bytes,
                     hipStream_t stream) {
-    const int mult = fp8 ? 16 : 8;   // one 16-byte load holds 16 E4M3 or 8 bf16 weights
+    // one 16-byte load holds 8 bf16 or 16 E4M3 weights; MXFP4 rows are whole 32-value blocks
+    const int mult = fmt == apex::WeightFormat::kBf16 ? 8 : fmt == apex::WeightFormat::kE4M3 ? 16 : 32;
     APEX_REQUIRE(B >= 0, "%s: B=%d must be >= 0", fn, B);
     APEX_REQUIRE(E >= 1, "%s: E=%d must be >= 1", fn, E);
     if (E > APEX_MAX_EXPERTS)
@@ -41,16 +43,19 @@ apex_status moe_ffn(const char *fn, bool fp8, const float *x, int B, int d, int 
                           need);
     if (B == 1) {
         float *h = static_cast<float *>(workspace);
-        if (fp8)
-            return apex::ffn_b1_fp8(x, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
-                                    static_cast<const uint8_t *>(slots), n_slots, h, y,
-                                    accumulate, stream);
+        const uint8_t *codes = static_cast<const uint8_t *>(slots);
+        if (fmt == apex::WeightFormat::kE4M3)
+            return apex::ffn_b1_fp8(x, d, I, E, k, exec_idx, exec_gate, slot_of_expert, codes,
+                                    n_slots, h, y, accumulate, stream);
+        if (fmt == apex::WeightFormat::kMxfp4)
+            return apex::ffn_b1_mxfp4(x, d, I, E, k, exec_idx, exec_gate, slot_of_expert, codes,
+                                      n_slots, h, y, accumulate, stream);
         return apex::ffn_b1(x, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
                             static_cast<const uint16_t *>(slots), n_slots, h, y, accumulate,
                             stream);
     }
     return apex::ffn_grouped(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots,
-                             n_slots, fp8, y, accumulate, workspace, stream);
+                             n_slots, fmt, y, accumulate, workspace, stream);
 }
 
 }  // namespace
@@ -60,8 +65,9 @@ extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, 
                                     const int32_t *slot_of_expert, const uint16_t *slots,
                                     int n_slots, float *y, int accumulate, void *workspace,
                                     size_t workspace_bytes, hipStream_t stream) {
-    return moe_ffn("apex_moe_ffn", false, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
-                   slots, n_slots, y, accumulate, workspace, workspace_bytes, stream);
+    return moe_ffn("apex_moe_ffn", apex::WeightFormat::kBf16, x, B, d, I, E, k, exec_idx,
+                   exec_gate, slot_of_expert, slots, n_slots, y, accumulate, workspace,
+                   workspace_bytes, stream);
 }
 
 extern "C" apex_status apex_moe_ffn_fp8(const float *x, int B, int d, int I, int E, int k,
@@ -69,7 +75,18 @@ extern "C" apex_status apex_moe_ffn_fp8(const float *x, int B, int d, int I, int
                                         const int32_t *slot_of_expert, const void *slots,
                                         int n_slots, float *y, int accumulate, void *workspace,
                                         size_t workspace_bytes, hipStream_t stream) {
-    return moe_ffn("apex_moe_ffn_fp8", true, x, B, d, I, E, k, exec_idx, exec_gate,
-                   slot_of_expert, slots, n_slots, y, accumulate, workspace, workspace_bytes,
-                   stream);
+    return moe_ffn("apex_moe_ffn_fp8", apex::WeightFormat::kE4M3, x, B, d, I, E, k, exec_idx,
+                   exec_gate, slot_of_expert, slots, n_slots, y, accumulate, workspace,
+                   workspace_bytes, stream);
+}
+
+extern "C" apex_status apex_moe_ffn_mxfp4(const float *x, int B, int d, int I, int E, int k,
+                                          const int32_t *exec_idx, const float *exec_gate,
+                                          const int32_t *slot_of_expert, const void *slots,
+                                          int n_slots, float *y, int accumulate,
+                                          void *workspace, size_t workspace_bytes,
+                                          hipStream_t stream) {
+    return moe_ffn("apex_moe_ffn_mxfp4", apex::WeightFormat::kMxfp4, x, B, d, I, E, k,
+                   exec_idx, exec_gate, slot_of_expert, slots, n_slots, y, accumulate,
+                   workspace, workspace_bytes, stream);
 }

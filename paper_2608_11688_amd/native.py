@@ -23,7 +23,7 @@ PLAN_LIB_PATH = os.path.join(PKG, "libapex_plan.so")
 APEX_OK, APEX_E_INVAL, APEX_E_UNSUPPORTED, APEX_E_HIP, APEX_E_CAPACITY = 0, -1, -2, -3, -4
 SEL_CUMPROB, SEL_ORDINAL_CDF, SEL_STATIC, SEL_NONE = 0, 1, 2, 3
 MODE_EXACT, MODE_STALL_FREE = 0, 1
-WEIGHTS_BF16, WEIGHTS_FP8_E4M3 = 0, 1
+WEIGHTS_BF16, WEIGHTS_FP8_E4M3, WEIGHTS_MXFP4 = 0, 1, 2
 ABI_VERSION = 3
 MAX_EXPERTS = 64
 MAX_PAIRS = 1024
@@ -81,9 +81,12 @@ SIGNATURES = {
     "apex_pack_expert": (I32, [P, P, P, I32, I32, P]),
     "apex_expert_bytes_fp8": (SZ, [I32, I32]),
     "apex_pack_expert_fp8": (I32, [P, P, P, I32, I32, P]),
+    "apex_expert_bytes_mxfp4": (SZ, [I32, I32]),
+    "apex_pack_expert_mxfp4": (I32, [P, P, P, I32, I32, P]),
     "apex_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32, I32]),
     "apex_moe_ffn": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_fp8": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
+    "apex_moe_ffn_mxfp4": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_attention_workspace_bytes": (SZ, [I32, I32, I32, I32, I32]),
     "apex_attention_decode": (I32, [P, P, P, I32, I32, I32, I32, I32, P, P, I32, I32, P, P, SZ,
                                     P]),
@@ -108,7 +111,8 @@ SIGNATURES = {
 }
 
 HOST_ONLY = ("apex_abi_version", "apex_last_error", "apex_expert_bytes", "apex_pack_expert",
-             "apex_expert_bytes_fp8", "apex_pack_expert_fp8", "apex_plan_residency")
+             "apex_expert_bytes_fp8", "apex_pack_expert_fp8", "apex_expert_bytes_mxfp4",
+             "apex_pack_expert_mxfp4", "apex_plan_residency")
 
 
 def header_functions(path=HEADER):
@@ -207,6 +211,14 @@ def apex_pack_expert_fp8(w1, w3, w2, d, I, out, L=None):
     _call("apex_pack_expert_fp8", ptr(w1), ptr(w3), ptr(w2), d, I, ptr(out), L=L)
 
 
+def apex_expert_bytes_mxfp4(d, I, L=None):
+    return (L or lib()).apex_expert_bytes_mxfp4(d, I)
+
+
+def apex_pack_expert_mxfp4(w1, w3, w2, d, I, out, L=None):
+    _call("apex_pack_expert_mxfp4", ptr(w1), ptr(w3), ptr(w2), d, I, ptr(out), L=L)
+
+
 def apex_moe_ffn_workspace_bytes(B, d, I, k):
     return lib().apex_moe_ffn_workspace_bytes(B, d, I, k)
 
@@ -223,6 +235,31 @@ def apex_moe_ffn_fp8(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slot
     _call("apex_moe_ffn_fp8", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
           ptr(slot_of_expert), ptr(slots), n_slots, ptr(y), int(accumulate), ptr(workspace),
           workspace_bytes, stream)
+
+
+def apex_moe_ffn_mxfp4(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots,
+                       y, accumulate, workspace, workspace_bytes, stream=None):
+    _call("apex_moe_ffn_mxfp4", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
+          ptr(slot_of_expert), ptr(slots), n_slots, ptr(y), int(accumulate), ptr(workspace),
+          workspace_bytes, stream)
+
+
+# weight format name -> (decode-driver code, bytes of one packed expert, packer, FFN entry)
+WEIGHT_FORMATS = {
+    "bf16": (WEIGHTS_BF16, "apex_expert_bytes", "apex_pack_expert", "apex_moe_ffn"),
+    "fp8": (WEIGHTS_FP8_E4M3, "apex_expert_bytes_fp8", "apex_pack_expert_fp8", "apex_moe_ffn_fp8"),
+    "mxfp4": (WEIGHTS_MXFP4, "apex_expert_bytes_mxfp4", "apex_pack_expert_mxfp4",
+              "apex_moe_ffn_mxfp4"),
+}
+
+
+def weight_format(name):
+    """(code, expert_bytes(d, I), pack(w1, w3, w2, d, I, out), moe_ffn(...)) of a format."""
+    if name not in WEIGHT_FORMATS:
+        raise ValueError(f"weights must be one of {sorted(WEIGHT_FORMATS)}, not {name!r}")
+    code, nbytes, pack, ffn = WEIGHT_FORMATS[name]
+    g = globals()
+    return code, g[nbytes], g[pack], g[ffn]
 
 
 def apex_attention_workspace_bytes(B, H, G, hd, ctx_max):

@@ -59,8 +59,7 @@ class DecodeRunner:
         self.compute = torch.cuda.current_stream()
         self.side = torch.cuda.Stream()
         self.cs, self.ss = self.compute.cuda_stream, self.side.cuda_stream
-        if weights not in ("bf16", "fp8"):
-            raise ValueError(f"weights must be 'bf16' or 'fp8', not {weights!r}")
+        self._wcode, self._wbytes, self._wpack, self.moe_ffn = native.weight_format(weights)
         self.weights = weights
         if window not in ("spin", "attention"):
             raise ValueError(f"window must be 'spin' or 'attention', not {window!r}")
@@ -92,8 +91,7 @@ class DecodeRunner:
                                    k_max=cfg.k_max, policy=policy, tau=self.tau,
                                    static_delta=static_delta, mode=mode, t_attn_us=t_attn_us,
                                    n_scratch=self.n_scratch,
-                                   weights=(native.WEIGHTS_FP8_E4M3 if weights == "fp8"
-                                            else native.WEIGHTS_BF16),
+                                   weights=self._wcode,
                                    attn_heads=cfg.n_heads if window == "attention" else 0,
                                    attn_kv_heads=cfg.n_kv_heads, attn_ctx=ctx,
                                    n_shared=cfg.shared, I_shared=cfg.shared_I)
@@ -135,15 +133,10 @@ class DecodeRunner:
     # ------------------------------------------------------------------ setup
     def expert_bytes(self, I):
         """Bytes of one packed expert of intermediate size I in this runner's format."""
-        if self.weights == "fp8":
-            return native.apex_expert_bytes_fp8(self.cfg.d, I)
-        return native.apex_expert_bytes(self.cfg.d, I)
+        return self._wbytes(self.cfg.d, I)
 
     def pack(self, w1, w3, w2, d, I, out):
-        if self.weights == "fp8":
-            native.apex_pack_expert_fp8(w1, w3, w2, d, I, out)
-        else:
-            native.apex_pack_expert(w1, w3, w2, d, I, out)
+        self._wpack(w1, w3, w2, d, I, out)
 
     def _make_layer(self, l, pool, cdf):
         torch, cfg = self.torch, self.cfg

@@ -212,3 +212,14 @@ def test_decode_phi_shape(batch, mode):
 def test_decode_deepseek_shape_fp8_shared_experts():
     # the shared pool is packed in the layer's weight format as well
     check_decode(configs.DEEPSEEK_16B, 1, native.MODE_EXACT, 2, [7], weights="fp8")
+
+
+def test_decode_granite1b_mxfp4_experts():
+    # 4-bit experts through the whole decode path: packing, prefetch copies, misses, FFN
+    cfg = configs.GRANITE_1B
+    st = check_decode(cfg, 1, native.MODE_EXACT, 4, [0, 23], weights="mxfp4")
+    assert st["copies"] > 0
+
+
+def test_decode_deepseek_shape_mxfp4_batch16():
+    check_decode(configs.DEEPSEEK_16B, 16, native.MODE_STALL_FREE, 2, [4], weights="mxfp4")

@@ -204,8 +204,8 @@ class FfnCase:
         rng = np.random.default_rng(seed)
         self.cfg, self.B, self.weights = cfg, B, weights
         E, k = cfg.E, cfg.k
-        fp8 = weights == "fp8"
-        self.S = (native.apex_expert_bytes_fp8 if fp8 else native.apex_expert_bytes)(cfg.d, cfg.I)
+        _, nbytes, pack, self.ffn = native.weight_format(weights)
+        self.S = nbytes(cfg.d, cfg.I)
         self.x = rng.standard_normal((B, cfg.d)).astype(np.float32)
         self.exec_idx = np.stack([rng.choice(E, k, replace=False) for _ in range(B)]).astype(np.int32)
         if B > 1:
@@ -221,14 +221,12 @@ class FfnCase:
         for e, s in zip(self.resident, slot_ids):
             self.table[e] = s
         self.bits = {}
-        if fp8:
+        if weights != "bf16":
             pool = np.zeros(self.n_slots * self.S, np.uint8)
             piece = lambda s: pool[s * self.S:(s + 1) * self.S]
-            pack = native.apex_pack_expert_fp8
         else:
             pool = np.zeros(self.n_slots * self.S // 2, np.uint16)
             piece = lambda s: pool[s * self.S // 2:(s + 1) * self.S // 2]
-            pack = native.apex_pack_expert
         for e in self.resident:
             self.bits[e] = inputs.expert_weights(cfg, 0, e)
             pack(*self.bits[e], cfg.d, cfg.I, piece(int(self.table[e])))
@@ -242,8 +240,7 @@ class FfnCase:
         ws = torch.full((ws_bytes,), 0xAB, dtype=torch.uint8, device="cuda")
         y = dev(torch, y0) if y0 is not None else torch.full((B, cfg.d), float("nan"),
                                                               device="cuda")
-        ffn = native.apex_moe_ffn_fp8 if self.weights == "fp8" else native.apex_moe_ffn
-        ffn(dev(torch, self.x), B, cfg.d, cfg.I, cfg.E, cfg.k, dev(torch, self.exec_idx),
+        self.ffn(dev(torch, self.x), B, cfg.d, cfg.I, cfg.E, cfg.k, dev(torch, self.exec_idx),
             dev(torch, self.gate), dev(torch, table), self.pool, self.n_slots, y, accumulate, ws,
             ws_bytes)
         torch.cuda.synchronize()
@@ -395,6 +392,49 @@ def test_ffn_fp8_mixtral_batch1_and_two_passes(torch):
     y1 = case.run(t1)
     ffn_close(y1, case.oracle(only=first), "fp8 pass 1")
     ffn_close(case.run(t2, y0=y1, accumulate=1), case.oracle(), "fp8 pass 1 + pass 2")
+
+
+MXFP4_SHAPES = [
+    # MXFP4 experts (apex_moe_ffn_mxfp4): d and I multiples of 32
+    (configs.GRANITE_1B, 1), (configs.GRANITE_3B, 1), (configs.OLMOE, 1), (configs.TINY, 1),
+    (configs.PHI_7B, 1), (configs.DEEPSEEK_16B, 1),         # d = 4096; I = 1472
+    (configs.GRANITE_3B, 8), (configs.OLMOE, 16),
+    (shape("fp4_b48", 440, 512, 6, 2, I=256), 48),          # four token tiles per pass
+    (shape("fp4_split_a", 441, 800, 4, 2, I=992), 4),       # split K; ragged last K block
+    (shape("fp4_split_b", 442, 992, 4, 2, I=800), 5),
+    (shape("fp4_small", 443, 32, 3, 2, I=64), 3),           # one block per row
+]
+
+
+@pytest.mark.parametrize("cfg,B", MXFP4_SHAPES, ids=[f"{c.name}-B{b}" for c, b in MXFP4_SHAPES])
+def test_ffn_mxfp4_parity(torch, cfg, B):
+    case = FfnCase(torch, cfg, B, seed=cfg.cfg_id * 11 + B, weights="mxfp4")
+    y = case.run()
+    print(cfg.name, B, ffn_close(y, case.oracle(), f"{cfg.name} B{B} mxfp4"))
+
+
+def test_ffn_mxfp4_mixtral_batch1_and_two_passes(torch):
+    cfg = configs.MIXTRAL
+    case = FfnCase(torch, cfg, 1, seed=52, weights="mxfp4")
+    print("mixtral mxfp4", ffn_close(case.run(), case.oracle(), "mixtral B1 mxfp4"))
+    cfg = shape("fp4_pass", 444, 512, 12, 4, I=256)
+    case = FfnCase(torch, cfg, 20, seed=53, n_slots_extra=2, weights="mxfp4")
+    res = case.resident
+    first, second = res[: len(res) // 2], res[len(res) // 2:]
+    t1, t2 = case.table.copy(), case.table.copy()
+    t1[second] = -1
+    t2[first] = -1
+    y1 = case.run(t1)
+    ffn_close(y1, case.oracle(only=first), "mxfp4 pass 1")
+    ffn_close(case.run(t2, y0=y1, accumulate=1), case.oracle(), "mxfp4 pass 1 + pass 2")
+
+
+def test_ffn_mxfp4_rejects_partial_blocks(torch):
+    A = 4096
+    with pytest.raises(native.ApexError):
+        native.apex_moe_ffn_mxfp4(A, 1, 48, 64, 4, 1, A, A, A, A, 1, A, 0, A, 1 << 20)
+    with pytest.raises(native.ApexError):
+        native.apex_moe_ffn_mxfp4(A, 1, 64, 48, 4, 1, A, A, A, A, 1, A, 0, A, 1 << 20)
 
 
 def test_ffn_two_passes_equal_one(torch):

@@ -161,6 +161,42 @@ def test_workspace_size():
     assert big >= 512 * (1024 * 2 + 2048 * 4) + 64 * 2048 * 2 and big % 256 == 0
 
 
+def test_pack_expert_mxfp4_matches_the_oracle_quantiser(plan_lib):
+    # the packed nibbles and block scales equal the oracle's own MXFP4 quantisation, byte
+    # for byte, in the documented layout
+    from oracle import mxfp4
+    from oracle.bf16 import bf16_to_f64
+    d, I = 96, 64
+    rng = np.random.default_rng(42)
+
+    def bf16(a):
+        return (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    w1 = bf16(rng.standard_normal((I, d)) * 0.02)
+    w3 = bf16(rng.standard_normal((I, d)) * 1e-30)      # tiny blocks: very small exponents
+    w2 = bf16(rng.standard_normal((d, I)) * 0.02)
+    w1[5, 32:64] = 0                                     # an all-zero block
+    w3[2, 3] = bf16([-1.0])[0]                           # a negative peak
+    w2[7, :32] = bf16(np.linspace(-6.0, 6.0, 32))        # ties and the saturated top
+    nbytes = native.apex_expert_bytes_mxfp4(d, I, L=plan_lib)
+    assert nbytes == 3 * d * I // 2 + 3 * d * I // 32
+    out = np.zeros(nbytes, np.uint8)
+    native.apex_pack_expert_mxfp4(w1, w3, w2, d, I, out, L=plan_lib)
+    rows = out[:I * d].reshape(I, d)                    # [W1 codes | W3 codes] per row
+    c2 = out[I * d:3 * I * d // 2].reshape(d, I // 2)
+    sc = out[3 * I * d // 2:]
+    s1, s3, s2 = (sc[:I * d // 32].reshape(I, d // 32),
+                  sc[I * d // 32:2 * I * d // 32].reshape(I, d // 32),
+                  sc[2 * I * d // 32:].reshape(d, I // 32))
+    for mat, codes, scales in ((w1, rows[:, :d // 2], s1), (w3, rows[:, d // 2:], s3),
+                               (w2, c2, s2)):
+        want_codes, X = mxfp4.quantize_blocks(bf16_to_f64(mat))
+        assert np.array_equal(scales, mxfp4.scale_bytes(X))
+        assert np.array_equal(codes, mxfp4.pack_nibbles(want_codes))
+    assert s1[5, 1] == 0 and not rows[5, 16:32].any()
+    with pytest.raises(native.ApexError):
+        native.apex_pack_expert_mxfp4(w1, w3, w2, 80, I, out, L=plan_lib)  # d not a multiple of 32
+
+
 def test_pack_expert_fp8_matches_the_oracle_quantiser(plan_lib):
     # the packed codes and scales equal the oracle's own E4M3 quantisation, byte for byte
     from oracle import fp8
