@@ -292,12 +292,13 @@ apex_status apex_plan_residency(int E, int C, const int32_t *pf_idx, const int32
  * Prefetch of one layer (Sec. IV-A: asynchronous transfers for K_p issued while
  * attention runs; Sec. V-B prefetch-overlap bound, Eq. 12).
  * Runs apex_plan_residency on the host copy of the route output, then:
- *   side:    wait readers_done (if not NULL); one host-to-device copy per planned
- *            expert, host_experts[e] -> slots[s]; record `ready`;
+ *   side:    wait readers_done (if not NULL and not yet complete); one host-to-device
+ *            copy per planned expert, host_experts[e] -> slots[s]; record `ready`;
  *   compute: write the new table to slot_of_expert_dev[E] and, if not NULL, the
  *            resident mask to avail_dev[E] (1 = resident).
  * The caller must make the expert FFN wait for `ready` (apex_stream_wait_event)
- * before it reads the slots, and record readers_done on the compute stream after the
+ * before it reads the slots (when n_copied is 0 the slots are unchanged and that wait
+ * may be left out), and record readers_done on the compute stream after the
  * last kernel that reads this layer's slots.  The host call returns once everything
  * is enqueued; the copies run on the DMA engines.
  *   host_experts      pinned bf16 [E][expert_bytes/2] (apex_pack_expert layout)
@@ -325,8 +326,10 @@ apex_status apex_expert_prefetch(const uint16_t *host_experts, uint16_t *slots,
  * after waiting for scratch_free (if not NULL), then `ready` is recorded on side.
  * On `compute`, miss_table_dev[E] is written with miss_table[e] = i for the i-th
  * missing expert and -1 otherwise, so a second apex_moe_ffn pass over the scratch
- * pool with accumulate = 1 adds exactly the missing experts.  Returns APEX_E_CAPACITY
- * (enqueueing nothing) if |M| > n_scratch.
+ * pool with accumulate = 1 adds exactly the missing experts.  If M is empty nothing is
+ * enqueued (no second pass is needed; the table and `ready` are left as they were).
+ * Returns APEX_E_CAPACITY (enqueueing nothing) if |M| > n_scratch.  A wait on an event
+ * that has already completed is skipped (it would be a no-op).
  *   route_idx        host int32 [B, k] (apex_gate_topk route output, complete)
  *   expert_of_slot   host int32 [C] (resident set after this step's prefetch)
  *   missing          host int32 [min(B*k, E)] out or NULL;  n_missing host out

@@ -348,7 +348,9 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
                          0);
             if (st != APEX_OK) return st;
         }
-        APEX_HIP(hipStreamWaitEvent(cs, dec->ready[l], 0));
+        // the slots this layer's FFN reads: the copies just issued (none: every earlier copy
+        // into them completed before an earlier FFN of this layer read them)
+        if (n_copy > 0) APEX_HIP(hipStreamWaitEvent(cs, dec->ready[l], 0));
         st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], shared ? 1 : 0);
         if (st != APEX_OK) return st;
         int n_miss = 0;

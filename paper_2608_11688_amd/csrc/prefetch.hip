@@ -30,6 +30,15 @@ __global__ void publish_table_kernel(Table t, int E, int32_t *__restrict__ slot_
     }
 }
 
+// Makes `stream` wait for `ev` unless the event has already completed (or was never
+// recorded): the wait would then be a no-op, and enqueueing a cross-stream wait costs the
+// host more than a kernel launch.
+apex_status wait_unless_done(hipStream_t stream, hipEvent_t ev) {
+    if (!ev || hipEventQuery(ev) == hipSuccess) return APEX_OK;
+    APEX_HIP(hipStreamWaitEvent(stream, ev, 0));
+    return APEX_OK;
+}
+
 apex_status publish(const Table &t, int E, int32_t *slot_dev, uint8_t *avail_dev,
                     hipStream_t stream) {
     hipLaunchKernelGGL(publish_table_kernel, dim3(1), dim3(APEX_MAX_EXPERTS), 0, stream, t, E,
@@ -59,7 +68,8 @@ extern "C" apex_status apex_expert_prefetch(
                                          last_used, ce.data(), cs.data(), &n);
     if (st != APEX_OK) return st;
 
-    if (readers_done) APEX_HIP(hipStreamWaitEvent(side, readers_done, 0));
+    st = wait_unless_done(side, readers_done);
+    if (st != APEX_OK) return st;
     const char *src = reinterpret_cast<const char *>(host_experts);
     char *dst = reinterpret_cast<char *>(slots);
     for (int i = 0; i < n; ++i)
@@ -115,7 +125,12 @@ extern "C" apex_status apex_expert_fetch_misses(
         return apex::fail(APEX_E_CAPACITY, "%s: %d missing experts > %d scratch slots", fn, n,
                           n_scratch);
 
-    if (n > 0 && scratch_free) APEX_HIP(hipStreamWaitEvent(side, scratch_free, 0));
+    if (missing)
+        for (int i = 0; i < n; ++i) missing[i] = list[i];
+    *n_missing = n;
+    if (n == 0) return APEX_OK;   // no second pass reads the table: nothing to enqueue
+    apex_status st = wait_unless_done(side, scratch_free);
+    if (st != APEX_OK) return st;
     const char *src = reinterpret_cast<const char *>(host_experts);
     char *dst = reinterpret_cast<char *>(scratch);
     for (int i = 0; i < n; ++i)
@@ -126,10 +141,5 @@ extern "C" apex_status apex_expert_fetch_misses(
     Table t;
     std::fill(t.slot, t.slot + APEX_MAX_EXPERTS, -1);
     for (int i = 0; i < n; ++i) t.slot[list[i]] = i;
-    apex_status st = publish(t, E, miss_table_dev, nullptr, compute);
-    if (st != APEX_OK) return st;
-    if (missing)
-        for (int i = 0; i < n; ++i) missing[i] = list[i];
-    *n_missing = n;
-    return APEX_OK;
+    return publish(t, E, miss_table_dev, nullptr, compute);
 }
