@@ -223,3 +223,27 @@ def test_decode_granite1b_mxfp4_experts():
 
 def test_decode_deepseek_shape_mxfp4_batch16():
     check_decode(configs.DEEPSEEK_16B, 16, native.MODE_STALL_FREE, 2, [4], weights="mxfp4")
+
+
+def test_decode_create_rejects_bad_configurations():
+    # validation happens before anything is allocated or enqueued
+    from paper_2608_11688_amd.runtime import DecodeRunner
+    import dataclasses
+    cfg = configs.MoEConfig("val", 450, L=1, d=256, E=8, k=2, I=96, C=4, k_max=4, tau=0.9,
+                            steps=2)
+    # MXFP4 needs d and I multiples of 32 (I = 96 is; 80 is not)
+    bad_i = dataclasses.replace(cfg, I=80)
+    with pytest.raises(native.ApexError):
+        DecodeRunner(bad_i, batch=1, steps=1, weights="mxfp4")
+    # shared experts need an intermediate size that fits the weight format
+    bad_shared = dataclasses.replace(cfg, shared=1, I_shared=40)
+    with pytest.raises(native.ApexError):
+        DecodeRunner(bad_shared, batch=1, steps=1, weights="fp8")
+    # a good configuration still builds and steps
+    r = DecodeRunner(dataclasses.replace(cfg, shared=1, I_shared=64), batch=1, steps=1,
+                     weights="mxfp4")
+    try:
+        r.step()
+        r.finish()
+    finally:
+        r.close()
