@@ -272,7 +272,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              f"(the hot path is single-GPU; see DESIGN.md for how it would shard)",
+              f"(the hot path runs on one GPU; sharding it across GPUs is not built)",
               file=sys.stderr)
         return 2
     import torch
