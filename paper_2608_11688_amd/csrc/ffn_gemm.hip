@@ -97,24 +97,31 @@ struct ActSwiglu {       // h from SU split partials: u of split s at row + 2s*s
 // values of one row; kThrPerRow threads cover a 128-wide K block of the row and
 // kRowsPerPass rows are loaded per pass of the workgroup.
 // kKPerElem: K values per element of T; kFp8: fp32 row scales after the codes;
-// kBlockScale: one scale byte per 32 K values of a row (kPerLoad is then one block).
+// kBlockScale: one scale byte per 32 K values of a row (kPerLoad is then one block);
+// kCodes: the codes go to LDS as bytes, in K blocks of kb<MT>() values, and are widened
+// at fragment read (gemm_mainloop_codes); otherwise bf16 tiles of kKB (gemm_mainloop).
 struct WBf16 {           // apex_pack_expert slots: bf16 weights
     using T = uint16_t;
-    static constexpr bool kFp8 = false, kBlockScale = false;
+    static constexpr bool kFp8 = false, kBlockScale = false, kCodes = false;
+    template <int MT> static constexpr int kb() { return kKB; }
     static constexpr int kKPerElem = 1;
     static constexpr int kPerLoad = 8, kThrPerRow = kKB / 8, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
 };
 struct WE4M3 {           // apex_pack_expert_fp8 slots: E4M3 codes, fp32 row scales after them
     using T = uint8_t;
-    static constexpr bool kFp8 = true, kBlockScale = false;
+    static constexpr bool kFp8 = true, kBlockScale = false, kCodes = true;
+    // 256 bytes per row with one token tile, 128 with more (a smaller activation tile)
+    template <int MT> static constexpr int kb() { return MT == 1 ? 256 : 128; }
     static constexpr int kKPerElem = 1;
     static constexpr int kPerLoad = 16, kThrPerRow = kKB / 16, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
 };
 struct WMxfp4 {          // apex_pack_expert_mxfp4 slots: two E2M1 codes per byte, block scales
     using T = uint8_t;
-    static constexpr bool kFp8 = false, kBlockScale = true;
+    static constexpr bool kFp8 = false, kBlockScale = true, kCodes = true;
+    // 256 bytes per row with one token tile, 128 with more (a smaller activation tile)
+    template <int MT> static constexpr int kb() { return MT == 1 ? 512 : 256; }
     static constexpr int kKPerElem = 2;
     static constexpr int kPerLoad = 32, kThrPerRow = kKB / 32, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
@@ -308,10 +315,174 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
     }
 }
 
-__device__ __forceinline__ void split_range(int K, int splits, int z, int &b_lo, int &b_hi) {
-    const int nb = (K + kKB - 1) / kKB;
+__device__ __forceinline__ void split_range(int K, int kb, int splits, int z, int &b_lo,
+                                            int &b_hi) {
+    const int nb = (K + kb - 1) / kb;
     b_lo = z * nb / splits;
     b_hi = (z + 1) * nb / splits;
+}
+
+// LDS of one workgroup's tile: bf16 weights and activations for gemm_mainloop; codes,
+// MXFP4 block scales and activations for gemm_mainloop_codes.  Rows are padded by 16
+// bytes so that the 16 rows of a fragment read fall in distinct banks.
+template <int NW, int MT, class WF, bool C = WF::kCodes>
+struct GemmLds {
+    uint16_t Ws[NW][kRows][kLdsRow];
+    uint16_t Xs[16 * MT][kLdsRow];
+};
+template <int NW, int MT, class WF>
+struct GemmLds<NW, MT, WF, true> {
+    static constexpr int KB = WF::template kb<MT>();   // K values per block
+    static constexpr int RB = KB / WF::kKPerElem;      // code bytes per row and block
+    uint8_t Wc[NW][kRows][RB + 16];
+    uint8_t Sc[NW][kRows][KB / 32];                    // MXFP4 block scales
+    uint16_t Xs[16 * MT][KB + 8];
+};
+
+// 8 consecutive codes of row rr at K offset kc of the staged block, widened to bf16
+// exactly (E4M3 values are bf16 values; an E2M1 value times its power-of-two scale too).
+template <int NW, int MT, class WF>
+__device__ __forceinline__ uint4 widen8(const GemmLds<NW, MT, WF, true> &lds, int m, int rr,
+                                        int kc) {
+    if constexpr (WF::kBlockScale) {
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        const uint32_t c = *reinterpret_cast<const uint32_t *>(&lds.Wc[m][rr][kc / 2]);
+        const float sc = apex::ffn::mx_scale(lds.Sc[m][rr][kc / 32]);
+        return make_uint4(
+            __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(c, sc, 0)),
+            __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(c, sc, 1)),
+            __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(c, sc, 2)),
+            __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(c, sc, 3)));
+    } else {
+        const uint2 c = *reinterpret_cast<const uint2 *>(&lds.Wc[m][rr][kc]);
+        const auto a = __builtin_amdgcn_cvt_pk_f32_fp8(int(c.x), false);
+        const auto b = __builtin_amdgcn_cvt_pk_f32_fp8(int(c.x), true);
+        const auto e = __builtin_amdgcn_cvt_pk_f32_fp8(int(c.y), false);
+        const auto f = __builtin_amdgcn_cvt_pk_f32_fp8(int(c.y), true);
+        const auto pk = [](float lo, float hi) {
+            return (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xffff0000u);
+        };
+        return make_uint4(pk(a[0], a[1]), pk(b[0], b[1]), pk(e[0], e[1]), pk(f[0], f[1]));
+    }
+}
+
+// Mainloop for the compact formats (E4M3, MXFP4).  Same tile and MFMA work as
+// gemm_mainloop, but a K block holds as many weight bytes as a bf16 block (KB = 256 or
+// 512 values), its codes go to LDS unchanged (with the MXFP4 block scales beside them),
+// and each wavefront widens its own fragments right before the matrix cores take them:
+// every code is still converted once, while the bytes in flight per block match bf16
+// and the LDS moves a fraction of the widened data.
+template <int NW, int MT, class Act, class WF>
+__device__ __forceinline__ void gemm_mainloop_codes(
+    const uint8_t *const (&wbase)[NW], size_t wstride, const uint8_t *const (&sbase)[NW],
+    size_t sstride, int rows_valid, int K, int b_lo, int b_hi, const void *const (&xrow)[MT],
+    const bool (&xok)[MT], size_t xstride, int n_tiles, GemmLds<NW, MT, WF, true> &lds,
+    floatx4 (&acc)[NW][MT]) {
+    using L = GemmLds<NW, MT, WF, true>;
+    constexpr int KB = L::KB, RB = L::RB;
+    constexpr int TPR = RB / 16;              // threads per row of a block
+    constexpr int RPP = kThreads / TPR;       // rows per pass
+    constexpr int NL = kRows / RPP;           // 16-byte weight loads per thread and matrix
+    constexpr int QX = KB / 128;              // 8-value activation pieces per token row
+    constexpr int KPL = 16 * WF::kKPerElem;   // K values per 16-byte load
+    const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
+    const int wseg = t % TPR, wr0 = t / TPR;
+    const int seg = t & 15, r0 = t >> 4;
+    uint4 wreg[NW][NL], xreg[QX][MT];
+    uint32_t sreg[NW][NL];
+#pragma unroll
+    for (int m = 0; m < NW; ++m)
+#pragma unroll
+        for (int tt = 0; tt < MT; ++tt) acc[m][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int nb = b_hi - b_lo;
+    if (nb <= 0) return;
+    const int rot = int((blockIdx.x * 7u + blockIdx.y * 13u) % unsigned(nb));
+    const auto kblk = [nb, rot, b_lo](int b) {
+        const int q = b + rot;
+        return (b_lo + (q >= nb ? q - nb : q)) * KB;
+    };
+    // One block into registers: every address valid (rows and K clamped), pieces outside
+    // the tile zeroed after the load.
+    const auto load = [&](int k0) {
+        const int wk = k0 + KPL * wseg;
+        const bool win = wk < K;
+        const int wkc = win ? wk : K - KPL;
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int j = 0; j < NL; ++j) {
+                const int row = wr0 + RPP * j;
+                const int rc = row < rows_valid ? row : rows_valid - 1;
+                const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
+                                                                 wkc / WF::kKPerElem);
+                wreg[m][j] = keep_if(v, win && row < rows_valid);
+                if constexpr (WF::kBlockScale) sreg[m][j] = sbase[m][size_t(rc) * sstride + wkc / 32];
+            }
+#pragma unroll
+        for (int q = 0; q < QX; ++q) {
+            const int kk = k0 + 128 * q + 8 * seg;
+            const bool in = kk < K;
+            const int kc = in ? kk : K - 8;
+#pragma unroll
+            for (int j = 0; j < MT; ++j) {
+                uint4 v = make_uint4(0u, 0u, 0u, 0u);
+                if (in && xok[j]) v = Act::load(xrow[j], kc, xstride);
+                xreg[q][j] = v;
+            }
+        }
+    };
+    load(kblk(0));
+    for (int b = 0; b < nb; ++b) {
+        __syncthreads();   // the previous block's fragments have been read
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int j = 0; j < NL; ++j) {
+                const int row = wr0 + RPP * j;
+                *reinterpret_cast<uint4 *>(&lds.Wc[m][row][16 * wseg]) = wreg[m][j];
+                if constexpr (WF::kBlockScale) lds.Sc[m][row][wseg] = uint8_t(sreg[m][j]);
+            }
+#pragma unroll
+        for (int q = 0; q < QX; ++q)
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                *reinterpret_cast<uint4 *>(&lds.Xs[r0 + 16 * j][128 * q + 8 * seg]) = xreg[q][j];
+        __syncthreads();
+        if (b + 1 < nb) load(kblk(b + 1));
+        const int rr = 16 * wave + (lane & 15);
+#pragma unroll 4
+        for (int q = 0; q < KB / 32; ++q) {
+            const int kc = 32 * q + 8 * (lane >> 4);
+            uint4 wop[NW];
+#pragma unroll
+            for (int m = 0; m < NW; ++m) wop[m] = widen8(lds, m, rr, kc);
+#pragma unroll
+            for (int tt = 0; tt < MT; ++tt) {
+                if (tt >= n_tiles) continue;
+                const uint4 xop = *reinterpret_cast<const uint4 *>(&lds.Xs[16 * tt + (lane & 15)][kc]);
+#pragma unroll
+                for (int m = 0; m < NW; ++m)
+                    acc[m][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        as_bf16x8(xop), as_bf16x8(wop[m]), acc[m][tt], 0, 0, 0);
+            }
+        }
+    }
+}
+
+// The tile's mainloop for weight format WF.
+template <int NW, int MT, class Act, class WF>
+__device__ __forceinline__ void gemm_tile(const typename WF::T *const (&wbase)[NW],
+                                          size_t wstride, const uint8_t *const (&sbase)[NW],
+                                          size_t sstride, int rows_valid, int K, int b_lo,
+                                          int b_hi, const void *const (&xrow)[MT],
+                                          const bool (&xok)[MT], size_t xstride, int n_tiles,
+                                          GemmLds<NW, MT, WF> &lds, floatx4 (&acc)[NW][MT]) {
+    if constexpr (WF::kCodes)
+        gemm_mainloop_codes<NW, MT, Act, WF>(wbase, wstride, sbase, sstride, rows_valid, K,
+                                             b_lo, b_hi, xrow, xok, xstride, n_tiles, lds, acc);
+    else
+        gemm_mainloop<NW, MT, Act, WF>(wbase, wstride, sbase, sstride, rows_valid, K, b_lo,
+                                       b_hi, xrow, xok, xstride, n_tiles, lds.Ws, lds.Xs, acc);
 }
 
 // The fp32 row scales of an apex_pack_expert_fp8 slot: W1 rows, W3 rows, W2 rows.
@@ -332,8 +503,7 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
     const int32_t *__restrict__ slot_of_expert, int n_slots,
     const typename WF::T *__restrict__ slots, size_t slot_stride, __bf16 *__restrict__ hb,
     float *__restrict__ uv) {
-    __shared__ uint16_t Ws[2][kRows][kLdsRow];
-    __shared__ uint16_t Xs[16 * MT][kLdsRow];
+    __shared__ __align__(16) GemmLds<2, MT, WF> lds;
     __shared__ int list[APEX_MAX_PAIRS];
     __shared__ int cnt[APEX_MAX_PAIRS / kThreads][4];
     const int e = blockIdx.y;
@@ -343,7 +513,7 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
     const int n_e = expert_pairs(exec_idx, P, e, list, cnt);
     if (n_e == 0) return;
     int b_lo, b_hi;
-    split_range(d, gridDim.z, blockIdx.z, b_lo, b_hi);
+    split_range(d, WF::template kb<MT>(), gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const typename WF::T *slot = slots + size_t(s) * slot_stride;
     const typename WF::T *W = slot + size_t(i0) * 2 * d / WF::kKPerElem;
@@ -363,9 +533,9 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[2][MT];
-        gemm_mainloop<2, MT, ActF32, WF>(wbase, size_t(2) * d / WF::kKPerElem, sbase,
-                                         size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, 0,
-                                         n_tiles, Ws, Xs, acc);
+        gemm_tile<2, MT, ActF32, WF>(wbase, size_t(2) * d / WF::kKPerElem, sbase,
+                                     size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, 0,
+                                     n_tiles, lds, acc);
         const int i = i0 + 16 * wave + (lane & 15);
         float s1 = 1.f, s3 = 1.f;
         if constexpr (WF::kFp8) {
@@ -402,8 +572,7 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
     const int32_t *__restrict__ slot_of_expert, int n_slots,
     const typename WF::T *__restrict__ slots, size_t slot_stride, const void *__restrict__ act,
     size_t act_elem_bytes, float *__restrict__ yp) {
-    __shared__ uint16_t Ws[1][kRows][kLdsRow];
-    __shared__ uint16_t Xs[16 * MT][kLdsRow];
+    __shared__ __align__(16) GemmLds<1, MT, WF> lds;
     __shared__ int list[APEX_MAX_PAIRS];
     __shared__ int cnt[APEX_MAX_PAIRS / kThreads][4];
     const int e = blockIdx.y;
@@ -413,7 +582,7 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
     const int n_e = expert_pairs(exec_idx, P, e, list, cnt);
     if (n_e == 0) return;
     int b_lo, b_hi;
-    split_range(I, gridDim.z, blockIdx.z, b_lo, b_hi);
+    split_range(I, WF::template kb<MT>(), gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const typename WF::T *slot = slots + size_t(s) * slot_stride;
     const typename WF::T *const wbase[1] = {
@@ -434,9 +603,9 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[1][MT];
-        gemm_mainloop<1, MT, Act, WF>(wbase, size_t(I) / WF::kKPerElem, sbase, size_t(I / 32),
-                                      d - j0, I, b_lo, b_hi, hrow, hok, size_t(P) * I, n_tiles,
-                                      Ws, Xs, acc);
+        gemm_tile<1, MT, Act, WF>(wbase, size_t(I) / WF::kKPerElem, sbase, size_t(I / 32),
+                                  d - j0, I, b_lo, b_hi, hrow, hok, size_t(P) * I, n_tiles, lds,
+                                  acc);
         const int j = j0 + 16 * wave + (lane & 15);
         float s2 = 1.f;
         if constexpr (WF::kFp8) s2 = j < d ? row_scales<WF>(slot, d, I)[2 * I + j] : 0.f;
@@ -494,12 +663,18 @@ struct Plan {
     size_t h_bytes, y_bytes;
 };
 
+// The launch plan for weight format WF (its K block sets how many blocks a split needs).
+// The bf16 plan has the most splits, so its workspace covers every format's.
+template <class WF>
 Plan plan_for(int B, int d, int I, int k, int E, int n_slots) {
     Plan pl;
     // token tiles per pass: enough for the whole batch on one expert up to 64 tokens
     pl.MT = B >= 48 ? 4 : (B >= 24 ? 2 : 1);
     const int experts = std::min(std::min(E, B * k), n_slots);
-    const int nb_d = (d + kKB - 1) / kKB, nb_i = (I + kKB - 1) / kKB;
+    const int kb = pl.MT == 4   ? WF::template kb<4>()
+                   : pl.MT == 2 ? WF::template kb<2>()
+                                : WF::template kb<1>();
+    const int nb_d = (d + kb - 1) / kb, nb_i = (I + kb - 1) / kb;
     pl.SU = pl.MT == 1 ? pick_splits((I + kRows - 1) / kRows, experts, nb_d) : 1;
     pl.SD = pick_splits((d + kRows - 1) / kRows, experts, nb_i);
     const size_t P = size_t(B) * k;
@@ -526,10 +701,11 @@ void launch_down(dim3 g, hipStream_t st, int d, int I, int P, const int32_t *exe
 
 // The launches of one call for slots of weight format WF.
 template <class WF>
-apex_status run_grouped(const Plan &pl, const float *x, int B, int d, int I, int E, int k,
+apex_status run_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *exec_idx, const float *exec_gate,
                         const int32_t *soe, const typename WF::T *slots, size_t stride,
                         int n_slots, float *y, int accumulate, char *wsb, hipStream_t stream) {
+    const Plan pl = plan_for<WF>(B, d, I, k, E, n_slots);
     const int P = B * k;
     __bf16 *hb = reinterpret_cast<__bf16 *>(wsb);
     float *uv = reinterpret_cast<float *>(wsb);
@@ -580,7 +756,7 @@ size_t ffn_grouped_workspace(int B, int d, int I, int k) {
     // the largest plan over the slot counts the call can be given
     size_t worst = 0;
     for (int experts = 1; experts <= APEX_MAX_EXPERTS; ++experts) {
-        const Plan pl = plan_for(B, d, I, k, APEX_MAX_EXPERTS, experts);
+        const Plan pl = plan_for<WBf16>(B, d, I, k, APEX_MAX_EXPERTS, experts);
         worst = std::max(worst, align_up(pl.h_bytes, 256) + align_up(pl.y_bytes, 256));
     }
     return worst;
@@ -591,19 +767,18 @@ apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *slot_of_expert, const void *slots, int n_slots,
                         WeightFormat fmt, float *y, int accumulate, void *workspace,
                         hipStream_t stream) {
-    const Plan pl = plan_for(B, d, I, k, E, n_slots);
     char *wsb = static_cast<char *>(workspace);
     if (fmt == WeightFormat::kE4M3)
-        return run_grouped<WE4M3>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+        return run_grouped<WE4M3>(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
                                   static_cast<const uint8_t *>(slots),
                                   apex_expert_bytes_fp8(d, I), n_slots, y, accumulate, wsb,
                                   stream);
     if (fmt == WeightFormat::kMxfp4)
-        return run_grouped<WMxfp4>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+        return run_grouped<WMxfp4>(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
                                    static_cast<const uint8_t *>(slots),
                                    apex_expert_bytes_mxfp4(d, I), n_slots, y, accumulate, wsb,
                                    stream);
-    return run_grouped<WBf16>(pl, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+    return run_grouped<WBf16>(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
                               static_cast<const uint16_t *>(slots), size_t(3) * d * I, n_slots,
                               y, accumulate, wsb, stream);
 }
