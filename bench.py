@@ -129,6 +129,36 @@ def ffn_roofline_leg(torch, native, runner, reps=8, seed=123):
     return ms, nbytes, n
 
 
+def stream_floor_leg(torch, native, cs, nbytes, n=192, buf_bytes=1 << 30):
+    """Device time of a plain read of the FFN call's weight bytes, split into two
+    launches as the FFN splits them (W1/W3 rows, then W2 rows): the fastest any kernel
+    can bring those bytes in at that size on this GPU.  Each launch reads fresh memory
+    (a 1 GB buffer, far larger than the 256 MB Infinity Cache).  Returns mean us per
+    call."""
+    parts = [int(nbytes * 2 / 3) // 256 * 256, int(nbytes / 3) // 256 * 256]
+    buf = torch.empty(buf_bytes, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(native.apex_read_kernel_sink_words(max(parts)), dtype=torch.int32,
+                       device="cuda")
+    base, off = buf.data_ptr(), 0
+    e0, e1 = native.apex_event_create(True), native.apex_event_create(True)
+    torch.cuda.synchronize()
+    native.apex_spin_us(min(5000.0 + 30.0 * n, 1e6), cs)
+    native.apex_event_record(e0, cs)
+    for _ in range(n):
+        for part in parts:
+            if off + part > buf_bytes:
+                off = 0
+            native.apex_read_kernel(base + off, part, sink, cs)
+            off += part
+    native.apex_event_record(e1, cs)
+    native.apex_event_synchronize(e1)
+    us = native.apex_event_elapsed_ms(e0, e1) * 1e3 / n
+    native.apex_event_destroy(e0)
+    native.apex_event_destroy(e1)
+    del buf, sink
+    return us
+
+
 def attention_leg(torch, native, runner, reps=8):
     """Device time of one layer's decode attention (apex_attention_decode) in the decode
     launch configuration: calls cycling over the layers, queued behind a spin kernel,
@@ -300,6 +330,7 @@ def main():
     h2d_peak = pinned_h2d_peak(torch)
     ms_per_step = time_steps(torch, runner, args.steps, args.warmup)
     leg_ms, leg_bytes, leg_n = ffn_roofline_leg(torch, native, runner)
+    floor_us = stream_floor_leg(torch, native, runner.cs, leg_bytes)
     calib = copy_calibration(torch, native, runner.cs)
 
     L, B = len(runner.layers), args.batch
@@ -361,7 +392,10 @@ def main():
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic(cfg, B, args.weights),
-                     "bytes_per_launch": leg_bytes, "launches": leg_n},
+                     "bytes_per_launch": leg_bytes, "launches": leg_n,
+                     # the same bytes read by a plain two-launch read stream
+                     "read_stream_us": round(floor_us, 3),
+                     "frac_of_read_stream": round(floor_us / (leg_ms * 1e3), 4)},
     }
     if args.policy == "static":
         out["config"]["static_delta"] = args.static_delta

@@ -465,6 +465,14 @@ apex_status apex_stream_synchronize(hipStream_t stream);
  * vector-load/store kernel; used to calibrate memory counters and bandwidth. */
 apex_status apex_copy_kernel(void *dst, const void *src, size_t bytes, hipStream_t stream);
 
+/* Read `bytes` (multiple of 16) of device memory with a streaming vector-load kernel
+ * (four 16-byte loads in flight per thread, 256 threads per workgroup, up to 1024
+ * workgroups) that writes only one word per workgroup to `sink`: the read-only rate any
+ * kernel can reach at that size, the floor against which the expert FFN is measured.
+ * sink: device uint32 [apex_read_kernel_sink_words(bytes)]. */
+size_t apex_read_kernel_sink_words(size_t bytes);
+apex_status apex_read_kernel(const void *src, size_t bytes, uint32_t *sink, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

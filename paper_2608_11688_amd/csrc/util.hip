@@ -1,4 +1,5 @@
-// Attention-window stand-in, a calibration copy kernel, and event/stream helpers.
+// Attention-window stand-in, calibration copy and read-stream kernels, and event/stream
+// helpers.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -20,6 +21,30 @@ __global__ __launch_bounds__(256) void copy_kernel(uint4 *__restrict__ dst,
     const size_t stride = size_t(gridDim.x) * blockDim.x;
     for (size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride)
         dst[i] = src[i];
+}
+
+// Reads n 16-byte chunks with four loads in flight per thread and folds them into one
+// word per workgroup (so the loads cannot be dropped); the fold is the only write.
+__global__ __launch_bounds__(256) void read_kernel(const uint4 *__restrict__ src, size_t n,
+                                                   uint32_t *__restrict__ sink) {
+    const size_t stride = size_t(gridDim.x) * blockDim.x;
+    uint32_t acc = 0;
+    size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride],
+                    d = src[i + 3 * stride];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^
+               d.z ^ d.w;
+    }
+    for (; i < n; i += stride) {
+        const uint4 a = src[i];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o, 64);
+    __shared__ uint32_t part[4];
+    if (threadIdx.x % 64 == 0) part[threadIdx.x / 64] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
 }
 
 }  // namespace
@@ -48,6 +73,24 @@ extern "C" apex_status apex_copy_kernel(void *dst, const void *src, size_t bytes
     if (blocks > 8192) blocks = 8192;
     hipLaunchKernelGGL(copy_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream,
                        static_cast<uint4 *>(dst), static_cast<const uint4 *>(src), n);
+    APEX_HIP(hipGetLastError());
+    return APEX_OK;
+}
+
+extern "C" size_t apex_read_kernel_sink_words(size_t bytes) {
+    const size_t n = bytes / 16;
+    size_t blocks = (n + 1023) / 1024;
+    return blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
+}
+
+extern "C" apex_status apex_read_kernel(const void *src, size_t bytes, uint32_t *sink,
+                                        hipStream_t stream) {
+    APEX_REQUIRE(bytes % 16 == 0, "apex_read_kernel: bytes=%zu not a multiple of 16", bytes);
+    if (bytes == 0) return APEX_OK;
+    APEX_REQUIRE(src && sink && apex::aligned16(src), "apex_read_kernel: NULL or misaligned pointer");
+    const size_t blocks = apex_read_kernel_sink_words(bytes);
+    hipLaunchKernelGGL(read_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream,
+                       static_cast<const uint4 *>(src), bytes / 16, sink);
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }

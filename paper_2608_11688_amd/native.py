@@ -108,6 +108,8 @@ SIGNATURES = {
     "apex_stream_wait_event": (I32, [P, P]),
     "apex_stream_synchronize": (I32, [P]),
     "apex_copy_kernel": (I32, [P, P, SZ, P]),
+    "apex_read_kernel_sink_words": (SZ, [SZ]),
+    "apex_read_kernel": (I32, [P, SZ, P, P]),
 }
 
 HOST_ONLY = ("apex_abi_version", "apex_last_error", "apex_expert_bytes", "apex_pack_expert",
@@ -361,3 +363,11 @@ def apex_stream_synchronize(stream=None):
 
 def apex_copy_kernel(dst, src, nbytes, stream=None):
     _call("apex_copy_kernel", ptr(dst), ptr(src), nbytes, stream)
+
+
+def apex_read_kernel_sink_words(nbytes):
+    return lib().apex_read_kernel_sink_words(nbytes)
+
+
+def apex_read_kernel(src, nbytes, sink, stream=None):
+    _call("apex_read_kernel", ptr(src), nbytes, ptr(sink), stream)

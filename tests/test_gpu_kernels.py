@@ -554,3 +554,19 @@ def test_spin_and_copy_kernel(torch):
     assert torch.equal(src, dst)
     native.apex_event_destroy(a)
     native.apex_event_destroy(b)
+
+
+def test_read_kernel_reads_every_chunk(torch):
+    # the fold of all words equals the XOR of the buffer: every 16-byte chunk was read
+    s = torch.cuda.current_stream().cuda_stream
+    for n_words in (4, 4 * 1000 + 4, 1 << 22):           # tails shorter than one stride
+        src = torch.randint(-2 ** 31, 2 ** 31 - 1, (n_words,), dtype=torch.int32, device="cuda")
+        words = native.apex_read_kernel_sink_words(n_words * 4)
+        sink = torch.full((words,), 0, dtype=torch.int32, device="cuda")
+        native.apex_read_kernel(src, n_words * 4, sink, s)
+        torch.cuda.synchronize()
+        want = np.bitwise_xor.reduce(src.cpu().numpy().view(np.uint32))
+        got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+        assert got == want, n_words
+    with pytest.raises(native.ApexError):
+        native.apex_read_kernel(src, 12, sink, s)
