@@ -9,16 +9,17 @@
 // order.  When a projection has too few row tiles to keep the chip's loads in flight, its
 // K range is split over blockIdx.z and each split writes fp32 partial sums:
 //   * up_gemm with one split writes h = bf16(silu(W1 x) * (W3 x)) per pair; with several
-//     it writes the partial W1 x and W3 x, and down_gemm forms h from their sums while
-//     it stages its activations;
+//     it writes the partial W1 x and W3 x, and swiglu_reduce adds them (in split order)
+//     into the same bf16 h, once, before down_gemm reads it from every row tile;
 //   * down_gemm writes per-split, per-pair outputs; combine_pairs adds the splits and the
 //     gated positions of each token in a fixed order.
 // Slots hold bf16 weights (apex_pack_expert), E4M3 codes with fp32 row scales
 // (apex_pack_expert_fp8) or MXFP4 codes with a power-of-two scale per block of 32
-// (apex_pack_expert_mxfp4).  E4M3 and MXFP4 tiles are widened to bf16 exactly as they go
-// to LDS (MXFP4 with its block scales applied); the E4M3 row scales multiply the outputs.  Every executed expert's weights are read once
-// per call whatever the number of tokens routed to it, and no atomics are used, so
-// results are deterministic.
+// (apex_pack_expert_mxfp4).  E4M3 and MXFP4 codes are staged in LDS as bytes and widened
+// to bf16 exactly at fragment read (MXFP4 with its block scales applied); the E4M3 row
+// scales multiply the outputs.  Every executed expert's weights are read once per call
+// whatever the number of tokens routed to it, and no atomics are used, so results are
+// deterministic.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -65,33 +66,32 @@ struct ActF32 {          // fp32 rows (the FFN input x), rounded here
         return pack_bf16(a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w);
     }
 };
-struct ActBf16 {         // bf16 rows (h written by a one-split up_gemm)
+struct ActBf16 {         // bf16 rows (h)
     static __device__ __forceinline__ uint4 load(const void *row, int kc, size_t) {
         return *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(row) + kc);
     }
 };
+// h = bf16(silu(u) * v) of 8 consecutive values from SU split partials: u of split s at
+// r + 2s*stride, v at r + (2s+1)*stride, the splits added in order.
 template <int SU>
-struct ActSwiglu {       // h from SU split partials: u of split s at row + 2s*stride, v at +1
-    static __device__ __forceinline__ uint4 load(const void *row, int kc, size_t stride) {
-        const float *r = static_cast<const float *>(row) + kc;
-        float u[8], v[8];
+__device__ __forceinline__ uint4 swiglu8(const float *r, size_t stride) {
+    float u[8], v[8];
 #pragma unroll
-        for (int c = 0; c < 8; ++c) u[c] = v[c] = 0.f;
+    for (int c = 0; c < 8; ++c) u[c] = v[c] = 0.f;
 #pragma unroll
-        for (int s = 0; s < SU; ++s) {
-            const float4 *pu = reinterpret_cast<const float4 *>(r + 2 * s * stride);
-            const float4 *pv = reinterpret_cast<const float4 *>(r + (2 * s + 1) * stride);
-            const float4 u0 = pu[0], u1 = pu[1], v0 = pv[0], v1 = pv[1];
-            u[0] += u0.x; u[1] += u0.y; u[2] += u0.z; u[3] += u0.w;
-            u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
-            v[0] += v0.x; v[1] += v0.y; v[2] += v0.z; v[3] += v0.w;
-            v[4] += v1.x; v[5] += v1.y; v[6] += v1.z; v[7] += v1.w;
-        }
-        return pack_bf16(silu(u[0]) * v[0], silu(u[1]) * v[1], silu(u[2]) * v[2],
-                         silu(u[3]) * v[3], silu(u[4]) * v[4], silu(u[5]) * v[5],
-                         silu(u[6]) * v[6], silu(u[7]) * v[7]);
+    for (int s = 0; s < SU; ++s) {
+        const float4 *pu = reinterpret_cast<const float4 *>(r + 2 * s * stride);
+        const float4 *pv = reinterpret_cast<const float4 *>(r + (2 * s + 1) * stride);
+        const float4 u0 = pu[0], u1 = pu[1], v0 = pv[0], v1 = pv[1];
+        u[0] += u0.x; u[1] += u0.y; u[2] += u0.z; u[3] += u0.w;
+        u[4] += u1.x; u[5] += u1.y; u[6] += u1.z; u[7] += u1.w;
+        v[0] += v0.x; v[1] += v0.y; v[2] += v0.z; v[3] += v0.w;
+        v[4] += v1.x; v[5] += v1.y; v[6] += v1.z; v[7] += v1.w;
     }
-};
+    return pack_bf16(silu(u[0]) * v[0], silu(u[1]) * v[1], silu(u[2]) * v[2],
+                     silu(u[3]) * v[3], silu(u[4]) * v[4], silu(u[5]) * v[5],
+                     silu(u[6]) * v[6], silu(u[7]) * v[7]);
+}
 
 // Weight formats of a slot.  One 16-byte load per thread covers kPerLoad consecutive K
 // values of one row; kThrPerRow threads cover a 128-wide K block of the row and
@@ -565,13 +565,13 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
 
 // down_gemm: grid (ceil(d / 64), E, SD).  64 rows j of W2 of expert blockIdx.y, K (= I)
 // blocks of split blockIdx.z.  yp[z * P*d + pair*d + j] = W2[j] . h[pair] over the split.
-// The activations come from Act: bf16 h rows, or h formed from up_gemm's split partials.
-template <int MT, class Act, class WF>
+// The activations are the bf16 h rows.
+template <int MT, class WF>
 __global__ __launch_bounds__(kThreads) void down_gemm(
     int d, int I, int P, const int32_t *__restrict__ exec_idx,
     const int32_t *__restrict__ slot_of_expert, int n_slots,
-    const typename WF::T *__restrict__ slots, size_t slot_stride, const void *__restrict__ act,
-    size_t act_elem_bytes, float *__restrict__ yp) {
+    const typename WF::T *__restrict__ slots, size_t slot_stride, const __bf16 *__restrict__ hb,
+    float *__restrict__ yp) {
     __shared__ __align__(16) GemmLds<1, MT, WF> lds;
     __shared__ int list[APEX_MAX_PAIRS];
     __shared__ int cnt[APEX_MAX_PAIRS / kThreads][4];
@@ -590,7 +590,6 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
     const uint8_t *const sbase[1] = {reinterpret_cast<const uint8_t *>(slot) +
                                      size_t(3) * I * d / 2 + size_t(2) * I * (d / 32) +
                                      size_t(j0) * (I / 32)};
-    const char *ab = static_cast<const char *>(act);
     float *out = yp + size_t(blockIdx.z) * P * d;
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
         const void *hrow[MT];
@@ -599,13 +598,13 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
         for (int j = 0; j < MT; ++j) {
             const int tok = t0 + (threadIdx.x >> 4) + 16 * j;
             hok[j] = tok < n_e;
-            hrow[j] = ab + size_t(list[hok[j] ? tok : 0]) * I * act_elem_bytes;
+            hrow[j] = hb + size_t(list[hok[j] ? tok : 0]) * I;
         }
         const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[1][MT];
-        gemm_tile<1, MT, Act, WF>(wbase, size_t(I) / WF::kKPerElem, sbase, size_t(I / 32),
-                                  d - j0, I, b_lo, b_hi, hrow, hok, size_t(P) * I, n_tiles, lds,
-                                  acc);
+        gemm_tile<1, MT, ActBf16, WF>(wbase, size_t(I) / WF::kKPerElem, sbase,
+                                      size_t(I / 32), d - j0, I, b_lo, b_hi, hrow, hok, 0,
+                                      n_tiles, lds, acc);
         const int j = j0 + 16 * wave + (lane & 15);
         float s2 = 1.f;
         if constexpr (WF::kFp8) s2 = j < d ? row_scales<WF>(slot, d, I)[2 * I + j] : 0.f;
@@ -619,6 +618,26 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
             }
         __syncthreads();   // LDS is reused by the next pass
     }
+}
+
+// swiglu_reduce: h[pair, i] = bf16(silu(sum_z u_z) * sum_z v_z) from up_gemm's SU split
+// partials (splits added in order), for the pairs whose expert has a slot; 8 consecutive
+// i per thread.
+template <int SU>
+__global__ __launch_bounds__(kThreads) void swiglu_reduce(
+    int P, int I, int E, const int32_t *__restrict__ exec_idx,
+    const int32_t *__restrict__ slot_of_expert, int n_slots, const float *__restrict__ uv,
+    __bf16 *__restrict__ hb) {
+    const int per = I / 8;
+    const int g = blockIdx.x * kThreads + threadIdx.x;
+    if (g >= P * per) return;
+    const int p = g / per, i = 8 * (g - p * per);
+    const int e = exec_idx[p];
+    if (e < 0 || e >= E) return;
+    const int sl = slot_of_expert[e];
+    if (sl < 0 || sl >= n_slots) return;
+    const size_t at = size_t(p) * I + i;
+    *reinterpret_cast<uint4 *>(hb + at) = swiglu8<SU>(uv + at, size_t(P) * I);
 }
 
 // combine: y[b, j] (+)= sum over positions q of token b, in position order, of
@@ -660,7 +679,7 @@ int pick_splits(int tiles, int experts, int nb) {
 
 struct Plan {
     int MT, SU, SD;
-    size_t h_bytes, y_bytes;
+    size_t uv_bytes, h_bytes, y_bytes;   // h_bytes: the split partials (if any) and h
 };
 
 // The launch plan for weight format WF (its K block sets how many blocks a split needs).
@@ -678,7 +697,9 @@ Plan plan_for(int B, int d, int I, int k, int E, int n_slots) {
     pl.SU = pl.MT == 1 ? pick_splits((I + kRows - 1) / kRows, experts, nb_d) : 1;
     pl.SD = pick_splits((d + kRows - 1) / kRows, experts, nb_i);
     const size_t P = size_t(B) * k;
-    pl.h_bytes = pl.SU == 1 ? P * I * 2 : size_t(2) * pl.SU * P * I * sizeof(float);
+    pl.uv_bytes =
+        pl.SU == 1 ? 0 : apex::align_up(size_t(2) * pl.SU * P * I * sizeof(float), 256);
+    pl.h_bytes = pl.uv_bytes + P * I * 2;
     pl.y_bytes = size_t(pl.SD) * P * d * sizeof(float);
     return pl;
 }
@@ -691,12 +712,12 @@ void launch_up(dim3 g, hipStream_t st, const float *x, int d, int I, int P, int 
                        soe, n_slots, slots, stride, hb, uv);
 }
 
-template <int MT, class Act, class WF>
+template <int MT, class WF>
 void launch_down(dim3 g, hipStream_t st, int d, int I, int P, const int32_t *exec_idx,
                  const int32_t *soe, int n_slots, const typename WF::T *slots, size_t stride,
-                 const void *act, size_t act_bytes, float *yp) {
-    hipLaunchKernelGGL((down_gemm<MT, Act, WF>), g, dim3(kThreads), 0, st, d, I, P, exec_idx, soe,
-                       n_slots, slots, stride, act, act_bytes, yp);
+                 const __bf16 *hb, float *yp) {
+    hipLaunchKernelGGL((down_gemm<MT, WF>), g, dim3(kThreads), 0, st, d, I, P, exec_idx, soe,
+                       n_slots, slots, stride, hb, yp);
 }
 
 // The launches of one call for slots of weight format WF.
@@ -707,8 +728,8 @@ apex_status run_grouped(const float *x, int B, int d, int I, int E, int k,
                         int n_slots, float *y, int accumulate, char *wsb, hipStream_t stream) {
     const Plan pl = plan_for<WF>(B, d, I, k, E, n_slots);
     const int P = B * k;
-    __bf16 *hb = reinterpret_cast<__bf16 *>(wsb);
     float *uv = reinterpret_cast<float *>(wsb);
+    __bf16 *hb = reinterpret_cast<__bf16 *>(wsb + pl.uv_bytes);
     float *yp = reinterpret_cast<float *>(wsb + apex::align_up(pl.h_bytes, 256));
     const dim3 gu((I + kRows - 1) / kRows, E, pl.SU);
     if (pl.MT == 4)
@@ -724,21 +745,27 @@ apex_status run_grouped(const float *x, int B, int d, int I, int E, int k,
     else
         launch_up<1, 4, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
     APEX_HIP(hipGetLastError());
+    if (pl.SU > 1) {
+        const dim3 gr((P * (I / 8) + kThreads - 1) / kThreads);
+        if (pl.SU == 2)
+            hipLaunchKernelGGL(swiglu_reduce<2>, gr, dim3(kThreads), 0, stream, P, I, E, exec_idx,
+                               soe, n_slots, uv, hb);
+        else if (pl.SU == 3)
+            hipLaunchKernelGGL(swiglu_reduce<3>, gr, dim3(kThreads), 0, stream, P, I, E, exec_idx,
+                               soe, n_slots, uv, hb);
+        else
+            hipLaunchKernelGGL(swiglu_reduce<4>, gr, dim3(kThreads), 0, stream, P, I, E, exec_idx,
+                               soe, n_slots, uv, hb);
+        APEX_HIP(hipGetLastError());
+    }
 
     const dim3 gd((d + kRows - 1) / kRows, E, pl.SD);
-    const void *act = pl.SU == 1 ? static_cast<const void *>(hb) : static_cast<const void *>(uv);
     if (pl.MT == 4)
-        launch_down<4, ActBf16, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 2, yp);
+        launch_down<4, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, hb, yp);
     else if (pl.MT == 2)
-        launch_down<2, ActBf16, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 2, yp);
-    else if (pl.SU == 1)
-        launch_down<1, ActBf16, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 2, yp);
-    else if (pl.SU == 2)
-        launch_down<1, ActSwiglu<2>, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 4, yp);
-    else if (pl.SU == 3)
-        launch_down<1, ActSwiglu<3>, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 4, yp);
+        launch_down<2, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, hb, yp);
     else
-        launch_down<1, ActSwiglu<4>, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, act, 4, yp);
+        launch_down<1, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, hb, yp);
     APEX_HIP(hipGetLastError());
     hipLaunchKernelGGL(combine_pairs, dim3((d + kThreads - 1) / kThreads, B), dim3(kThreads), 0,
                        stream, B, d, E, k, pl.SD, exec_idx, exec_gate, soe, n_slots, yp, y,
@@ -751,7 +778,8 @@ apex_status run_grouped(const float *x, int B, int d, int I, int E, int k,
 
 namespace apex {
 
-// [h: bf16 B*k x I, or 2*SU fp32 partials][per-split, per-pair outputs: SD x B*k x d fp32]
+// [2*SU fp32 split partials, when SU > 1][h: bf16 B*k x I][per-split, per-pair outputs:
+//  SD x B*k x d fp32]
 size_t ffn_grouped_workspace(int B, int d, int I, int k) {
     // the largest plan over the slot counts the call can be given
     size_t worst = 0;
