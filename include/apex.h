@@ -41,7 +41,7 @@
 extern "C" {
 #endif
 
-#define APEX_ABI_VERSION 3
+#define APEX_ABI_VERSION 4
 #define APEX_MAX_EXPERTS 64
 #define APEX_MAX_PAIRS 1024     /* B * k limit of apex_moe_ffn */
 
@@ -242,6 +242,19 @@ apex_status apex_moe_ffn_mxfp4(const float *x, int B, int d, int I, int E, int k
                                const int32_t *slot_of_expert, const void *slots, int n_slots,
                                float *y, int accumulate, void *workspace,
                                size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * The launch plan apex_moe_ffn (weights = APEX_WEIGHTS_BF16), apex_moe_ffn_fp8 and
+ * apex_moe_ffn_mxfp4 take for B >= 2 tokens with E experts of which n_slots have a slot
+ * (host only; no GPU work): plan[0] = 16-token tiles per pass (1, 2 or 4), plan[1] = K
+ * splits of the gate/up projection, plan[2] = K splits of the down projection (1 to 4
+ * each; splits of one projection are added in a fixed order, so the result depends on
+ * the plan but not on timing).  B < 2 (the batch-1 kernels) gives {0, 0, 0}.
+ *   plan   host int32 [3] out
+ * Errors: APEX_E_INVAL for a NULL plan, an unknown weights value or sizes out of range.
+ */
+apex_status apex_moe_ffn_plan(int B, int d, int I, int E, int k, int n_slots, int weights,
+                              int32_t *plan);
 
 /*
  * Decode attention of one layer: the block that runs between the prefetch router and

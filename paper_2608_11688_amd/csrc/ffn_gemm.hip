@@ -96,6 +96,7 @@ __device__ __forceinline__ uint4 swiglu8(const float *r, size_t stride) {
 // Weight formats of a slot.  One 16-byte load per thread covers kPerLoad consecutive K
 // values of one row; kThrPerRow threads cover a 128-wide K block of the row and
 // kRowsPerPass rows are loaded per pass of the workgroup.
+// kUpGroups: workgroups the gate/up projection's K splits aim at (see plan_for);
 // kKPerElem: K values per element of T; kFp8: fp32 row scales after the codes;
 // kBlockScale: one scale byte per 32 K values of a row (kPerLoad is then one block);
 // kCodes: the codes go to LDS as bytes, in K blocks of kb<MT>() values, and are widened
@@ -104,6 +105,7 @@ struct WBf16 {           // apex_pack_expert slots: bf16 weights
     using T = uint16_t;
     static constexpr bool kFp8 = false, kBlockScale = false, kCodes = false;
     template <int MT> static constexpr int kb() { return kKB; }
+    static constexpr int kUpGroups = 400;
     static constexpr int kKPerElem = 1;
     static constexpr int kPerLoad = 8, kThrPerRow = kKB / 8, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
@@ -113,6 +115,7 @@ struct WE4M3 {           // apex_pack_expert_fp8 slots: E4M3 codes, fp32 row sca
     static constexpr bool kFp8 = true, kBlockScale = false, kCodes = true;
     // 256 bytes per row with one token tile, 128 with more (a smaller activation tile)
     template <int MT> static constexpr int kb() { return MT == 1 ? 256 : 128; }
+    static constexpr int kUpGroups = 800;
     static constexpr int kKPerElem = 1;
     static constexpr int kPerLoad = 16, kThrPerRow = kKB / 16, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
@@ -122,6 +125,7 @@ struct WMxfp4 {          // apex_pack_expert_mxfp4 slots: two E2M1 codes per byt
     static constexpr bool kFp8 = false, kBlockScale = true, kCodes = true;
     // 256 bytes per row with one token tile, 128 with more (a smaller activation tile)
     template <int MT> static constexpr int kb() { return MT == 1 ? 512 : 256; }
+    static constexpr int kUpGroups = 1400;
     static constexpr int kKPerElem = 2;
     static constexpr int kPerLoad = 32, kThrPerRow = kKB / 32, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
@@ -238,7 +242,10 @@ __device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][WF::kLoads],
 // that each group of 16 threads reads 256 contiguous bytes of one weight row (whole
 // cache lines), the block goes to LDS, and while the matrix cores work on it the next
 // block is already loading into registers.  Wavefront w multiplies its 16 rows with
-// every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.
+// every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.  Tiles past
+// the expert's last token multiply zero rows: skipping them on the token count made the
+// compiler move the accumulators between register files around the skip, and the E4M3
+// kernel with two tiles then gave wrong sums that changed from run to run.
 template <int NW, int MT, class Act, class WF>
 __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbase)[NW],
                                               size_t wstride, const uint8_t *const (&sbase)[NW],
@@ -246,7 +253,7 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
                                               int rows_valid, int K, int b_lo, int b_hi,
                                               const void *const (&xrow)[MT],
                                               const bool (&xok)[MT], size_t xstride,
-                                              int n_tiles, uint16_t (*Ws)[kRows][kLdsRow],
+                                              uint16_t (*Ws)[kRows][kLdsRow],
                                               uint16_t (*Xs)[kLdsRow], floatx4 (&acc)[NW][MT]) {
     const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
     const int seg = t & 15, r0 = t >> 4;
@@ -304,7 +311,6 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
                 wop[m] = *reinterpret_cast<const uint4 *>(&Ws[m][16 * wave + (lane & 15)][kc]);
 #pragma unroll
             for (int tt = 0; tt < MT; ++tt) {
-                if (tt >= n_tiles) continue;
                 const uint4 xop = *reinterpret_cast<const uint4 *>(&Xs[16 * tt + (lane & 15)][kc]);
 #pragma unroll
                 for (int m = 0; m < NW; ++m)
@@ -376,7 +382,7 @@ template <int NW, int MT, class Act, class WF>
 __device__ __forceinline__ void gemm_mainloop_codes(
     const uint8_t *const (&wbase)[NW], size_t wstride, const uint8_t *const (&sbase)[NW],
     size_t sstride, int rows_valid, int K, int b_lo, int b_hi, const void *const (&xrow)[MT],
-    const bool (&xok)[MT], size_t xstride, int n_tiles, GemmLds<NW, MT, WF, true> &lds,
+    const bool (&xok)[MT], size_t xstride, GemmLds<NW, MT, WF, true> &lds,
     floatx4 (&acc)[NW][MT]) {
     using L = GemmLds<NW, MT, WF, true>;
     constexpr int KB = L::KB, RB = L::RB;
@@ -458,7 +464,6 @@ __device__ __forceinline__ void gemm_mainloop_codes(
             for (int m = 0; m < NW; ++m) wop[m] = widen8(lds, m, rr, kc);
 #pragma unroll
             for (int tt = 0; tt < MT; ++tt) {
-                if (tt >= n_tiles) continue;
                 const uint4 xop = *reinterpret_cast<const uint4 *>(&lds.Xs[16 * tt + (lane & 15)][kc]);
 #pragma unroll
                 for (int m = 0; m < NW; ++m)
@@ -475,14 +480,14 @@ __device__ __forceinline__ void gemm_tile(const typename WF::T *const (&wbase)[N
                                           size_t wstride, const uint8_t *const (&sbase)[NW],
                                           size_t sstride, int rows_valid, int K, int b_lo,
                                           int b_hi, const void *const (&xrow)[MT],
-                                          const bool (&xok)[MT], size_t xstride, int n_tiles,
+                                          const bool (&xok)[MT], size_t xstride,
                                           GemmLds<NW, MT, WF> &lds, floatx4 (&acc)[NW][MT]) {
     if constexpr (WF::kCodes)
         gemm_mainloop_codes<NW, MT, Act, WF>(wbase, wstride, sbase, sstride, rows_valid, K,
-                                             b_lo, b_hi, xrow, xok, xstride, n_tiles, lds, acc);
+                                             b_lo, b_hi, xrow, xok, xstride, lds, acc);
     else
         gemm_mainloop<NW, MT, Act, WF>(wbase, wstride, sbase, sstride, rows_valid, K, b_lo,
-                                       b_hi, xrow, xok, xstride, n_tiles, lds.Ws, lds.Xs, acc);
+                                       b_hi, xrow, xok, xstride, lds.Ws, lds.Xs, acc);
 }
 
 // The fp32 row scales of an apex_pack_expert_fp8 slot: W1 rows, W3 rows, W2 rows.
@@ -531,11 +536,10 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
             xok[j] = tok < n_e;
             xrow[j] = x + size_t(list[xok[j] ? tok : 0] / k) * d;
         }
-        const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[2][MT];
         gemm_tile<2, MT, ActF32, WF>(wbase, size_t(2) * d / WF::kKPerElem, sbase,
-                                     size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, 0,
-                                     n_tiles, lds, acc);
+                                     size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, 0, lds,
+                                     acc);
         const int i = i0 + 16 * wave + (lane & 15);
         float s1 = 1.f, s3 = 1.f;
         if constexpr (WF::kFp8) {
@@ -548,7 +552,7 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
-                if (tt < n_tiles && tok < n_e && i < I) {
+                if (tok < n_e && i < I) {
                     const size_t at = size_t(list[tok]) * I + i;
                     const float u = s1 * acc[0][tt][r], v = s3 * acc[1][tt][r];
                     if (SU == 1) {
@@ -600,11 +604,10 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
             hok[j] = tok < n_e;
             hrow[j] = hb + size_t(list[hok[j] ? tok : 0]) * I;
         }
-        const int n_tiles = min(MT, (n_e - t0 + 15) / 16);
         floatx4 acc[1][MT];
         gemm_tile<1, MT, ActBf16, WF>(wbase, size_t(I) / WF::kKPerElem, sbase,
-                                      size_t(I / 32), d - j0, I, b_lo, b_hi, hrow, hok, 0,
-                                      n_tiles, lds, acc);
+                                      size_t(I / 32), d - j0, I, b_lo, b_hi, hrow, hok, 0, lds,
+                                      acc);
         const int j = j0 + 16 * wave + (lane & 15);
         float s2 = 1.f;
         if constexpr (WF::kFp8) s2 = j < d ? row_scales<WF>(slot, d, I)[2 * I + j] : 0.f;
@@ -613,7 +616,7 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int tok = t0 + 16 * tt + 4 * (lane >> 4) + r;
-                if (tt < n_tiles && tok < n_e && j < d)
+                if (tok < n_e && j < d)
                     out[size_t(list[tok]) * d + j] = s2 * acc[0][tt][r];
             }
         __syncthreads();   // LDS is reused by the next pass
@@ -642,38 +645,73 @@ __global__ __launch_bounds__(kThreads) void swiglu_reduce(
 
 // combine: y[b, j] (+)= sum over positions q of token b, in position order, of
 // gate[q] * (sum over splits z, in order, of yp[z, pair, j]) for the pairs this pass
-// executed.
+// executed.  Four consecutive j per thread.  Lane q of every wavefront looks up position
+// q (its expert, slot and gate; k <= 64 since k <= E), so all positions cost one chain of
+// dependent loads, and the wavefront reads them back with readlane.  The partial outputs
+// of a group of positions are loaded before any is added (those of positions that were
+// not executed are read and dropped).
+template <int SD>
 __global__ __launch_bounds__(kThreads) void combine_pairs(
-    int B, int d, int E, int k, int SD, const int32_t *__restrict__ exec_idx,
+    int B, int d, int E, int k, const int32_t *__restrict__ exec_idx,
     const float *__restrict__ exec_gate, const int32_t *__restrict__ slot_of_expert, int n_slots,
     const float *__restrict__ yp, float *__restrict__ y, int accumulate) {
+    constexpr int kGroup = SD <= 2 ? 8 : 4;
     const int b = blockIdx.y;
-    const int j = blockIdx.x * kThreads + threadIdx.x;
-    if (b >= B || j >= d) return;
-    const size_t Pd = size_t(B) * k * d;
-    float s = 0.f;
-    for (int q = 0; q < k; ++q) {
-        const int p = b * k + q;
+    const int j = 4 * (blockIdx.x * kThreads + threadIdx.x);
+    const int lane = threadIdx.x % kWave;
+    int pos_ok = 0;
+    float pos_gate = 0.f;
+    if (lane < k) {
+        const int p = b * k + lane;
         const int e = exec_idx[p];
-        if (e < 0 || e >= E) continue;
-        const int sl = slot_of_expert[e];
-        if (sl < 0 || sl >= n_slots) continue;
-        float v = 0.f;
-        for (int z = 0; z < SD; ++z) v += yp[z * Pd + size_t(p) * d + j];
-        s += exec_gate[p] * v;
+        const bool e_ok = e >= 0 && e < E;
+        const int sl = slot_of_expert[e_ok ? e : 0];
+        pos_ok = e_ok && sl >= 0 && sl < n_slots;
+        pos_gate = exec_gate[p];
     }
-    float *dst = y + size_t(b) * d + j;
-    *dst = (accumulate ? *dst : 0.f) + s;
+    if (j >= d) return;
+    const size_t Pd = size_t(B) * k * d;
+    const float *row = yp + size_t(b) * k * d + j;
+    float4 *dst = reinterpret_cast<float4 *>(y + size_t(b) * d + j);
+    const float4 o = *dst;   // read whether or not it is added, so no branch waits on it
+    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    const auto group = [&](int q0) {
+        float4 v[kGroup][SD];
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            const int q = min(q0 + u, k - 1);
+#pragma unroll
+            for (int z = 0; z < SD; ++z)
+                v[u][z] = *reinterpret_cast<const float4 *>(row + z * Pd + size_t(q) * d);
+        }
+#pragma unroll
+        for (int u = 0; u < kGroup; ++u) {
+            if (q0 + u >= k) break;
+            if (!__builtin_amdgcn_readlane(pos_ok, q0 + u)) continue;
+            const float g = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pos_gate), q0 + u));
+            float4 t = v[u][0];
+#pragma unroll
+            for (int z = 1; z < SD; ++z) {
+                t.x += v[u][z].x; t.y += v[u][z].y; t.z += v[u][z].z; t.w += v[u][z].w;
+            }
+            s.x += g * t.x; s.y += g * t.y; s.z += g * t.z; s.w += g * t.w;
+        }
+    };
+    group(0);   // outside the loop, so its loads issue together with the read of y
+    for (int q0 = kGroup; q0 < k; q0 += kGroup) group(q0);
+    if (accumulate) s = make_float4(o.x + s.x, o.y + s.y, o.z + s.z, o.w + s.w);
+    *dst = s;
 }
 
-// Splits for a projection with `tiles` row tiles per expert and K blocks `nb`: enough
-// workgroups for about four per compute unit over the experts that can run at once.
-int pick_splits(int tiles, int experts, int nb) {
-    constexpr int kTargetGroups = 1024;
-    const int groups = std::max(1, tiles * experts);
-    int s = (kTargetGroups + groups - 1) / groups;
+// K splits of a projection with `groups` workgroups of work (row tiles times experts)
+// and `nb` K blocks: `target` workgroups over all splits (rounded to the nearest split
+// count when `nearest`, else up), at most kMaxSplit, and at least `min_blocks` K blocks
+// per split.
+int pick_splits(int groups, int nb, int target, bool nearest, int min_blocks) {
+    groups = std::max(1, groups);
+    int s = nearest ? (target + groups / 2) / groups : (target + groups - 1) / groups;
     s = std::min(s, kMaxSplit);
-    s = std::min(s, std::max(1, nb / 2));   // at least two K blocks per split
+    s = std::min(s, std::max(1, nb / min_blocks));
     return std::max(s, 1);
 }
 
@@ -682,8 +720,16 @@ struct Plan {
     size_t uv_bytes, h_bytes, y_bytes;   // h_bytes: the split partials (if any) and h
 };
 
-// The launch plan for weight format WF (its K block sets how many blocks a split needs).
-// The bf16 plan has the most splits, so its workspace covers every format's.
+// The launch plan for weight format WF.  The split rules were fitted to timings of
+// every split pair (1-4 each) on grouped calls of the Granite-3B, OLMoE, Mixtral,
+// DeepSeek-16B and Phi-7B expert shapes in all three formats (24 to 64 resident
+// experts): each K split adds a prologue (finding the expert's pairs, the first load)
+// and partial sums, and pays only when the projection has too few workgroups to keep
+// HBM busy.  The gate/up target grows with the per-byte cost of widening the codes
+// (bf16 none, E4M3 most per byte); the down projection splits only over long K (for
+// Mixtral's I = 14336).  The rule is within 1 % of the best split pair on average over
+// those calls (the earlier rule, a common 1024-workgroup target with two K blocks per
+// split, was 7 % off, and up to 25 % on OLMoE B64 with E4M3 experts).
 template <class WF>
 Plan plan_for(int B, int d, int I, int k, int E, int n_slots) {
     Plan pl;
@@ -694,8 +740,8 @@ Plan plan_for(int B, int d, int I, int k, int E, int n_slots) {
                    : pl.MT == 2 ? WF::template kb<2>()
                                 : WF::template kb<1>();
     const int nb_d = (d + kb - 1) / kb, nb_i = (I + kb - 1) / kb;
-    pl.SU = pl.MT == 1 ? pick_splits((I + kRows - 1) / kRows, experts, nb_d) : 1;
-    pl.SD = pick_splits((d + kRows - 1) / kRows, experts, nb_i);
+    pl.SU = pick_splits((I + kRows - 1) / kRows * experts, nb_d, WF::kUpGroups, true, 3);
+    pl.SD = pick_splits((d + kRows - 1) / kRows * experts, nb_i, 1024, false, 8);
     const size_t P = size_t(B) * k;
     pl.uv_bytes =
         pl.SU == 1 ? 0 : apex::align_up(size_t(2) * pl.SU * P * I * sizeof(float), 256);
@@ -710,6 +756,20 @@ void launch_up(dim3 g, hipStream_t st, const float *x, int d, int I, int P, int 
                const typename WF::T *slots, size_t stride, __bf16 *hb, float *uv) {
     hipLaunchKernelGGL((up_gemm<MT, SU, WF>), g, dim3(kThreads), 0, st, x, d, I, P, k, exec_idx,
                        soe, n_slots, slots, stride, hb, uv);
+}
+
+template <int MT, class WF>
+void launch_up_splits(int SU, dim3 g, hipStream_t st, const float *x, int d, int I, int P, int k,
+                      const int32_t *exec_idx, const int32_t *soe, int n_slots,
+                      const typename WF::T *slots, size_t stride, __bf16 *hb, float *uv) {
+    if (SU == 1)
+        launch_up<MT, 1, WF>(g, st, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else if (SU == 2)
+        launch_up<MT, 2, WF>(g, st, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else if (SU == 3)
+        launch_up<MT, 3, WF>(g, st, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+    else
+        launch_up<MT, 4, WF>(g, st, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
 }
 
 template <int MT, class WF>
@@ -733,17 +793,14 @@ apex_status run_grouped(const float *x, int B, int d, int I, int E, int k,
     float *yp = reinterpret_cast<float *>(wsb + apex::align_up(pl.h_bytes, 256));
     const dim3 gu((I + kRows - 1) / kRows, E, pl.SU);
     if (pl.MT == 4)
-        launch_up<4, 1, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+        launch_up_splits<4, WF>(pl.SU, gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots,
+                                stride, hb, uv);
     else if (pl.MT == 2)
-        launch_up<2, 1, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
-    else if (pl.SU == 1)
-        launch_up<1, 1, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
-    else if (pl.SU == 2)
-        launch_up<1, 2, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
-    else if (pl.SU == 3)
-        launch_up<1, 3, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+        launch_up_splits<2, WF>(pl.SU, gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots,
+                                stride, hb, uv);
     else
-        launch_up<1, 4, WF>(gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots, stride, hb, uv);
+        launch_up_splits<1, WF>(pl.SU, gu, stream, x, d, I, P, k, exec_idx, soe, n_slots, slots,
+                                stride, hb, uv);
     APEX_HIP(hipGetLastError());
     if (pl.SU > 1) {
         const dim3 gr((P * (I / 8) + kThreads - 1) / kThreads);
@@ -767,9 +824,19 @@ apex_status run_grouped(const float *x, int B, int d, int I, int E, int k,
     else
         launch_down<1, WF>(gd, stream, d, I, P, exec_idx, soe, n_slots, slots, stride, hb, yp);
     APEX_HIP(hipGetLastError());
-    hipLaunchKernelGGL(combine_pairs, dim3((d + kThreads - 1) / kThreads, B), dim3(kThreads), 0,
-                       stream, B, d, E, k, pl.SD, exec_idx, exec_gate, soe, n_slots, yp, y,
-                       accumulate);
+    const dim3 gc((d / 4 + kThreads - 1) / kThreads, B);
+    if (pl.SD == 1)
+        hipLaunchKernelGGL(combine_pairs<1>, gc, dim3(kThreads), 0, stream, B, d, E, k, exec_idx,
+                           exec_gate, soe, n_slots, yp, y, accumulate);
+    else if (pl.SD == 2)
+        hipLaunchKernelGGL(combine_pairs<2>, gc, dim3(kThreads), 0, stream, B, d, E, k, exec_idx,
+                           exec_gate, soe, n_slots, yp, y, accumulate);
+    else if (pl.SD == 3)
+        hipLaunchKernelGGL(combine_pairs<3>, gc, dim3(kThreads), 0, stream, B, d, E, k, exec_idx,
+                           exec_gate, soe, n_slots, yp, y, accumulate);
+    else
+        hipLaunchKernelGGL(combine_pairs<4>, gc, dim3(kThreads), 0, stream, B, d, E, k, exec_idx,
+                           exec_gate, soe, n_slots, yp, y, accumulate);
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }
@@ -781,13 +848,27 @@ namespace apex {
 // [2*SU fp32 split partials, when SU > 1][h: bf16 B*k x I][per-split, per-pair outputs:
 //  SD x B*k x d fp32]
 size_t ffn_grouped_workspace(int B, int d, int I, int k) {
-    // the largest plan over the slot counts the call can be given
+    // the largest plan over the slot counts and weight formats the call can be given
     size_t worst = 0;
-    for (int experts = 1; experts <= APEX_MAX_EXPERTS; ++experts) {
-        const Plan pl = plan_for<WBf16>(B, d, I, k, APEX_MAX_EXPERTS, experts);
+    const auto cover = [&](const Plan &pl) {
         worst = std::max(worst, align_up(pl.h_bytes, 256) + align_up(pl.y_bytes, 256));
+    };
+    for (int experts = 1; experts <= APEX_MAX_EXPERTS; ++experts) {
+        cover(plan_for<WBf16>(B, d, I, k, APEX_MAX_EXPERTS, experts));
+        cover(plan_for<WE4M3>(B, d, I, k, APEX_MAX_EXPERTS, experts));
+        cover(plan_for<WMxfp4>(B, d, I, k, APEX_MAX_EXPERTS, experts));
     }
     return worst;
+}
+
+void ffn_grouped_plan(int B, int d, int I, int E, int k, int n_slots, WeightFormat fmt,
+                      int32_t out[3]) {
+    const Plan pl = fmt == WeightFormat::kE4M3    ? plan_for<WE4M3>(B, d, I, k, E, n_slots)
+                    : fmt == WeightFormat::kMxfp4 ? plan_for<WMxfp4>(B, d, I, k, E, n_slots)
+                                                  : plan_for<WBf16>(B, d, I, k, E, n_slots);
+    out[0] = pl.MT;
+    out[1] = pl.SU;
+    out[2] = pl.SD;
 }
 
 apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,

@@ -36,6 +36,10 @@ apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32
 // Two or more tokens: grouped GEMMs on the matrix cores, over slots of format fmt.  `workspace` is 256-byte aligned and holds ffn_grouped_workspace(B, d, I, k)
 // bytes.
 size_t ffn_grouped_workspace(int B, int d, int I, int k);
+// The grouped path's launch plan: out = {token tiles per pass, gate/up K splits, down K
+// splits}.
+void ffn_grouped_plan(int B, int d, int I, int E, int k, int n_slots, WeightFormat fmt,
+                      int32_t out[3]);
 apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         const int32_t *exec_idx, const float *exec_gate,
                         const int32_t *slot_of_expert, const void *slots, int n_slots,

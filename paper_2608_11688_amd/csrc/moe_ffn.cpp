@@ -9,6 +9,23 @@ extern "C" size_t apex_moe_ffn_workspace_bytes(int B, int d, int I, int k) {
     return B == 1 ? apex::ffn_b1_workspace(d, I, k) : apex::ffn_grouped_workspace(B, d, I, k);
 }
 
+extern "C" apex_status apex_moe_ffn_plan(int B, int d, int I, int E, int k, int n_slots,
+                                         int weights, int32_t *plan) {
+    APEX_REQUIRE(plan, "apex_moe_ffn_plan: NULL pointer");
+    APEX_REQUIRE(weights >= APEX_WEIGHTS_BF16 && weights <= APEX_WEIGHTS_MXFP4,
+                 "apex_moe_ffn_plan: weights=%d is not an APEX_WEIGHTS_* value", weights);
+    APEX_REQUIRE(B >= 0 && d >= 1 && I >= 1 && E >= 1 && k >= 1 && k <= E && n_slots >= 1,
+                 "apex_moe_ffn_plan: B=%d d=%d I=%d E=%d k=%d n_slots=%d out of range", B, d, I,
+                 E, k, n_slots);
+    plan[0] = plan[1] = plan[2] = 0;
+    if (B < 2) return APEX_OK;
+    const apex::WeightFormat fmt = weights == APEX_WEIGHTS_FP8_E4M3 ? apex::WeightFormat::kE4M3
+                                   : weights == APEX_WEIGHTS_MXFP4  ? apex::WeightFormat::kMxfp4
+                                                                    : apex::WeightFormat::kBf16;
+    apex::ffn_grouped_plan(B, d, I, E, k, n_slots, fmt, plan);
+    return APEX_OK;
+}
+
 namespace {
 
 apex_status moe_ffn(const char *fn, apex::WeightFormat fmt, const float *x, int B, int d, int I,

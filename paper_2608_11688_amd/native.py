@@ -24,7 +24,7 @@ APEX_OK, APEX_E_INVAL, APEX_E_UNSUPPORTED, APEX_E_HIP, APEX_E_CAPACITY = 0, -1, 
 SEL_CUMPROB, SEL_ORDINAL_CDF, SEL_STATIC, SEL_NONE = 0, 1, 2, 3
 MODE_EXACT, MODE_STALL_FREE = 0, 1
 WEIGHTS_BF16, WEIGHTS_FP8_E4M3, WEIGHTS_MXFP4 = 0, 1, 2
-ABI_VERSION = 3
+ABI_VERSION = 4
 MAX_EXPERTS = 64
 MAX_PAIRS = 1024
 
@@ -87,6 +87,7 @@ SIGNATURES = {
     "apex_moe_ffn": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_fp8": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_mxfp4": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
+    "apex_moe_ffn_plan": (I32, [I32, I32, I32, I32, I32, I32, I32, P]),
     "apex_attention_workspace_bytes": (SZ, [I32, I32, I32, I32, I32]),
     "apex_attention_decode": (I32, [P, P, P, I32, I32, I32, I32, I32, P, P, I32, I32, P, P, SZ,
                                     P]),
@@ -223,6 +224,14 @@ def apex_pack_expert_mxfp4(w1, w3, w2, d, I, out, L=None):
 
 def apex_moe_ffn_workspace_bytes(B, d, I, k):
     return lib().apex_moe_ffn_workspace_bytes(B, d, I, k)
+
+
+def apex_moe_ffn_plan(B, d, I, E, k, n_slots, weights="bf16"):
+    """(token tiles per pass, gate/up K splits, down K splits) of a grouped call."""
+    plan = (C.c_int32 * 3)()
+    code = WEIGHT_FORMATS[weights][0] if isinstance(weights, str) else int(weights)
+    _call("apex_moe_ffn_plan", B, d, I, E, k, n_slots, code, C.addressof(plan))
+    return tuple(plan)
 
 
 def apex_moe_ffn(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots, y,

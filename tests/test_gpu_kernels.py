@@ -13,6 +13,7 @@ from oracle import ffn as offn
 from oracle import gating, routing
 from oracle.residency import Residency
 from paper_2608_11688_amd import configs, inputs, native
+from tests.ffn_plans import PLAN_CASES
 from tests.parity import TieLedger, ffn_close
 
 pytestmark = pytest.mark.gpu
@@ -294,8 +295,8 @@ MFMA_SHAPES = [
     (shape("mfma_b48", 411, 512, 6, 2, I=256), 48),       # four token tiles per pass
     (shape("mfma_b16", 412, 1024, 32, 8, I=512), 16),     # one tile per pass
     (shape("mfma_b2", 415, 1024, 32, 8, I=512), 2),       # smallest batch on this path
-    # four experts, so both projections split K: up over 3 splits and down over 4, then
-    # up over 4 and down over 3; ragged K tails on both sides
+    # four experts with ragged K tails on both sides (every split plan is run by
+    # test_ffn_every_plan_matches_oracle)
     (shape("mfma_split_a", 416, 776, 4, 2, I=1000), 4),
     (shape("mfma_split_b", 417, 1000, 4, 2, I=776), 5),
 ]
@@ -306,6 +307,18 @@ def test_ffn_mfma_parity(torch, cfg, B):
     case = FfnCase(torch, cfg, B, seed=cfg.cfg_id)
     y = case.run()
     print(cfg.name, B, ffn_close(y, case.oracle(), cfg.name))
+
+
+@pytest.mark.parametrize("weights,B,d,I,E,plan", PLAN_CASES,
+                         ids=[f"{w}-B{b}-d{d}-I{i}-{'x'.join(map(str, p))}"
+                              for w, b, d, i, _, p in PLAN_CASES])
+def test_ffn_every_plan_matches_oracle(torch, weights, B, d, I, E, plan):
+    cfg = shape(f"plan_{weights}_{B}_{d}_{I}", 460 + PLAN_CASES.index(
+        (weights, B, d, I, E, plan)), d, E, 2, I=I)
+    case = FfnCase(torch, cfg, B, seed=cfg.cfg_id, weights=weights)
+    assert native.apex_moe_ffn_plan(B, d, I, E, 2, case.n_slots, weights) == plan
+    y = case.run()
+    print(cfg.name, plan, ffn_close(y, case.oracle(), f"{cfg.name} {plan}"))
 
 
 def test_ffn_mfma_skewed_expert_takes_every_token(torch):
@@ -364,8 +377,8 @@ FP8_SHAPES = [
     (configs.GRANITE_1B, 1), (configs.GRANITE_3B, 1), (configs.OLMOE, 1), (configs.TINY, 1),
     (configs.GRANITE_3B, 8), (configs.OLMOE, 16),
     (shape("fp8_b48", 430, 512, 6, 2, I=256), 48),         # four token tiles per pass
-    (shape("fp8_split_a", 431, 784, 4, 2, I=1008), 4),     # up 3 splits, down 4; ragged K
-    (shape("fp8_split_b", 432, 1008, 4, 2, I=784), 5),     # up 4 splits, down 3
+    (shape("fp8_split_a", 431, 784, 4, 2, I=1008), 4),     # few experts, ragged K tails
+    (shape("fp8_split_b", 432, 1008, 4, 2, I=784), 5),
     (shape("fp8_small", 433, 16, 3, 2, I=48), 3),          # one 16-byte chunk per row
 ]
 
@@ -400,7 +413,7 @@ MXFP4_SHAPES = [
     (configs.PHI_7B, 1), (configs.DEEPSEEK_16B, 1),         # d = 4096; I = 1472
     (configs.GRANITE_3B, 8), (configs.OLMOE, 16),
     (shape("fp4_b48", 440, 512, 6, 2, I=256), 48),          # four token tiles per pass
-    (shape("fp4_split_a", 441, 800, 4, 2, I=992), 4),       # split K; ragged last K block
+    (shape("fp4_split_a", 441, 800, 4, 2, I=992), 4),       # few experts; ragged last K block
     (shape("fp4_split_b", 442, 992, 4, 2, I=800), 5),
     (shape("fp4_small", 443, 32, 3, 2, I=64), 3),           # one block per row
 ]

@@ -225,3 +225,26 @@ def test_pack_expert_fp8_matches_the_oracle_quantiser(plan_lib):
     assert sc[5] == 0 and not rows[5, :d].any()
     with pytest.raises(native.ApexError):
         native.apex_pack_expert_fp8(w1, w3, w2, 44, I, out, L=plan_lib)   # d not a multiple of 8
+
+
+def test_moe_ffn_plan():
+    # batch 1 takes the batch-1 kernels; bad arguments are errors
+    assert native.apex_moe_ffn_plan(1, 2048, 1024, 64, 8, 24) == (0, 0, 0)
+    with pytest.raises(native.ApexError):
+        native.apex_moe_ffn_plan(8, 2048, 1024, 64, 8, 24, weights=7)
+    with pytest.raises(native.ApexError):
+        native.apex_moe_ffn_plan(8, 2048, 1024, 4, 8, 4)          # k > E
+    # every plan the GPU parity test relies on is still taken by its shape (all of the
+    # shape's experts resident; k = 2)
+    from tests.ffn_plans import PLAN_CASES
+    seen = set()
+    for weights, B, d, I, E, plan in PLAN_CASES:
+        assert native.apex_moe_ffn_plan(B, d, I, E, 2, E, weights) == plan, (weights, B, d, I)
+        seen.add((weights, plan[0], plan[1] > 1, plan[2] > 1))
+    assert len(seen) == 3 * 3 * 2 * 2
+    # the workspace covers the largest plan of every format
+    for weights, B, d, I, E, plan in PLAN_CASES:
+        MT, SU, SD = plan
+        P = B * 2
+        need = (2 * SU * P * I * 4 if SU > 1 else 0) + P * I * 2 + SD * P * d * 4
+        assert native.apex_moe_ffn_workspace_bytes(B, d, I, 2) >= need
