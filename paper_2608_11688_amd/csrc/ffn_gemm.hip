@@ -23,7 +23,6 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <type_traits>
 
 #include "ffn_device.h"
 #include "ffn_internal.h"
@@ -58,18 +57,28 @@ __device__ __forceinline__ uint4 keep_if(uint4 v, bool c) {
     return make_uint4(c ? v.x : 0u, c ? v.y : 0u, c ? v.z : 0u, c ? v.w : 0u);
 }
 
-// Activation sources: 8 consecutive K values of one row as bf16.
-struct ActF32 {          // fp32 rows (the FFN input x), rounded here
-    static __device__ __forceinline__ uint4 load(const void *row, int kc, size_t) {
+// Activation sources: 8 consecutive K values of one row.  load() fetches them as they are
+// stored and to_bf16() converts them when the block is staged in LDS, so that no
+// arithmetic follows a load directly (which would make the compiler wait for it, and for
+// every older load, before the matrix cores work on the previous block).
+struct ActF32 {          // fp32 rows (the FFN input x), rounded to bf16 at staging
+    struct Raw {
+        float4 a, b;
+    };
+    static __device__ __forceinline__ Raw load(const void *row, int kc) {
         const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(row) + kc);
-        const float4 a = p[0], b = p[1];
-        return pack_bf16(a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w);
+        return Raw{p[0], p[1]};
+    }
+    static __device__ __forceinline__ uint4 to_bf16(const Raw &r) {
+        return pack_bf16(r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w);
     }
 };
 struct ActBf16 {         // bf16 rows (h)
-    static __device__ __forceinline__ uint4 load(const void *row, int kc, size_t) {
+    using Raw = uint4;
+    static __device__ __forceinline__ Raw load(const void *row, int kc) {
         return *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(row) + kc);
     }
+    static __device__ __forceinline__ uint4 to_bf16(const Raw &r) { return r; }
 };
 // h = bf16(silu(u) * v) of 8 consecutive values from SU split partials: u of split s at
 // r + 2s*stride, v at r + (2s+1)*stride, the splits added in order.
@@ -93,21 +102,21 @@ __device__ __forceinline__ uint4 swiglu8(const float *r, size_t stride) {
                      silu(u[6]) * v[6], silu(u[7]) * v[7]);
 }
 
-// Weight formats of a slot.  One 16-byte load per thread covers kPerLoad consecutive K
-// values of one row; kThrPerRow threads cover a 128-wide K block of the row and
-// kRowsPerPass rows are loaded per pass of the workgroup.
+// Weight formats of a slot.
 // kUpGroups: workgroups the gate/up projection's K splits aim at (see plan_for);
 // kKPerElem: K values per element of T; kFp8: fp32 row scales after the codes;
-// kBlockScale: one scale byte per 32 K values of a row (kPerLoad is then one block);
+// kBlockScale: one scale byte per 32 K values of a row;
 // kCodes: the codes go to LDS as bytes, in K blocks of kb<MT>() values, and are widened
-// at fragment read (gemm_mainloop_codes); otherwise bf16 tiles of kKB (gemm_mainloop).
+// at fragment read (gemm_mainloop_codes); otherwise bf16 tiles of kKB (gemm_mainloop),
+// where one 16-byte load covers 8 K values of a row, kThrPerRow threads cover a block of
+// the row and kRowsPerPass rows are loaded per pass of the workgroup.
 struct WBf16 {           // apex_pack_expert slots: bf16 weights
     using T = uint16_t;
     static constexpr bool kFp8 = false, kBlockScale = false, kCodes = false;
     template <int MT> static constexpr int kb() { return kKB; }
     static constexpr int kUpGroups = 400;
     static constexpr int kKPerElem = 1;
-    static constexpr int kPerLoad = 8, kThrPerRow = kKB / 8, kRowsPerPass = kThreads / kThrPerRow;
+    static constexpr int kThrPerRow = kKB / 8, kRowsPerPass = kThreads / kThrPerRow;
     static constexpr int kLoads = kRows / kRowsPerPass;
 };
 struct WE4M3 {           // apex_pack_expert_fp8 slots: E4M3 codes, fp32 row scales after them
@@ -117,8 +126,6 @@ struct WE4M3 {           // apex_pack_expert_fp8 slots: E4M3 codes, fp32 row sca
     template <int MT> static constexpr int kb() { return MT == 1 ? 256 : 128; }
     static constexpr int kUpGroups = 800;
     static constexpr int kKPerElem = 1;
-    static constexpr int kPerLoad = 16, kThrPerRow = kKB / 16, kRowsPerPass = kThreads / kThrPerRow;
-    static constexpr int kLoads = kRows / kRowsPerPass;
 };
 struct WMxfp4 {          // apex_pack_expert_mxfp4 slots: two E2M1 codes per byte, block scales
     using T = uint8_t;
@@ -127,44 +134,7 @@ struct WMxfp4 {          // apex_pack_expert_mxfp4 slots: two E2M1 codes per byt
     template <int MT> static constexpr int kb() { return MT == 1 ? 512 : 256; }
     static constexpr int kUpGroups = 1400;
     static constexpr int kKPerElem = 2;
-    static constexpr int kPerLoad = 32, kThrPerRow = kKB / 32, kRowsPerPass = kThreads / kThrPerRow;
-    static constexpr int kLoads = kRows / kRowsPerPass;
 };
-
-// 16 E4M3 codes (little-endian bytes of v) as 16 bf16 values, exactly: every E4M3 value
-// is a bf16 value, so dropping the low half of the fp32 conversion loses nothing.
-__device__ __forceinline__ void widen_e4m3(uint4 v, uint4 &lo, uint4 &hi) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t o[8];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const auto a = __builtin_amdgcn_cvt_pk_f32_fp8(int(w[q]), false);   // bytes 0, 1
-        const auto b = __builtin_amdgcn_cvt_pk_f32_fp8(int(w[q]), true);    // bytes 2, 3
-        o[2 * q] = (__float_as_uint(a[0]) >> 16) | (__float_as_uint(a[1]) & 0xffff0000u);
-        o[2 * q + 1] = (__float_as_uint(b[0]) >> 16) | (__float_as_uint(b[1]) & 0xffff0000u);
-    }
-    lo = make_uint4(o[0], o[1], o[2], o[3]);
-    hi = make_uint4(o[4], o[5], o[6], o[7]);
-}
-
-// 32 E2M1 codes (two per byte of v, the low nibble first) times their block's scale as
-// 32 bf16 values, exactly (an E2M1 value times a power of two is a bf16 value).
-__device__ __forceinline__ void widen_mxfp4(uint4 v, uint32_t scale_byte, uint4 (&out)[4]) {
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    const float sc = apex::ffn::mx_scale(scale_byte);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const auto cvt = [&](auto sel) {   // byte sel of w[q]: elements 2 sel, 2 sel + 1
-            return __builtin_bit_cast(
-                uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w[q], sc, decltype(sel)::value));
-        };
-        out[q] = make_uint4(cvt(std::integral_constant<int, 0>{}),
-                            cvt(std::integral_constant<int, 1>{}),
-                            cvt(std::integral_constant<int, 2>{}),
-                            cvt(std::integral_constant<int, 3>{}));
-    }
-}
 
 // The pairs p < P with exec_idx[p] == e, in ascending order, into list[]; returns how
 // many.  256 threads; P <= 1024 (four rounds of wave ballots).
@@ -196,70 +166,34 @@ __device__ int expert_pairs(const int32_t *__restrict__ exec_idx, int P, int e, 
     return base;
 }
 
-// One K block of the tile into registers.  Every weight address is valid (rows and K
-// are clamped) and pieces outside the tile are zeroed after the load instead of
-// branching, so the weight loads issue back to back.
-template <int NW, int MT, class Act, class WF>
-__device__ __forceinline__ void gemm_load(uint4 (&wreg)[NW][WF::kLoads],
-                                          uint32_t (&sreg)[NW][WF::kLoads], uint4 (&xreg)[MT],
-                                          const typename WF::T *const (&wbase)[NW],
-                                          size_t wstride, const uint8_t *const (&sbase)[NW],
-                                          size_t sstride, int rows_valid, int K,
-                                          const void *const (&xrow)[MT], const bool (&xok)[MT],
-                                          size_t xstride, int k0) {
-    const int t = threadIdx.x;
-    const int wseg = t % WF::kThrPerRow, wr0 = t / WF::kThrPerRow;
-    const int wk = k0 + WF::kPerLoad * wseg;
-    const bool win = wk < K;
-    const int wkc = win ? wk : K - WF::kPerLoad;
-#pragma unroll
-    for (int m = 0; m < NW; ++m)
-#pragma unroll
-        for (int j = 0; j < WF::kLoads; ++j) {
-            const int row = wr0 + WF::kRowsPerPass * j;
-            const int rc = row < rows_valid ? row : rows_valid - 1;
-            const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
-                                                             wkc / WF::kKPerElem);
-            wreg[m][j] = keep_if(v, win && row < rows_valid);
-            if constexpr (WF::kBlockScale) sreg[m][j] = sbase[m][size_t(rc) * sstride + wkc / 32];
-        }
-    // activation rows past the expert's tokens (tile padding) are not loaded at all
-    const int seg = t & 15;
-    const int kk = k0 + 8 * seg;
-    const bool in = kk < K;
-    const int kc = in ? kk : K - 8;
-#pragma unroll
-    for (int j = 0; j < MT; ++j) {
-        uint4 v = make_uint4(0u, 0u, 0u, 0u);
-        if (in && xok[j]) v = Act::load(xrow[j], kc, xstride);
-        xreg[j] = v;
-    }
-}
-
-// Grouped-GEMM mainloop shared by the gate/up and down projections.
+// Grouped-GEMM mainloop over bf16 slots, shared by the gate/up and down projections.
 // A workgroup (4 wavefronts) owns a tile of 64 weight rows of NW weight matrices and up
 // to 16*MT tokens, over the K blocks [b_lo, b_hi).  Every thread loads 16-byte pieces so
 // that each group of 16 threads reads 256 contiguous bytes of one weight row (whole
 // cache lines), the block goes to LDS, and while the matrix cores work on it the next
-// block is already loading into registers.  Wavefront w multiplies its 16 rows with
-// every token tile: v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.  Tiles past
-// the expert's last token multiply zero rows: skipping them on the token count made the
-// compiler move the accumulators between register files around the skip, and the E4M3
-// kernel with two tiles then gave wrong sums that changed from run to run.
-template <int NW, int MT, class Act, class WF>
-__device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbase)[NW],
-                                              size_t wstride, const uint8_t *const (&sbase)[NW],
-                                              size_t sstride,
-                                              int rows_valid, int K, int b_lo, int b_hi,
-                                              const void *const (&xrow)[MT],
-                                              const bool (&xok)[MT], size_t xstride,
+// block is already loading into registers.  Every load address is valid (rows and K are
+// clamped, padding token rows read a real row) and pieces outside the tile are zeroed
+// when the block is staged, not when it arrives: the first use of a loaded register is
+// then after the matrix-core work on the previous block, which is what keeps the loads
+// in flight across it.  Wavefront w multiplies its 16 rows with every token tile:
+// v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.  Tiles past the expert's last
+// token multiply zero rows: skipping them on the token count made the compiler move the
+// accumulators between register files around the skip, and the E4M3 kernel with two
+// tiles then gave wrong sums that changed from run to run.
+template <int NW, int MT, class Act>
+__device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW],
+                                              size_t wstride, int rows_valid, int K, int b_lo,
+                                              int b_hi, const void *const (&xrow)[MT],
+                                              const bool (&xok)[MT],
                                               uint16_t (*Ws)[kRows][kLdsRow],
                                               uint16_t (*Xs)[kLdsRow], floatx4 (&acc)[NW][MT]) {
+    constexpr int kLoads = WBf16::kLoads, kRpp = WBf16::kRowsPerPass, kTpr = WBf16::kThrPerRow;
     const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
     const int seg = t & 15, r0 = t >> 4;
-    const int wseg = t % WF::kThrPerRow, wr0 = t / WF::kThrPerRow;
-    uint4 wreg[NW][WF::kLoads], xreg[MT];
-    uint32_t sreg[NW][WF::kLoads];
+    const int wseg = t % kTpr, wr0 = t / kTpr;
+    uint4 wreg[NW][kLoads];
+    typename Act::Raw xraw[MT];
+    bool w_in = false, x_in = false;   // K range of the block held in the registers
 #pragma unroll
     for (int m = 0; m < NW; ++m)
 #pragma unroll
@@ -273,35 +207,41 @@ __device__ __forceinline__ void gemm_mainloop(const typename WF::T *const (&wbas
         const int q = b + rot;
         return (b_lo + (q >= nb ? q - nb : q)) * kKB;
     };
-    gemm_load<NW, MT, Act, WF>(wreg, sreg, xreg, wbase, wstride, sbase, sstride, rows_valid, K,
-                               xrow, xok, xstride, kblk(0));
+    const auto load = [&](int k0) {
+        const int wk = k0 + 8 * wseg;
+        w_in = wk < K;
+        const int wkc = w_in ? wk : K - 8;
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j) {
+                const int row = wr0 + kRpp * j;
+                const int rc = row < rows_valid ? row : rows_valid - 1;
+                wreg[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + wkc);
+            }
+        const int kk = k0 + 8 * seg;
+        x_in = kk < K;
+        const int kc = x_in ? kk : K - 8;
+#pragma unroll
+        for (int j = 0; j < MT; ++j) xraw[j] = Act::load(xrow[j], kc);
+    };
+    load(kblk(0));
     for (int b = 0; b < nb; ++b) {
         __syncthreads();   // the previous block's fragments have been read
 #pragma unroll
         for (int m = 0; m < NW; ++m)
 #pragma unroll
-            for (int j = 0; j < WF::kLoads; ++j) {
-                uint16_t *dst = &Ws[m][wr0 + WF::kRowsPerPass * j][WF::kPerLoad * wseg];
-                if constexpr (WF::kBlockScale) {
-                    uint4 q[4];
-                    widen_mxfp4(wreg[m][j], sreg[m][j], q);
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) *reinterpret_cast<uint4 *>(dst + 8 * c) = q[c];
-                } else if constexpr (WF::kFp8) {
-                    uint4 lo, hi;
-                    widen_e4m3(wreg[m][j], lo, hi);
-                    *reinterpret_cast<uint4 *>(dst) = lo;
-                    *reinterpret_cast<uint4 *>(dst + 8) = hi;
-                } else {
-                    *reinterpret_cast<uint4 *>(dst) = wreg[m][j];
-                }
+            for (int j = 0; j < kLoads; ++j) {
+                const int row = wr0 + kRpp * j;
+                *reinterpret_cast<uint4 *>(&Ws[m][row][8 * wseg]) =
+                    keep_if(wreg[m][j], w_in && row < rows_valid);
             }
 #pragma unroll
-        for (int j = 0; j < MT; ++j) *reinterpret_cast<uint4 *>(&Xs[r0 + 16 * j][8 * seg]) = xreg[j];
+        for (int j = 0; j < MT; ++j)
+            *reinterpret_cast<uint4 *>(&Xs[r0 + 16 * j][8 * seg]) =
+                keep_if(Act::to_bf16(xraw[j]), x_in && xok[j]);
         __syncthreads();
-        if (b + 1 < nb)
-            gemm_load<NW, MT, Act, WF>(wreg, sreg, xreg, wbase, wstride, sbase, sstride,
-                                       rows_valid, K, xrow, xok, xstride, kblk(b + 1));
+        if (b + 1 < nb) load(kblk(b + 1));
 #pragma unroll
         for (int q = 0; q < kKB / 32; ++q) {
             const int kc = 32 * q + 8 * (lane >> 4);
@@ -382,8 +322,7 @@ template <int NW, int MT, class Act, class WF>
 __device__ __forceinline__ void gemm_mainloop_codes(
     const uint8_t *const (&wbase)[NW], size_t wstride, const uint8_t *const (&sbase)[NW],
     size_t sstride, int rows_valid, int K, int b_lo, int b_hi, const void *const (&xrow)[MT],
-    const bool (&xok)[MT], size_t xstride, GemmLds<NW, MT, WF, true> &lds,
-    floatx4 (&acc)[NW][MT]) {
+    const bool (&xok)[MT], GemmLds<NW, MT, WF, true> &lds, floatx4 (&acc)[NW][MT]) {
     using L = GemmLds<NW, MT, WF, true>;
     constexpr int KB = L::KB, RB = L::RB;
     constexpr int TPR = RB / 16;              // threads per row of a block
@@ -394,8 +333,10 @@ __device__ __forceinline__ void gemm_mainloop_codes(
     const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
     const int wseg = t % TPR, wr0 = t / TPR;
     const int seg = t & 15, r0 = t >> 4;
-    uint4 wreg[NW][NL], xreg[QX][MT];
+    uint4 wreg[NW][NL];
     uint32_t sreg[NW][NL];
+    typename Act::Raw xraw[QX][MT];
+    bool w_in = false, x_in[QX];   // K range of the block held in the registers
 #pragma unroll
     for (int m = 0; m < NW; ++m)
 #pragma unroll
@@ -407,34 +348,30 @@ __device__ __forceinline__ void gemm_mainloop_codes(
         const int q = b + rot;
         return (b_lo + (q >= nb ? q - nb : q)) * KB;
     };
-    // One block into registers: every address valid (rows and K clamped), pieces outside
-    // the tile zeroed after the load.
+    // One block into registers: every address valid (rows and K clamped, padding token
+    // rows read a real row); pieces outside the tile are zeroed at staging, as in
+    // gemm_mainloop, so that the loads stay in flight across the matrix-core work.
     const auto load = [&](int k0) {
         const int wk = k0 + KPL * wseg;
-        const bool win = wk < K;
-        const int wkc = win ? wk : K - KPL;
+        w_in = wk < K;
+        const int wkc = w_in ? wk : K - KPL;
 #pragma unroll
         for (int m = 0; m < NW; ++m)
 #pragma unroll
             for (int j = 0; j < NL; ++j) {
                 const int row = wr0 + RPP * j;
                 const int rc = row < rows_valid ? row : rows_valid - 1;
-                const uint4 v = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
-                                                                 wkc / WF::kKPerElem);
-                wreg[m][j] = keep_if(v, win && row < rows_valid);
+                wreg[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
+                                                              wkc / WF::kKPerElem);
                 if constexpr (WF::kBlockScale) sreg[m][j] = sbase[m][size_t(rc) * sstride + wkc / 32];
             }
 #pragma unroll
         for (int q = 0; q < QX; ++q) {
             const int kk = k0 + 128 * q + 8 * seg;
-            const bool in = kk < K;
-            const int kc = in ? kk : K - 8;
+            x_in[q] = kk < K;
+            const int kc = x_in[q] ? kk : K - 8;
 #pragma unroll
-            for (int j = 0; j < MT; ++j) {
-                uint4 v = make_uint4(0u, 0u, 0u, 0u);
-                if (in && xok[j]) v = Act::load(xrow[j], kc, xstride);
-                xreg[q][j] = v;
-            }
+            for (int j = 0; j < MT; ++j) xraw[q][j] = Act::load(xrow[j], kc);
         }
     };
     load(kblk(0));
@@ -445,14 +382,16 @@ __device__ __forceinline__ void gemm_mainloop_codes(
 #pragma unroll
             for (int j = 0; j < NL; ++j) {
                 const int row = wr0 + RPP * j;
-                *reinterpret_cast<uint4 *>(&lds.Wc[m][row][16 * wseg]) = wreg[m][j];
+                *reinterpret_cast<uint4 *>(&lds.Wc[m][row][16 * wseg]) =
+                    keep_if(wreg[m][j], w_in && row < rows_valid);
                 if constexpr (WF::kBlockScale) lds.Sc[m][row][wseg] = uint8_t(sreg[m][j]);
             }
 #pragma unroll
         for (int q = 0; q < QX; ++q)
 #pragma unroll
             for (int j = 0; j < MT; ++j)
-                *reinterpret_cast<uint4 *>(&lds.Xs[r0 + 16 * j][128 * q + 8 * seg]) = xreg[q][j];
+                *reinterpret_cast<uint4 *>(&lds.Xs[r0 + 16 * j][128 * q + 8 * seg]) =
+                    keep_if(Act::to_bf16(xraw[q][j]), x_in[q] && xok[j]);
         __syncthreads();
         if (b + 1 < nb) load(kblk(b + 1));
         const int rr = 16 * wave + (lane & 15);
@@ -480,14 +419,14 @@ __device__ __forceinline__ void gemm_tile(const typename WF::T *const (&wbase)[N
                                           size_t wstride, const uint8_t *const (&sbase)[NW],
                                           size_t sstride, int rows_valid, int K, int b_lo,
                                           int b_hi, const void *const (&xrow)[MT],
-                                          const bool (&xok)[MT], size_t xstride,
-                                          GemmLds<NW, MT, WF> &lds, floatx4 (&acc)[NW][MT]) {
+                                          const bool (&xok)[MT], GemmLds<NW, MT, WF> &lds,
+                                          floatx4 (&acc)[NW][MT]) {
     if constexpr (WF::kCodes)
         gemm_mainloop_codes<NW, MT, Act, WF>(wbase, wstride, sbase, sstride, rows_valid, K,
-                                             b_lo, b_hi, xrow, xok, xstride, lds, acc);
+                                             b_lo, b_hi, xrow, xok, lds, acc);
     else
-        gemm_mainloop<NW, MT, Act, WF>(wbase, wstride, sbase, sstride, rows_valid, K, b_lo,
-                                       b_hi, xrow, xok, xstride, lds.Ws, lds.Xs, acc);
+        gemm_mainloop<NW, MT, Act>(wbase, wstride, rows_valid, K, b_lo, b_hi, xrow, xok,
+                                   lds.Ws, lds.Xs, acc);
 }
 
 // The fp32 row scales of an apex_pack_expert_fp8 slot: W1 rows, W3 rows, W2 rows.
@@ -538,8 +477,7 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
         }
         floatx4 acc[2][MT];
         gemm_tile<2, MT, ActF32, WF>(wbase, size_t(2) * d / WF::kKPerElem, sbase,
-                                     size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, 0, lds,
-                                     acc);
+                                     size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, lds, acc);
         const int i = i0 + 16 * wave + (lane & 15);
         float s1 = 1.f, s3 = 1.f;
         if constexpr (WF::kFp8) {
@@ -606,7 +544,7 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
         }
         floatx4 acc[1][MT];
         gemm_tile<1, MT, ActBf16, WF>(wbase, size_t(I) / WF::kKPerElem, sbase,
-                                      size_t(I / 32), d - j0, I, b_lo, b_hi, hrow, hok, 0, lds,
+                                      size_t(I / 32), d - j0, I, b_lo, b_hi, hrow, hok, lds,
                                       acc);
         const int j = j0 + 16 * wave + (lane & 15);
         float s2 = 1.f;
