@@ -209,8 +209,10 @@ def copy_calibration(torch, native, cs, nbytes=256 << 20, reps=5):
 def measured_traffic(cfg, batch, weights="bf16"):
     """HBM bytes per apex_moe_ffn call from the committed FETCH_SIZE / WRITE_SIZE records,
     or None when no record is for this workload and batch, or the source of the kernels
-    it covers has changed since the counters were taken."""
+    it covers or the compiler flags they are built with have changed since the counters
+    were taken."""
     import hashlib
+    from paper_2608_11688_amd import build as _build
     path = os.path.join(ROOT, "profiles", "moe_ffn_traffic.json")
     try:
         records = json.load(open(path))["records"]
@@ -225,6 +227,8 @@ def measured_traffic(cfg, batch, weights="bf16"):
         except (OSError, KeyError):
             return None
         if hashlib.sha256(src).hexdigest() != rec.get("kernel_source_sha256"):
+            return None
+        if rec.get("hipcc_flags") != list(_build.HIPCC_FLAGS):
             return None
         return rec.get("traffic_bytes_per_call")
     return None

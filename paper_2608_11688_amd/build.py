@@ -30,6 +30,10 @@ HOST_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "pack_mxfp4.cpp"]
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
                # keep the compiler from forming packed fp32 instructions
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               # load the first kernel arguments into SGPRs at dispatch (gfx950 kernarg
+               # preload; the code object keeps a fallback that loads them itself), so a
+               # kernel's prologue does not wait on several rounds of argument loads
+               "-mllvm", "-amdgpu-kernarg-preload-count=16",
                "-Wall", "-Wno-unused-result"]
 
 
