@@ -107,7 +107,7 @@ __device__ __forceinline__ uint4 swiglu8(const float *r, size_t stride) {
 // kKPerElem: K values per element of T; kFp8: fp32 row scales after the codes;
 // kBlockScale: one scale byte per 32 K values of a row;
 // kCodes: the codes go to LDS as bytes, in K blocks of kb<MT>() values, and are widened
-// at fragment read (gemm_mainloop_codes); otherwise bf16 tiles of kKB (gemm_mainloop),
+// at fragment read; otherwise bf16 tiles of kKB,
 // where one 16-byte load covers 8 K values of a row, kThrPerRow threads cover a block of
 // the row and kRowsPerPass rows are loaded per pass of the workgroup.
 struct WBf16 {           // apex_pack_expert slots: bf16 weights
@@ -136,140 +136,70 @@ struct WMxfp4 {          // apex_pack_expert_mxfp4 slots: two E2M1 codes per byt
     static constexpr int kKPerElem = 2;
 };
 
+constexpr int kPairRounds = APEX_MAX_PAIRS / kThreads;
+
+// This thread's exec_idx entries, pairs r * 256 + t (the index clamped to P - 1; entries
+// past P are dropped by expert_pairs).  Issued before a tile's first weight loads, so
+// that the pair scan waits only for these, not for the weights.
+__device__ __forceinline__ void pair_ids(const int32_t *__restrict__ exec_idx, int P,
+                                         int (&ev)[kPairRounds]) {
+#pragma unroll
+    for (int r = 0; r < kPairRounds; ++r) {
+        const int p = r * kThreads + threadIdx.x;
+        ev[r] = exec_idx[p < P ? p : P - 1];
+    }
+}
+
 // The pairs p < P with exec_idx[p] == e, in ascending order, into list[]; returns how
 // many.  256 threads; P <= 1024 (four rounds of wave ballots).
-__device__ int expert_pairs(const int32_t *__restrict__ exec_idx, int P, int e, int *list,
+__device__ int expert_pairs(const int (&ev)[kPairRounds], int P, int e, int *list,
                             int (*cnt)[4]) {
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-    int ev[APEX_MAX_PAIRS / kThreads];
+    bool hit[kPairRounds];
+    unsigned long long m[kPairRounds];
 #pragma unroll
-    for (int r = 0; r < APEX_MAX_PAIRS / kThreads; ++r) {
-        const int p = r * kThreads + t;
-        ev[r] = p < P ? exec_idx[p] : -1;
-    }
-    unsigned long long m[APEX_MAX_PAIRS / kThreads];
-#pragma unroll
-    for (int r = 0; r < APEX_MAX_PAIRS / kThreads; ++r) {
-        m[r] = __ballot(ev[r] == e);
+    for (int r = 0; r < kPairRounds; ++r) {
+        hit[r] = r * kThreads + t < P && ev[r] == e;
+        m[r] = __ballot(hit[r]);
         if (lane == 0) cnt[r][wave] = __popcll(m[r]);
     }
     __syncthreads();
     int base = 0;
 #pragma unroll
-    for (int r = 0; r < APEX_MAX_PAIRS / kThreads; ++r) {
+    for (int r = 0; r < kPairRounds; ++r) {
         int off = base;
         for (int w = 0; w < wave; ++w) off += cnt[r][w];
-        if (ev[r] == e) list[off + __popcll(m[r] & ((1ull << lane) - 1ull))] = r * kThreads + t;
+        if (hit[r]) list[off + __popcll(m[r] & ((1ull << lane) - 1ull))] = r * kThreads + t;
         base += cnt[r][0] + cnt[r][1] + cnt[r][2] + cnt[r][3];
     }
     __syncthreads();
     return base;
 }
 
-// Grouped-GEMM mainloop over bf16 slots, shared by the gate/up and down projections.
-// A workgroup (4 wavefronts) owns a tile of 64 weight rows of NW weight matrices and up
-// to 16*MT tokens, over the K blocks [b_lo, b_hi).  Every thread loads 16-byte pieces so
-// that each group of 16 threads reads 256 contiguous bytes of one weight row (whole
-// cache lines), the block goes to LDS, and while the matrix cores work on it the next
-// block is already loading into registers.  Every load address is valid (rows and K are
-// clamped, padding token rows read a real row) and pieces outside the tile are zeroed
-// when the block is staged, not when it arrives: the first use of a loaded register is
-// then after the matrix-core work on the previous block, which is what keeps the loads
-// in flight across it.  Wavefront w multiplies its 16 rows with every token tile:
-// v_mfma_f32_16x16x32_bf16, tokens as M, weight rows as N.  Tiles past the expert's last
-// token multiply zero rows: skipping them on the token count made the compiler move the
-// accumulators between register files around the skip, and the E4M3 kernel with two
-// tiles then gave wrong sums that changed from run to run.
-template <int NW, int MT, class Act>
-__device__ __forceinline__ void gemm_mainloop(const uint16_t *const (&wbase)[NW],
-                                              size_t wstride, int rows_valid, int K, int b_lo,
-                                              int b_hi, const void *const (&xrow)[MT],
-                                              const bool (&xok)[MT],
-                                              uint16_t (*Ws)[kRows][kLdsRow],
-                                              uint16_t (*Xs)[kLdsRow], floatx4 (&acc)[NW][MT]) {
-    constexpr int kLoads = WBf16::kLoads, kRpp = WBf16::kRowsPerPass, kTpr = WBf16::kThrPerRow;
-    const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
-    const int seg = t & 15, r0 = t >> 4;
-    const int wseg = t % kTpr, wr0 = t / kTpr;
-    uint4 wreg[NW][kLoads];
-    typename Act::Raw xraw[MT];
-    bool w_in = false, x_in = false;   // K range of the block held in the registers
-#pragma unroll
-    for (int m = 0; m < NW; ++m)
-#pragma unroll
-        for (int tt = 0; tt < MT; ++tt) acc[m][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const int nb = b_hi - b_lo;
-    if (nb <= 0) return;
-    // Workgroups start at different K blocks: tiles that run side by side then read
-    // different offsets of their rows instead of all hitting the same DRAM channels.
-    const int rot = int((blockIdx.x * 7u + blockIdx.y * 13u) % unsigned(nb));
-    const auto kblk = [nb, rot, b_lo](int b) {
+// The K blocks of split z of a K range cut into blocks of kb values: nb blocks from b_lo,
+// visited from a rotated start.  Workgroups start at different K blocks: tiles that run
+// side by side then read different offsets of their rows instead of all hitting the same
+// DRAM channels.
+struct KBlocks {
+    int b_lo, nb, rot, kb;
+    __device__ __forceinline__ int k0(int b) const {
         const int q = b + rot;
-        return (b_lo + (q >= nb ? q - nb : q)) * kKB;
-    };
-    const auto load = [&](int k0) {
-        const int wk = k0 + 8 * wseg;
-        w_in = wk < K;
-        const int wkc = w_in ? wk : K - 8;
-#pragma unroll
-        for (int m = 0; m < NW; ++m)
-#pragma unroll
-            for (int j = 0; j < kLoads; ++j) {
-                const int row = wr0 + kRpp * j;
-                const int rc = row < rows_valid ? row : rows_valid - 1;
-                wreg[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + wkc);
-            }
-        const int kk = k0 + 8 * seg;
-        x_in = kk < K;
-        const int kc = x_in ? kk : K - 8;
-#pragma unroll
-        for (int j = 0; j < MT; ++j) xraw[j] = Act::load(xrow[j], kc);
-    };
-    load(kblk(0));
-    for (int b = 0; b < nb; ++b) {
-        __syncthreads();   // the previous block's fragments have been read
-#pragma unroll
-        for (int m = 0; m < NW; ++m)
-#pragma unroll
-            for (int j = 0; j < kLoads; ++j) {
-                const int row = wr0 + kRpp * j;
-                *reinterpret_cast<uint4 *>(&Ws[m][row][8 * wseg]) =
-                    keep_if(wreg[m][j], w_in && row < rows_valid);
-            }
-#pragma unroll
-        for (int j = 0; j < MT; ++j)
-            *reinterpret_cast<uint4 *>(&Xs[r0 + 16 * j][8 * seg]) =
-                keep_if(Act::to_bf16(xraw[j]), x_in && xok[j]);
-        __syncthreads();
-        if (b + 1 < nb) load(kblk(b + 1));
-#pragma unroll
-        for (int q = 0; q < kKB / 32; ++q) {
-            const int kc = 32 * q + 8 * (lane >> 4);
-            uint4 wop[NW];
-#pragma unroll
-            for (int m = 0; m < NW; ++m)
-                wop[m] = *reinterpret_cast<const uint4 *>(&Ws[m][16 * wave + (lane & 15)][kc]);
-#pragma unroll
-            for (int tt = 0; tt < MT; ++tt) {
-                const uint4 xop = *reinterpret_cast<const uint4 *>(&Xs[16 * tt + (lane & 15)][kc]);
-#pragma unroll
-                for (int m = 0; m < NW; ++m)
-                    acc[m][tt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        as_bf16x8(xop), as_bf16x8(wop[m]), acc[m][tt], 0, 0, 0);
-            }
-        }
+        return (b_lo + (q >= nb ? q - nb : q)) * kb;
     }
+};
+
+__device__ __forceinline__ KBlocks k_blocks(int K, int kb, int splits, int z) {
+    const int n = (K + kb - 1) / kb;
+    KBlocks r;
+    r.b_lo = z * n / splits;
+    r.nb = (z + 1) * n / splits - r.b_lo;
+    r.kb = kb;
+    r.rot = int((blockIdx.x * 7u + blockIdx.y * 13u) % unsigned(r.nb > 0 ? r.nb : 1));
+    return r;
 }
 
-__device__ __forceinline__ void split_range(int K, int kb, int splits, int z, int &b_lo,
-                                            int &b_hi) {
-    const int nb = (K + kb - 1) / kb;
-    b_lo = z * nb / splits;
-    b_hi = (z + 1) * nb / splits;
-}
-
-// LDS of one workgroup's tile: bf16 weights and activations for gemm_mainloop; codes,
-// MXFP4 block scales and activations for gemm_mainloop_codes.  Rows are padded by 16
+// LDS of one workgroup's tile: bf16 weights and activations for bf16 slots; codes, MXFP4
+// block scales and activations for the compact formats.  Rows are padded by 16
 // bytes so that the 16 rows of a fragment read fall in distinct banks.
 template <int NW, int MT, class WF, bool C = WF::kCodes>
 struct GemmLds {
@@ -312,59 +242,130 @@ __device__ __forceinline__ uint4 widen8(const GemmLds<NW, MT, WF, true> &lds, in
     }
 }
 
-// Mainloop for the compact formats (E4M3, MXFP4).  Same tile and MFMA work as
-// gemm_mainloop, but a K block holds as many weight bytes as a bf16 block (KB = 256 or
-// 512 values), its codes go to LDS unchanged (with the MXFP4 block scales beside them),
-// and each wavefront widens its own fragments right before the matrix cores take them:
-// every code is still converted once, while the bytes in flight per block match bf16
-// and the LDS moves a fraction of the widened data.
-template <int NW, int MT, class Act, class WF>
-__device__ __forceinline__ void gemm_mainloop_codes(
-    const uint8_t *const (&wbase)[NW], size_t wstride, const uint8_t *const (&sbase)[NW],
-    size_t sstride, int rows_valid, int K, int b_lo, int b_hi, const void *const (&xrow)[MT],
-    const bool (&xok)[MT], GemmLds<NW, MT, WF, true> &lds, floatx4 (&acc)[NW][MT]) {
+// One K block of a tile's weights in registers: every address valid (rows and K
+// clamped), pieces outside the tile zeroed when the block is staged in LDS, not when it
+// arrives, so that the loads stay in flight until then.
+// bf16 slots: 16 threads per 256-byte piece of a row, 16 rows per pass of 256 threads.
+template <int NW, int MT, class WF, bool C = WF::kCodes>
+struct WRegs {
+    static constexpr int kLoads = WBf16::kLoads, kRpp = WBf16::kRowsPerPass,
+                         kTpr = WBf16::kThrPerRow;
+    uint4 v[NW][kLoads];
+    bool in = false;
+    __device__ __forceinline__ void load(const uint16_t *const (&wbase)[NW], size_t wstride,
+                                         const uint8_t *const (&)[NW], size_t, int rows_valid,
+                                         int K, int k0) {
+        const int t = threadIdx.x, wseg = t % kTpr, wr0 = t / kTpr;
+        const int wk = k0 + 8 * wseg;
+        in = wk < K;
+        const int wkc = in ? wk : K - 8;
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j) {
+                const int row = wr0 + kRpp * j;
+                const int rc = row < rows_valid ? row : rows_valid - 1;
+                v[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + wkc);
+            }
+    }
+    __device__ __forceinline__ void stage(GemmLds<NW, MT, WF> &lds, int rows_valid) const {
+        const int t = threadIdx.x, wseg = t % kTpr, wr0 = t / kTpr;
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int j = 0; j < kLoads; ++j) {
+                const int row = wr0 + kRpp * j;
+                *reinterpret_cast<uint4 *>(&lds.Ws[m][row][8 * wseg]) =
+                    keep_if(v[m][j], in && row < rows_valid);
+            }
+    }
+};
+
+// E4M3 and MXFP4 slots: the codes (and MXFP4 block scales) as stored, RB bytes per row
+// and block.
+template <int NW, int MT, class WF>
+struct WRegs<NW, MT, WF, true> {
     using L = GemmLds<NW, MT, WF, true>;
-    constexpr int KB = L::KB, RB = L::RB;
-    constexpr int TPR = RB / 16;              // threads per row of a block
-    constexpr int RPP = kThreads / TPR;       // rows per pass
-    constexpr int NL = kRows / RPP;           // 16-byte weight loads per thread and matrix
-    constexpr int QX = KB / 128;              // 8-value activation pieces per token row
-    constexpr int KPL = 16 * WF::kKPerElem;   // K values per 16-byte load
-    const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
-    const int wseg = t % TPR, wr0 = t / TPR;
-    const int seg = t & 15, r0 = t >> 4;
-    uint4 wreg[NW][NL];
-    uint32_t sreg[NW][NL];
-    typename Act::Raw xraw[QX][MT];
-    bool w_in = false, x_in[QX];   // K range of the block held in the registers
-#pragma unroll
-    for (int m = 0; m < NW; ++m)
-#pragma unroll
-        for (int tt = 0; tt < MT; ++tt) acc[m][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const int nb = b_hi - b_lo;
-    if (nb <= 0) return;
-    const int rot = int((blockIdx.x * 7u + blockIdx.y * 13u) % unsigned(nb));
-    const auto kblk = [nb, rot, b_lo](int b) {
-        const int q = b + rot;
-        return (b_lo + (q >= nb ? q - nb : q)) * KB;
-    };
-    // One block into registers: every address valid (rows and K clamped, padding token
-    // rows read a real row); pieces outside the tile are zeroed at staging, as in
-    // gemm_mainloop, so that the loads stay in flight across the matrix-core work.
-    const auto load = [&](int k0) {
+    static constexpr int TPR = L::RB / 16;          // threads per row of a block
+    static constexpr int RPP = kThreads / TPR;      // rows per pass
+    static constexpr int NL = kRows / RPP;          // 16-byte loads per thread and matrix
+    static constexpr int KPL = 16 * WF::kKPerElem;  // K values per 16-byte load
+    uint4 v[NW][NL];
+    uint32_t sc[NW][NL];
+    bool in = false;
+    __device__ __forceinline__ void load(const uint8_t *const (&wbase)[NW], size_t wstride,
+                                         const uint8_t *const (&sbase)[NW], size_t sstride,
+                                         int rows_valid, int K, int k0) {
+        const int t = threadIdx.x, wseg = t % TPR, wr0 = t / TPR;
         const int wk = k0 + KPL * wseg;
-        w_in = wk < K;
-        const int wkc = w_in ? wk : K - KPL;
+        in = wk < K;
+        const int wkc = in ? wk : K - KPL;
 #pragma unroll
         for (int m = 0; m < NW; ++m)
 #pragma unroll
             for (int j = 0; j < NL; ++j) {
                 const int row = wr0 + RPP * j;
                 const int rc = row < rows_valid ? row : rows_valid - 1;
-                wreg[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
-                                                              wkc / WF::kKPerElem);
-                if constexpr (WF::kBlockScale) sreg[m][j] = sbase[m][size_t(rc) * sstride + wkc / 32];
+                v[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
+                                                           wkc / WF::kKPerElem);
+                if constexpr (WF::kBlockScale) sc[m][j] = sbase[m][size_t(rc) * sstride + wkc / 32];
             }
+    }
+    __device__ __forceinline__ void stage(L &lds, int rows_valid) const {
+        const int t = threadIdx.x, wseg = t % TPR, wr0 = t / TPR;
+#pragma unroll
+        for (int m = 0; m < NW; ++m)
+#pragma unroll
+            for (int j = 0; j < NL; ++j) {
+                const int row = wr0 + RPP * j;
+                *reinterpret_cast<uint4 *>(&lds.Wc[m][row][16 * wseg]) =
+                    keep_if(v[m][j], in && row < rows_valid);
+                if constexpr (WF::kBlockScale) lds.Sc[m][row][wseg] = uint8_t(sc[m][j]);
+            }
+    }
+};
+
+// Grouped-GEMM mainloop, shared by the gate/up and down projections and the weight
+// formats.  A workgroup (4 wavefronts) owns a tile of 64 weight rows of NW weight
+// matrices and up to 16*MT tokens, over the K blocks of kr.  Every thread loads 16-byte
+// pieces so that each group of threads reads whole cache lines of one weight row, the
+// block goes to LDS, and while the matrix cores work on it the next block is already
+// loading into registers: every load address is valid (padding token rows read a real
+// row), and zeroing and the fp32-to-bf16 conversion of activations happen at staging,
+// so the first use of a loaded register comes after the matrix-core work on the previous
+// block.  `w` may already hold the first block (w_ready): the kernels issue it before
+// they look up the expert's pairs.
+// bf16 slots: K blocks of kKB values as bf16 tiles.  E4M3 and MXFP4 slots: a block holds
+// as many code bytes per row as a bf16 block (256 or 512 K values with one token tile,
+// 128 or 256 with more), the codes go to LDS unchanged (the MXFP4 block scales beside
+// them), and each wavefront widens its own fragments right before the matrix cores take
+// them: every code is converted once, the bytes in flight per block match bf16, and the
+// LDS moves a fraction of the widened data.
+// Wavefront w multiplies its 16 rows with every token tile: v_mfma_f32_16x16x32_bf16,
+// tokens as M, weight rows as N.  Tiles past the expert's last token multiply zero rows:
+// skipping them on the token count made the compiler move the accumulators between
+// register files around the skip, and the E4M3 kernel with two tiles then gave wrong
+// sums that changed from run to run.
+template <int NW, int MT, class Act, class WF>
+__device__ __forceinline__ void gemm_tile(WRegs<NW, MT, WF> &w, bool w_ready,
+                                          const typename WF::T *const (&wbase)[NW],
+                                          size_t wstride, const uint8_t *const (&sbase)[NW],
+                                          size_t sstride, int rows_valid, int K,
+                                          const KBlocks &kr, const void *const (&xrow)[MT],
+                                          const bool (&xok)[MT], GemmLds<NW, MT, WF> &lds,
+                                          floatx4 (&acc)[NW][MT]) {
+    constexpr int KB = WF::template kb<MT>();
+    constexpr int QX = KB / 128;   // 8-value activation pieces per token row and thread
+    const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
+    const int seg = t & 15, r0 = t >> 4;
+    typename Act::Raw xraw[QX][MT];
+    bool x_in[QX];
+#pragma unroll
+    for (int m = 0; m < NW; ++m)
+#pragma unroll
+        for (int tt = 0; tt < MT; ++tt) acc[m][tt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (kr.nb <= 0) return;
+    const auto load_x = [&](int k0) {
 #pragma unroll
         for (int q = 0; q < QX; ++q) {
             const int kk = k0 + 128 * q + 8 * seg;
@@ -374,18 +375,11 @@ __device__ __forceinline__ void gemm_mainloop_codes(
             for (int j = 0; j < MT; ++j) xraw[q][j] = Act::load(xrow[j], kc);
         }
     };
-    load(kblk(0));
-    for (int b = 0; b < nb; ++b) {
+    if (!w_ready) w.load(wbase, wstride, sbase, sstride, rows_valid, K, kr.k0(0));
+    load_x(kr.k0(0));
+    for (int b = 0; b < kr.nb; ++b) {
         __syncthreads();   // the previous block's fragments have been read
-#pragma unroll
-        for (int m = 0; m < NW; ++m)
-#pragma unroll
-            for (int j = 0; j < NL; ++j) {
-                const int row = wr0 + RPP * j;
-                *reinterpret_cast<uint4 *>(&lds.Wc[m][row][16 * wseg]) =
-                    keep_if(wreg[m][j], w_in && row < rows_valid);
-                if constexpr (WF::kBlockScale) lds.Sc[m][row][wseg] = uint8_t(sreg[m][j]);
-            }
+        w.stage(lds, rows_valid);
 #pragma unroll
         for (int q = 0; q < QX; ++q)
 #pragma unroll
@@ -393,14 +387,22 @@ __device__ __forceinline__ void gemm_mainloop_codes(
                 *reinterpret_cast<uint4 *>(&lds.Xs[r0 + 16 * j][128 * q + 8 * seg]) =
                     keep_if(Act::to_bf16(xraw[q][j]), x_in[q] && xok[j]);
         __syncthreads();
-        if (b + 1 < nb) load(kblk(b + 1));
+        if (b + 1 < kr.nb) {
+            w.load(wbase, wstride, sbase, sstride, rows_valid, K, kr.k0(b + 1));
+            load_x(kr.k0(b + 1));
+        }
         const int rr = 16 * wave + (lane & 15);
 #pragma unroll 4
         for (int q = 0; q < KB / 32; ++q) {
             const int kc = 32 * q + 8 * (lane >> 4);
             uint4 wop[NW];
 #pragma unroll
-            for (int m = 0; m < NW; ++m) wop[m] = widen8(lds, m, rr, kc);
+            for (int m = 0; m < NW; ++m) {
+                if constexpr (WF::kCodes)
+                    wop[m] = widen8(lds, m, rr, kc);
+                else
+                    wop[m] = *reinterpret_cast<const uint4 *>(&lds.Ws[m][rr][kc]);
+            }
 #pragma unroll
             for (int tt = 0; tt < MT; ++tt) {
                 const uint4 xop = *reinterpret_cast<const uint4 *>(&lds.Xs[16 * tt + (lane & 15)][kc]);
@@ -411,22 +413,6 @@ __device__ __forceinline__ void gemm_mainloop_codes(
             }
         }
     }
-}
-
-// The tile's mainloop for weight format WF.
-template <int NW, int MT, class Act, class WF>
-__device__ __forceinline__ void gemm_tile(const typename WF::T *const (&wbase)[NW],
-                                          size_t wstride, const uint8_t *const (&sbase)[NW],
-                                          size_t sstride, int rows_valid, int K, int b_lo,
-                                          int b_hi, const void *const (&xrow)[MT],
-                                          const bool (&xok)[MT], GemmLds<NW, MT, WF> &lds,
-                                          floatx4 (&acc)[NW][MT]) {
-    if constexpr (WF::kCodes)
-        gemm_mainloop_codes<NW, MT, Act, WF>(wbase, wstride, sbase, sstride, rows_valid, K,
-                                             b_lo, b_hi, xrow, xok, lds, acc);
-    else
-        gemm_mainloop<NW, MT, Act>(wbase, wstride, rows_valid, K, b_lo, b_hi, xrow, xok,
-                                   lds.Ws, lds.Xs, acc);
 }
 
 // The fp32 row scales of an apex_pack_expert_fp8 slot: W1 rows, W3 rows, W2 rows.
@@ -449,23 +435,30 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
     float *__restrict__ uv) {
     __shared__ __align__(16) GemmLds<2, MT, WF> lds;
     __shared__ int list[APEX_MAX_PAIRS];
-    __shared__ int cnt[APEX_MAX_PAIRS / kThreads][4];
+    __shared__ int cnt[kPairRounds][4];
     const int e = blockIdx.y;
     const int s = slot_of_expert[e];
     if (s < 0 || s >= n_slots) return;
+    int ev[kPairRounds];
+    pair_ids(exec_idx, P, ev);
     const int i0 = blockIdx.x * kRows;
-    const int n_e = expert_pairs(exec_idx, P, e, list, cnt);
-    if (n_e == 0) return;
-    int b_lo, b_hi;
-    split_range(d, WF::template kb<MT>(), gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const typename WF::T *slot = slots + size_t(s) * slot_stride;
     const typename WF::T *W = slot + size_t(i0) * 2 * d / WF::kKPerElem;
     const typename WF::T *const wbase[2] = {W, W + d / WF::kKPerElem};
+    const size_t wstride = size_t(2) * d / WF::kKPerElem;
     // MXFP4 block scales of W1 and W3 rows i0.. (unused by the other formats)
     const uint8_t *sc = reinterpret_cast<const uint8_t *>(slot) + size_t(3) * I * d / 2;
     const uint8_t *const sbase[2] = {sc + size_t(i0) * (d / 32),
                                      sc + size_t(I + i0) * (d / 32)};
+    const KBlocks kr = k_blocks(d, WF::template kb<MT>(), gridDim.z, blockIdx.z);
+    // The first block's weights load while the expert's pairs are looked up, with no
+    // branch in between (an empty split loads a clamped, valid block and drops it): at
+    // the join after a branch the compiler would wait for the weights before the scan.
+    WRegs<2, MT, WF> w;
+    w.load(wbase, wstride, sbase, size_t(d / 32), I - i0, d, kr.k0(0));
+    const int n_e = expert_pairs(ev, P, e, list, cnt);
+    if (n_e == 0) return;
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
         const void *xrow[MT];
         bool xok[MT];
@@ -476,8 +469,8 @@ __global__ __launch_bounds__(kThreads) void up_gemm(
             xrow[j] = x + size_t(list[xok[j] ? tok : 0] / k) * d;
         }
         floatx4 acc[2][MT];
-        gemm_tile<2, MT, ActF32, WF>(wbase, size_t(2) * d / WF::kKPerElem, sbase,
-                                     size_t(d / 32), I - i0, d, b_lo, b_hi, xrow, xok, lds, acc);
+        gemm_tile<2, MT, ActF32, WF>(w, t0 == 0, wbase, wstride, sbase, size_t(d / 32), I - i0,
+                                     d, kr, xrow, xok, lds, acc);
         const int i = i0 + 16 * wave + (lane & 15);
         float s1 = 1.f, s3 = 1.f;
         if constexpr (WF::kFp8) {
@@ -516,22 +509,27 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
     float *__restrict__ yp) {
     __shared__ __align__(16) GemmLds<1, MT, WF> lds;
     __shared__ int list[APEX_MAX_PAIRS];
-    __shared__ int cnt[APEX_MAX_PAIRS / kThreads][4];
+    __shared__ int cnt[kPairRounds][4];
     const int e = blockIdx.y;
     const int s = slot_of_expert[e];
     if (s < 0 || s >= n_slots) return;
+    int ev[kPairRounds];
+    pair_ids(exec_idx, P, ev);
     const int j0 = blockIdx.x * kRows;
-    const int n_e = expert_pairs(exec_idx, P, e, list, cnt);
-    if (n_e == 0) return;
-    int b_lo, b_hi;
-    split_range(I, WF::template kb<MT>(), gridDim.z, blockIdx.z, b_lo, b_hi);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const typename WF::T *slot = slots + size_t(s) * slot_stride;
     const typename WF::T *const wbase[1] = {
         slot + (size_t(2) * I * d + size_t(j0) * I) / WF::kKPerElem};
+    const size_t wstride = size_t(I) / WF::kKPerElem;
     const uint8_t *const sbase[1] = {reinterpret_cast<const uint8_t *>(slot) +
                                      size_t(3) * I * d / 2 + size_t(2) * I * (d / 32) +
                                      size_t(j0) * (I / 32)};
+    const KBlocks kr = k_blocks(I, WF::template kb<MT>(), gridDim.z, blockIdx.z);
+    // the first block's weights load while the expert's pairs are looked up (as in up_gemm)
+    WRegs<1, MT, WF> w;
+    w.load(wbase, wstride, sbase, size_t(I / 32), d - j0, I, kr.k0(0));
+    const int n_e = expert_pairs(ev, P, e, list, cnt);
+    if (n_e == 0) return;
     float *out = yp + size_t(blockIdx.z) * P * d;
     for (int t0 = 0; t0 < n_e; t0 += 16 * MT) {
         const void *hrow[MT];
@@ -543,9 +541,8 @@ __global__ __launch_bounds__(kThreads) void down_gemm(
             hrow[j] = hb + size_t(list[hok[j] ? tok : 0]) * I;
         }
         floatx4 acc[1][MT];
-        gemm_tile<1, MT, ActBf16, WF>(wbase, size_t(I) / WF::kKPerElem, sbase,
-                                      size_t(I / 32), d - j0, I, b_lo, b_hi, hrow, hok, lds,
-                                      acc);
+        gemm_tile<1, MT, ActBf16, WF>(w, t0 == 0, wbase, wstride, sbase, size_t(I / 32), d - j0,
+                                      I, kr, hrow, hok, lds, acc);
         const int j = j0 + 16 * wave + (lane & 15);
         float s2 = 1.f;
         if constexpr (WF::kFp8) s2 = j < d ? row_scales<WF>(slot, d, I)[2 * I + j] : 0.f;
