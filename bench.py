@@ -68,6 +68,8 @@ def parse():
     p.add_argument("--no-compute-only", action="store_true",
                    help="skip the all-resident run that the exposed stall is measured against")
     p.add_argument("--cpu-budget-s", type=float, default=15.0)
+    p.add_argument("--cpu-1thread-budget-s", type=float, default=6.0,
+                   help="seconds of the oracle under one BLAS thread (0: skip)")
     return p.parse_args()
 
 
@@ -235,9 +237,13 @@ def measured_traffic(cfg, batch, weights="bf16"):
 
 
 def time_steps(torch, runner, steps, warmup):
-    """Runs warmup untimed steps, then times `steps` decode steps; ms per step."""
+    """Runs warmup untimed steps, then times `steps` decode steps; ms per step.  The
+    metrics of the warm-up steps alone (cold cache first) are kept in
+    runner.warmup_summary; the runner's own metrics then cover the timed steps only."""
     for _ in range(warmup):
         runner.step()
+    runner.finish()
+    runner.warmup_summary = runner.summary() if warmup else None
     runner.reset_metrics()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -273,33 +279,48 @@ def delta_star_leg(cfg, tokens=256, max_layers=8):
 
 
 def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=None,
-                 weights="bf16"):
-    """The oracle, as it stands, on the first layer-steps of the same workload."""
+                 weights="bf16", threads_limit=None):
+    """The oracle, as it stands, on the first layer-steps of the same workload; with
+    threads_limit, under that many BLAS threads.  Also counts the near ties the oracle
+    finds in the sample (decision margins below 1e-5 at the gate's top-k cut and at the
+    prefetch selection's cut), the points where a GPU set may differ legitimately."""
     from oracle import decode
+    import contextlib
     try:
         import threadpoolctl
-        threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()),
-                      default=1)
+        limit = (threadpoolctl.threadpool_limits(threads_limit) if threads_limit
+                 else contextlib.nullcontext())
     except Exception:
-        threads = 1
+        threadpoolctl, limit = None, contextlib.nullcontext()
     layers = list(range(min(cfg.L, 4)))
     steps = 64
-    gen = decode.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers, policy=policy,
-                     static_delta=static_delta, cdf=cdf, weights=weights)
-    # timed as the oracle runs: its seeded input generation is inside the sample
-    n, elapsed = 0, 0.0
-    it = iter(gen)
-    t0 = time.perf_counter()
-    for t, l, out in it:
-        n += 1
-        elapsed = time.perf_counter() - t0
-        if elapsed > budget_s:
-            break
-    return dict(value=elapsed * 1e6 / (n * batch), unit="us/token/layer", cores=int(threads),
+    n, elapsed, gate_ties, cut_ties, rows = 0, 0.0, 0, 0, 0
+    with limit:
+        threads = 1
+        if threadpoolctl is not None:
+            threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()),
+                          default=1)
+        gen = decode.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers, policy=policy,
+                         static_delta=static_delta, cdf=cdf, weights=weights)
+        # timed as the oracle runs: its seeded input generation is inside the sample
+        it = iter(gen)
+        t0 = time.perf_counter()
+        for t, l, out in it:
+            n += 1
+            gate_ties += int((out["gate"]["margin"] < 1e-5).sum())
+            cut_ties += int((out["route"]["margin"] < 1e-5).sum())
+            rows += len(out["gate"]["margin"])
+            elapsed = time.perf_counter() - t0
+            if elapsed > budget_s:
+                break
+    base = dict(value=elapsed * 1e6 / (n * batch), unit="us/token/layer", cores=int(threads),
                 kind="oracle",
                 sample=f"{cfg.name} batch {batch} {['exact', 'stall_free'][mode]} mode, first {n} "
                        f"layer-steps (layers {layers[0]}-{layers[-1]}, steps from 0), fp64 "
                        f"NumPy, includes seeded weight generation of the experts it touches")
+    ties = dict(token_layers=rows, gate_cut=gate_ties, prefetch_cut=cut_ties, margin_below=1e-5,
+                sample=f"the oracle's {n} layer-steps above")
+    return base, ties
 
 
 def main():
@@ -345,6 +366,7 @@ def main():
     S = runner.S
     achieved = leg_bytes / (leg_ms * 1e-3) / 1e9
     s = runner.summary()
+    warm = runner.warmup_summary
     copied_bytes_per_step = s["copies_per_layer_step"] * L * S
     runner.close()
     # exposed stall: this timeline against the same one with every expert resident
@@ -365,9 +387,10 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": {"fp8": "fp8 e4m3 weights with fp32 row scales, fp32 accumulate",
-                  "mxfp4": "mxfp4 (e2m1, e8m0 block scales) weights, fp32 accumulate",
-                  "bf16": "bf16 weights, fp32 accumulate"}[args.weights],
+        "dtype": {"fp8": "fp8-e4m3", "mxfp4": "mxfp4", "bf16": "bf16"}[args.weights],
+        "arithmetic": {"fp8": "fp8 e4m3 weights with fp32 row scales, fp32 accumulate",
+                       "mxfp4": "mxfp4 (e2m1, e8m0 block scales) weights, fp32 accumulate",
+                       "bf16": "bf16 weights, fp32 accumulate"}[args.weights],
         "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) bf16 experts)",
         "config": {"workload": cfg.name, "layers": L, "d": cfg.d, "E": cfg.E, "k": cfg.k,
                    "I": cfg.I, "C": cfg.C, "k_max": cfg.k_max, "tau": tau, "batch": B,
@@ -386,6 +409,12 @@ def main():
         "copies_per_layer_step": round(s["copies_per_layer_step"], 4),
         "copied_MB_per_layer_step": round(s["copies_per_layer_step"] * S / 1e6, 3),
         "misses_per_layer_step": round(s["misses_per_layer_step"], 4),
+        "warmup_cold_cache": None if warm is None else {
+            "steps": args.warmup, "recall": round(warm["recall"], 5),
+            "full_coverage": round(warm["full_coverage"], 5),
+            "cache_hit_rate": round(warm["hit_rate"], 5),
+            "copies_per_layer_step": round(warm["copies_per_layer_step"], 4),
+            "misses_per_layer_step": round(warm["misses_per_layer_step"], 4)},
         "compute_only_us_per_token_layer": (None if value_resident is None
                                             else round(value_resident, 3)),
         "exposed_stall_us_per_token_layer": None if stall is None else round(stall, 3),
@@ -410,8 +439,12 @@ def main():
     if cdf_report is not None:
         out["ordinal_fit"] = cdf_report
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, B, mode, tau, args.cpu_budget_s, policy,
-                                           args.static_delta, cdf, args.weights)
+        out["cpu_baseline"], out["oracle_near_ties"] = cpu_baseline(
+            cfg, B, mode, tau, args.cpu_budget_s, policy, args.static_delta, cdf, args.weights)
+        if args.cpu_1thread_budget_s > 0:
+            out["cpu_baseline_1thread"], _ = cpu_baseline(
+                cfg, B, mode, tau, args.cpu_1thread_budget_s, policy, args.static_delta, cdf,
+                args.weights, threads_limit=1)
     print(json.dumps(out), flush=True)
     return 0
 
