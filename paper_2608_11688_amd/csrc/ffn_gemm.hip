@@ -4,10 +4,12 @@
 // up_gemm and down_gemm take tokens as the M dimension (tiles of 16, padded), weight
 // rows as N and the hidden / intermediate dimension as K, with v_mfma_f32_16x16x32_bf16
 // (activations rounded to bf16, fp32 accumulation).  A workgroup owns 64 weight rows of
-// one expert (blockIdx.y is the expert id; experts without a slot or without tokens exit
-// at once) and finds that expert's (token, position) pairs itself from exec_idx, in pair
-// order.  When a projection has too few row tiles to keep the chip's loads in flight, its
-// K range is split over blockIdx.z and each split writes fp32 partial sums:
+// one expert (blockIdx.y is the expert id; experts without a slot exit at once) and
+// finds that expert's (token, position) pairs itself from exec_idx, in pair order, while
+// its first weight block loads (an expert without tokens then exits and drops that
+// block).  When a projection has too few row tiles to keep the chip's loads in flight
+// (plan_for), its K range is split over blockIdx.z and each split writes fp32 partial
+// sums:
 //   * up_gemm with one split writes h = bf16(silu(W1 x) * (W3 x)) per pair; with several
 //     it writes the partial W1 x and W3 x, and swiglu_reduce adds them (in split order)
 //     into the same bf16 h, once, before down_gemm reads it from every row tile;
