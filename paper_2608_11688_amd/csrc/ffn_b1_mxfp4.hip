@@ -194,8 +194,10 @@ apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32
                            exec_idx, slot_of_expert, slots, n_slots, slot_bytes, h, y,
                            accumulate);
     } else {
-        const dim3 gu(I / 8 + (I % 8 != 0), k);
-        hipLaunchKernelGGL((up_b1_mxfp4<4, 2, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
+        // one row per wavefront: 2 rows took 178 VGPRs (2 wavefronts per SIMD) and left the
+        // conversions and the loads of a wavefront little to overlap with
+        const dim3 gu(I / 4 + (I % 4 != 0), k);
+        hipLaunchKernelGGL((up_b1_mxfp4<4, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
                            exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_bytes, h);
         APEX_HIP(hipGetLastError());
         hipLaunchKernelGGL((down_b1_mxfp4<4, 4, 4>), dim3(d / 16 + (d % 16 != 0)), dim3(256), 0,
