@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "common.h"
+#include "route_internal.h"
 
 struct apex_decode {
     apex_decode_config cfg;
@@ -38,6 +39,11 @@ struct apex_decode {
     int32_t *pf_count_h = nullptr;    // [B]
     int32_t *route_idx_h = nullptr;   // [L][B][k]
     float *route_gate_h = nullptr;    // [L][B][k]
+    // completion flags the router and gate kernels write into pinned memory after their
+    // outputs: route_done[b], gate_done_h[l][b] = the layer-step's sequence number
+    int32_t *route_done = nullptr;    // [B]
+    int32_t *gate_done_h = nullptr;   // [L][B]
+    int32_t seq = 0;
     // events
     hipEvent_t ev_route = nullptr, ready_miss = nullptr, scratch_free = nullptr;
     std::vector<hipEvent_t> ready, readers_done, gate_done;
@@ -54,18 +60,26 @@ struct apex_decode {
 
 namespace {
 
-// Busy-polls an event (lower wake-up latency than a blocking wait); gives up after
-// 30 s so that a device that stopped making progress surfaces as an error.
-apex_status poll(hipEvent_t ev) {
+// Waits until the kernel enqueued before `ev` has published its outputs: every done[b]
+// equals seq (the kernel writes them after its outputs, behind a system-scope fence), or
+// the event completed, whichever the host sees first; the flags arrive before the
+// completion signal.  Busy-polls (lower wake-up latency than a blocking wait) and gives
+// up after 30 s, so that a device that stopped making progress surfaces as an error.
+apex_status poll_done(const int32_t *done, int n, int32_t seq, hipEvent_t ev) {
     const auto t0 = std::chrono::steady_clock::now();
     for (unsigned it = 0;; ++it) {
-        const hipError_t e = hipEventQuery(ev);
-        if (e == hipSuccess) return APEX_OK;
-        if (e != hipErrorNotReady)
-            return apex::fail(APEX_E_HIP, "hipEventQuery failed: %s", hipGetErrorString(e));
-        if ((it & 1023u) == 1023u &&
-            std::chrono::steady_clock::now() - t0 > std::chrono::seconds(30))
-            return apex::fail(APEX_E_HIP, "apex_decode_step: event not reached after 30 s");
+        bool all = true;
+        for (int b = 0; b < n && all; ++b)
+            all = __atomic_load_n(done + b, __ATOMIC_ACQUIRE) == seq;
+        if (all) return APEX_OK;
+        if ((it & 255u) == 255u) {
+            const hipError_t e = hipEventQuery(ev);
+            if (e == hipSuccess) return APEX_OK;
+            if (e != hipErrorNotReady)
+                return apex::fail(APEX_E_HIP, "hipEventQuery failed: %s", hipGetErrorString(e));
+            if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(30))
+                return apex::fail(APEX_E_HIP, "apex_decode_step: event not reached after 30 s");
+        }
     }
 }
 
@@ -215,6 +229,15 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     if (e == hipSuccess)
         e = hipHostMalloc(reinterpret_cast<void **>(&dec->route_gate_h),
                           sizeof(float) * c.L * c.B * c.k);
+    if (e == hipSuccess)
+        e = hipHostMalloc(reinterpret_cast<void **>(&dec->route_done), sizeof(int32_t) * c.B);
+    if (e == hipSuccess)
+        e = hipHostMalloc(reinterpret_cast<void **>(&dec->gate_done_h),
+                          sizeof(int32_t) * c.L * c.B);
+    if (e == hipSuccess) {
+        std::fill(dec->route_done, dec->route_done + c.B, 0);
+        std::fill(dec->gate_done_h, dec->gate_done_h + size_t(c.L) * c.B, 0);
+    }
     if (e != hipSuccess)
         return cleanup(apex::fail(APEX_E_HIP, "%s: hipHostMalloc failed: %s", fn,
                                   hipGetErrorString(e)));
@@ -279,10 +302,14 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         // prefetch stage: router on the pre-attention state, then the attention window
         // (the no-prefetch baseline has no router: its prefetched sets are empty)
         const bool route = c.policy != APEX_SEL_NONE;
+        // sequence number of this layer-step (never 0, the flags' initial value)
+        dec->seq = dec->seq == INT32_MAX ? 1 : dec->seq + 1;
+        const int32_t seq = dec->seq;
         if (route) {
-            st = apex_prefetch_route(h_pre[l], Ly.w_pf, Ly.b_pf, c.B, c.d, c.E, c.k, c.k_max,
-                                     c.policy, c.tau, c.static_delta, Ly.cdf_w, Ly.cdf_theta,
-                                     dec->pf_idx_h, dec->pf_count_h, nullptr, cs);
+            st = apex::prefetch_route(h_pre[l], Ly.w_pf, Ly.b_pf, c.B, c.d, c.E, c.k, c.k_max,
+                                      c.policy, c.tau, c.static_delta, Ly.cdf_w, Ly.cdf_theta,
+                                      dec->pf_idx_h, dec->pf_count_h, nullptr, dec->route_done,
+                                      seq, cs);
             if (st != APEX_OK) return st;
             APEX_HIP(hipEventRecord(dec->ev_route, cs));
         } else {
@@ -300,7 +327,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
             if (st != APEX_OK) return st;
         }
         if (route) {
-            st = poll(dec->ev_route);
+            st = poll_done(dec->route_done, c.B, seq, dec->ev_route);
             if (st != APEX_OK) return st;
         }
         // earlier layers' gates precede this route on the stream: fold their statistics
@@ -336,8 +363,10 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         // execution stage: original router, then the experts once the copies landed
         int32_t *route_h = dec->route_idx_h + size_t(l) * c.B * c.k;
         float *route_g = dec->route_gate_h + size_t(l) * c.B * c.k;
-        st = apex_gate_topk(h_post[l], Ly.w_g, Ly.b_g, c.B, c.d, c.E, c.k, c.mode, Ly.avail_dev,
-                            0, route_h, route_g, dec->exec_idx, dec->exec_gate, nullptr, cs);
+        int32_t *gate_flags = dec->gate_done_h + size_t(l) * c.B;
+        st = apex::gate_topk(h_post[l], Ly.w_g, Ly.b_g, c.B, c.d, c.E, c.k, c.mode,
+                             Ly.avail_dev, 0, route_h, route_g, dec->exec_idx, dec->exec_gate,
+                             nullptr, gate_flags, seq, cs);
         if (st != APEX_OK) return st;
         APEX_HIP(hipEventRecord(dec->gate_done[l], cs));
         // shared experts first: they need no copy, so they run while the copies land
@@ -356,7 +385,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         int n_miss = 0;
         if (c.mode == APEX_MODE_EXACT) {
             // asynchronous miss correction: the resident experts run while misses copy
-            st = poll(dec->gate_done[l]);
+            st = poll_done(gate_flags, c.B, seq, dec->gate_done[l]);
             if (st != APEX_OK) return st;
             st = apex_expert_fetch_misses(Ly.host_experts, dec->scratch, c.n_scratch, c.E, c.C,
                                           dec->expert_bytes, route_h, c.B, c.k,
@@ -412,7 +441,8 @@ extern "C" apex_status apex_decode_destroy(apex_decode *dec) {
         for (hipEvent_t e : *v)
             if (e) (void)hipEventDestroy(e);
     for (void *p : {static_cast<void *>(dec->pf_idx_h), static_cast<void *>(dec->pf_count_h),
-                    static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h)})
+                    static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h),
+                    static_cast<void *>(dec->route_done), static_cast<void *>(dec->gate_done_h)})
         if (p) (void)hipHostFree(p);
     if (dec->attn_ws) (void)hipFree(dec->attn_ws);
     for (void *p : {static_cast<void *>(dec->shared_idx), static_cast<void *>(dec->shared_gate),

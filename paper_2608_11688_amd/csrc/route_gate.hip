@@ -6,11 +6,15 @@
 // dot products with cross-lane shuffles.  Softmax,
 // ranking and the selection rules then run in wavefront 0 with one lane per expert
 // (E <= 64), exchanging values through registers (readlane, shuffles, ballots).
+// Optionally each token's workgroup then writes `seq` into done[token], after its
+// outputs and a system-scope fence, so that a host polling pinned memory learns that the
+// outputs are there before the kernel's completion signal reaches it.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 
 #include "common.h"
+#include "route_internal.h"
 
 namespace {
 
@@ -109,6 +113,14 @@ __device__ __forceinline__ int masked_rank(float z, int E, int lane, unsigned lo
     return r;
 }
 
+// Marks token b's outputs as written: every store of this wavefront first reaches the
+// system (host memory included), then done[b] = seq, written by lane 0 (a vector store).
+__device__ __forceinline__ void signal_done(int32_t *done, int32_t seq, int b, int lane) {
+    if (!done) return;
+    __threadfence_system();
+    if (lane == 0) __hip_atomic_store(done + b, seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 __device__ __forceinline__ float logit_of(float tau) {
     if (tau <= 0.f) return -INFINITY;
     if (tau >= 1.f) return INFINITY;
@@ -120,7 +132,8 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     const float *__restrict__ h_pre, const uint16_t *__restrict__ w_pf,
     const float *__restrict__ b_pf, int d, int E, int k, int k_max, int policy, float tau,
     int static_delta, const float *__restrict__ cdf_w, const float *__restrict__ cdf_theta,
-    int32_t *__restrict__ pf_idx, int32_t *__restrict__ pf_count, float *__restrict__ pf_prob) {
+    int32_t *__restrict__ pf_idx, int32_t *__restrict__ pf_count, float *__restrict__ pf_prob,
+    int32_t *__restrict__ done, int32_t seq) {
     __shared__ float z_lds[APEX_MAX_EXPERTS];
     __shared__ float sorted_q[APEX_MAX_EXPERTS];
     __shared__ int sorted_id[APEX_MAX_EXPERTS];
@@ -173,6 +186,7 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     if (lane < k_max) pf_idx[size_t(b) * k_max + lane] = lane < m ? sorted_id[lane] : -1;
     if (lane == 0) pf_count[b] = m;
     if (pf_prob && live) pf_prob[size_t(b) * E + lane] = q;
+    signal_done(done, seq, b, lane);
 }
 
 template <int NC, int EPP>
@@ -181,7 +195,8 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     const float *__restrict__ b_g, int d, int E, int k, int mode,
     const uint8_t *__restrict__ avail, int avail_stride, int32_t *__restrict__ route_idx,
     float *__restrict__ route_gate, int32_t *__restrict__ exec_idx,
-    float *__restrict__ exec_gate, float *__restrict__ gate_prob) {
+    float *__restrict__ exec_gate, float *__restrict__ gate_prob, int32_t *__restrict__ done,
+    int32_t seq) {
     __shared__ float z_lds[APEX_MAX_EXPERTS];
 
     const int b = blockIdx.x;
@@ -227,6 +242,7 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
         }
     }
     if (gate_prob && live) gate_prob[size_t(b) * E + lane] = p / psum;
+    signal_done(done, seq, b, lane);
 }
 
 // Shape of token_logits: experts per wavefront (1, 2 or 4 for E <= 16, 32, 64) and
@@ -262,12 +278,13 @@ apex_status check_router_args(const char *fn, const float *h, const uint16_t *w,
 
 }  // namespace
 
-extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w_pf,
-                                           const float *b_pf, int B, int d, int E, int k,
-                                           int k_max, int policy, float tau, int static_delta,
-                                           const float *cdf_w, const float *cdf_theta,
-                                           int32_t *pf_idx, int32_t *pf_count, float *pf_prob,
-                                           hipStream_t stream) {
+namespace apex {
+
+apex_status prefetch_route(const float *h_pre, const uint16_t *w_pf, const float *b_pf, int B,
+                           int d, int E, int k, int k_max, int policy, float tau,
+                           int static_delta, const float *cdf_w, const float *cdf_theta,
+                           int32_t *pf_idx, int32_t *pf_count, float *pf_prob, int32_t *done,
+                           int32_t seq, hipStream_t stream) {
     const char *fn = "apex_prefetch_route";
     apex_status st = check_router_args(fn, h_pre, w_pf, B, d, E, k);
     if (st != APEX_OK) return st;
@@ -287,7 +304,7 @@ extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w
 #define APEX_ROUTE(NC_, EPP_)                                                              \
     hipLaunchKernelGGL((prefetch_route_kernel<NC_, EPP_>), dim3(B), dim3(kThreads), 0, stream,  \
                        h_pre, w_pf, b_pf, d, E, k, k_max, policy, tau, static_delta, cdf_w,    \
-                       cdf_theta, pf_idx, pf_count, pf_prob)
+                       cdf_theta, pf_idx, pf_count, pf_prob, done, seq)
     const LogitShape sh = logit_shape(d, E);
     if (sh.epp == 1) {
         if (sh.nc == 1) APEX_ROUTE(1, 1);
@@ -306,11 +323,10 @@ extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w
     return APEX_OK;
 }
 
-extern "C" apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, const float *b_g,
-                                      int B, int d, int E, int k, int mode,
-                                      const uint8_t *avail, int avail_stride, int32_t *route_idx,
-                                      float *route_gate, int32_t *exec_idx, float *exec_gate,
-                                      float *gate_prob, hipStream_t stream) {
+apex_status gate_topk(const float *h_post, const uint16_t *w_g, const float *b_g, int B, int d,
+                      int E, int k, int mode, const uint8_t *avail, int avail_stride,
+                      int32_t *route_idx, float *route_gate, int32_t *exec_idx, float *exec_gate,
+                      float *gate_prob, int32_t *done, int32_t seq, hipStream_t stream) {
     const char *fn = "apex_gate_topk";
     apex_status st = check_router_args(fn, h_post, w_g, B, d, E, k);
     if (st != APEX_OK) return st;
@@ -326,7 +342,7 @@ extern "C" apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, 
 #define APEX_GATE(NC_, EPP_)                                                               \
     hipLaunchKernelGGL((gate_topk_kernel<NC_, EPP_>), dim3(B), dim3(kThreads), 0, stream,       \
                        h_post, w_g, b_g, d, E, k, mode, avail, avail_stride, route_idx,        \
-                       route_gate, exec_idx, exec_gate, gate_prob)
+                       route_gate, exec_idx, exec_gate, gate_prob, done, seq)
     const LogitShape sh = logit_shape(d, E);
     if (sh.epp == 1) {
         if (sh.nc == 1) APEX_GATE(1, 1);
@@ -343,4 +359,25 @@ extern "C" apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, 
 #undef APEX_GATE
     APEX_HIP(hipGetLastError());
     return APEX_OK;
+}
+
+}  // namespace apex
+
+extern "C" apex_status apex_prefetch_route(const float *h_pre, const uint16_t *w_pf,
+                                           const float *b_pf, int B, int d, int E, int k,
+                                           int k_max, int policy, float tau, int static_delta,
+                                           const float *cdf_w, const float *cdf_theta,
+                                           int32_t *pf_idx, int32_t *pf_count, float *pf_prob,
+                                           hipStream_t stream) {
+    return apex::prefetch_route(h_pre, w_pf, b_pf, B, d, E, k, k_max, policy, tau, static_delta,
+                                cdf_w, cdf_theta, pf_idx, pf_count, pf_prob, nullptr, 0, stream);
+}
+
+extern "C" apex_status apex_gate_topk(const float *h_post, const uint16_t *w_g, const float *b_g,
+                                      int B, int d, int E, int k, int mode,
+                                      const uint8_t *avail, int avail_stride, int32_t *route_idx,
+                                      float *route_gate, int32_t *exec_idx, float *exec_gate,
+                                      float *gate_prob, hipStream_t stream) {
+    return apex::gate_topk(h_post, w_g, b_g, B, d, E, k, mode, avail, avail_stride, route_idx,
+                           route_gate, exec_idx, exec_gate, gate_prob, nullptr, 0, stream);
 }
