@@ -305,16 +305,21 @@ apex_status apex_plan_residency(int E, int C, const int32_t *pf_idx, const int32
  * Prefetch of one layer (Sec. IV-A: asynchronous transfers for K_p issued while
  * attention runs; Sec. V-B prefetch-overlap bound, Eq. 12).
  * Runs apex_plan_residency on the host copy of the route output, then:
- *   side:    wait readers_done (if not NULL and not yet complete); one host-to-device
- *            copy per planned expert, host_experts[e] -> slots[s]; record `ready`;
+ *   side:    wait readers_done (if not NULL and not yet complete); one copy-kernel
+ *            launch that moves every planned expert, host_experts[e] -> slots[s]
+ *            (32 workgroups per expert, reading the pinned copies over PCIe);
+ *            record `ready`;
  *   compute: write the new table to slot_of_expert_dev[E] and, if not NULL, the
  *            resident mask to avail_dev[E] (1 = resident).
  * The caller must make the expert FFN wait for `ready` (apex_stream_wait_event)
  * before it reads the slots (when n_copied is 0 the slots are unchanged and that wait
  * may be left out), and record readers_done on the compute stream after the
  * last kernel that reads this layer's slots.  The host call returns once everything
- * is enqueued; the copies run on the DMA engines.
- *   host_experts      pinned bf16 [E][expert_bytes/2] (apex_pack_expert layout)
+ * is enqueued.
+ *   host_experts      pinned [E][expert_bytes] bytes (apex_pack_expert layout),
+ *                     16-byte aligned; memory the device cannot read (pageable, or a
+ *                     range whose last byte is not in pinned memory) is refused with
+ *                     APEX_E_INVAL before anything changes
  *   slots             device [C][expert_bytes/2]
  *   pf_idx, pf_count  host (pinned or pageable) copies of apex_prefetch_route's output;
  *                     they must be complete when the call is made
@@ -336,7 +341,8 @@ apex_status apex_expert_prefetch(const uint16_t *host_experts, uint16_t *slots,
  * correction): the routed experts of the batch that are not resident,
  *   M = union_b K_r[b] minus {expert_of_slot[s]},
  * in ascending id order, are copied host -> scratch slot i (i = 0..|M|-1) on `side`
- * after waiting for scratch_free (if not NULL), then `ready` is recorded on side.
+ * after waiting for scratch_free (if not NULL), by one launch of the prefetch's copy
+ * kernel, then `ready` is recorded on side.  host_experts follows the prefetch's rules.
  * On `compute`, miss_table_dev[E] is written with miss_table[e] = i for the i-th
  * missing expert and -1 otherwise, so a second apex_moe_ffn pass over the scratch
  * pool with accumulate = 1 adds exactly the missing experts.  If M is empty nothing is

@@ -551,6 +551,55 @@ def test_expert_prefetch_and_miss_fetch(torch):
     native.apex_event_destroy(done)
 
 
+def test_expert_copies_span_strides_and_refuse_pageable_memory(torch):
+    # experts of 1.63 MB: each copy workgroup row walks several strides and a ragged tail
+    d, I, E, C = 1032, 264, 6, 3
+    S = native.apex_expert_bytes(d, I)
+    assert (S // 16) % (32 * 512) != 0
+    rng = np.random.default_rng(21)
+    host = torch.empty(E * S // 2, dtype=torch.int16, pin_memory=True)
+    host.copy_(torch.from_numpy(rng.integers(-30000, 30000, E * S // 2).astype(np.int16)))
+    slots = torch.zeros(C * S // 2, dtype=torch.int16, device="cuda")
+    eos = np.full(C, -1, np.int32)
+    lu = np.full(E, -1, np.int64)
+    slot_dev = torch.full((E,), -1, dtype=torch.int32, device="cuda")
+    side = torch.cuda.Stream()
+    cs, ss = torch.cuda.current_stream().cuda_stream, side.cuda_stream
+    ready = native.apex_event_create(False)
+    pf_idx = np.array([[4, 1, 5, -1]], np.int32)
+    pf_cnt = np.array([3], np.int32)
+    # pageable memory (which a kernel cannot read) is refused before any table changes or
+    # anything is enqueued
+    for bad in (np.zeros(E * S // 2, np.int16),):
+        with pytest.raises(native.ApexError, match="pinned"):
+            native.apex_expert_prefetch(bad, slots, E, C, S, pf_idx, pf_cnt, 1, 4, 0, eos, lu,
+                                        slot_dev, None, ss, cs, None, ready)
+        with pytest.raises(native.ApexError, match="pinned"):
+            native.apex_expert_fetch_misses(bad, slots, C, E, C, S, np.array([[0, 2]], np.int32),
+                                            1, 2, eos, slot_dev, ss, cs, None, ready)
+        assert (eos == -1).all() and (lu == -1).all()
+    n = native.apex_expert_prefetch(host, slots, E, C, S, pf_idx, pf_cnt, 1, 4, 0, eos, lu,
+                                    slot_dev, None, ss, cs, None, ready)
+    assert n == 3
+    native.apex_stream_wait_event(cs, ready)
+    torch.cuda.synchronize()
+    hs, ds = host.view(E, -1), slots.view(C, -1).cpu()
+    assert sorted(eos.tolist()) == [1, 4, 5]
+    for s in range(C):
+        assert torch.equal(ds[s], hs[int(eos[s])]), s
+    # misses: experts 0 and 2 into a scratch pool of 2
+    scratch = torch.zeros(2 * S // 2, dtype=torch.int16, device="cuda")
+    miss_tab = torch.full((E,), -9, dtype=torch.int32, device="cuda")
+    n = native.apex_expert_fetch_misses(host, scratch, 2, E, C, S, np.array([[2, 5, 0]], np.int32),
+                                        1, 3, eos, miss_tab, ss, cs, None, ready)
+    assert n == 2
+    native.apex_stream_wait_event(cs, ready)
+    torch.cuda.synchronize()
+    sc = scratch.view(2, -1).cpu()
+    assert torch.equal(sc[0], hs[0]) and torch.equal(sc[1], hs[2])
+    native.apex_event_destroy(ready)
+
+
 def test_spin_and_copy_kernel(torch):
     s = torch.cuda.current_stream().cuda_stream
     a, b = native.apex_event_create(True), native.apex_event_create(True)
