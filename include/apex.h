@@ -308,14 +308,16 @@ apex_status apex_plan_residency(int E, int C, const int32_t *pf_idx, const int32
  *   side:    wait readers_done (if not NULL and not yet complete); one copy-kernel
  *            launch that moves every planned expert, host_experts[e] -> slots[s]
  *            (32 workgroups per expert, reading the pinned copies over PCIe);
- *            record `ready`;
+ *            record `ready` (if not NULL);
  *   compute: write the new table to slot_of_expert_dev[E] and, if not NULL, the
  *            resident mask to avail_dev[E] (1 = resident).
  * The caller must make the expert FFN wait for `ready` (apex_stream_wait_event)
  * before it reads the slots (when n_copied is 0 the slots are unchanged and that wait
  * may be left out), and record readers_done on the compute stream after the
- * last kernel that reads this layer's slots.  The host call returns once everything
+ * last kernel that reads this layer's slots.  Both events may be NULL when `side` is
+ * the stream that runs the readers: stream order then keeps copies and readers apart.  The host call returns once everything
  * is enqueued.
+ *   expert_bytes      a positive multiple of 16, below 64 GiB
  *   host_experts      pinned [E][expert_bytes] bytes (apex_pack_expert layout),
  *                     16-byte aligned; memory the device cannot read (pageable, or a
  *                     range whose last byte is not in pinned memory) is refused with
@@ -342,7 +344,8 @@ apex_status apex_expert_prefetch(const uint16_t *host_experts, uint16_t *slots,
  *   M = union_b K_r[b] minus {expert_of_slot[s]},
  * in ascending id order, are copied host -> scratch slot i (i = 0..|M|-1) on `side`
  * after waiting for scratch_free (if not NULL), by one launch of the prefetch's copy
- * kernel, then `ready` is recorded on side.  host_experts follows the prefetch's rules.
+ * kernel, then `ready` (if not NULL) is recorded on side.  host_experts follows the
+ * prefetch's rules.
  * On `compute`, miss_table_dev[E] is written with miss_table[e] = i for the i-th
  * missing expert and -1 otherwise, so a second apex_moe_ffn pass over the scratch
  * pool with accumulate = 1 adds exactly the missing experts.  If M is empty nothing is
@@ -366,21 +369,27 @@ apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scr
  * Decode driver: one decode step through every MoE layer, in native code, composed of
  * the entry points above in the order of the paper's two-stage runtime (Sec. IV-A;
  * Sec. IV-D "Runtime Operation"; Sec. IV-E).  Per layer:
- *   compute: apex_prefetch_route (K_p written to pinned host memory); attention-window
- *            stand-in (apex_spin_us, t_attn_us);
- *   host:    poll until the route is done; apex_expert_prefetch (copies on side);
- *   compute: apex_gate_topk; the shared experts, if any (apex_moe_ffn over the layer's
- *            shared pool, every token, weight 1); wait for the copies; apex_moe_ffn
- *            pass 1 (added to the shared experts' output);
- *   EXACT:   host waits for the gate, apex_expert_fetch_misses, and if any expert is
- *            missing: compute waits for it and runs apex_moe_ffn pass 2 (accumulate).
- * Layers are processed in order on the compute stream, so a layer's router starts after
- * the previous layer's FFN, as in a model where each layer feeds the next.
+ *   compute: apex_prefetch_route (K_p written to pinned host memory);
+ *   side:    after the router: attention-window stand-in (apex_spin_us, t_attn_us);
+ *   host:    poll until the route is done; apex_expert_prefetch (the copies on compute,
+ *            the slot table on side);
+ *   side:    apex_gate_topk; the shared experts, if any (apex_moe_ffn over the layer's
+ *            shared pool, every token, weight 1);
+ *   EXACT:   host waits for the gate, apex_expert_fetch_misses (copies on compute);
+ *   compute: after the gate (and the shared experts): apex_moe_ffn pass 1 (added to the
+ *            shared experts' output) and, if any expert was missing, pass 2 (accumulate).
+ * The copies, the FFN and the next layer's router follow each other on the compute
+ * stream with no event between them, so a layer's router starts after the previous
+ * layer's FFN, as in a model where each layer feeds the next, and the copies of a layer
+ * start after every earlier read of its slots.  A layer-step that copies nothing runs
+ * the window, the gate and the shared experts on the compute stream instead.  Work still
+ * running on the side stream when the step returns is waited for by the compute stream,
+ * so synchronizing the compute stream covers the step.
  *
  * Shared experts (n_shared > 0; DeepSeek-style, Sec. V-A) run for every token with
  * weight 1 and stay out of the adaptive decision: they live in a resident pool per layer
  * (shared_slots) and never enter the cache, the prefetch or the miss path.  They run
- * while the routed experts' copies are still in flight.
+ * on the side stream while the routed experts' copies are still in flight.
  *
  * With attn_heads > 0 the attention window is the layer's real decode attention
  * (apex_attention_decode on h_pre, writing position attn_ctx of its caches) instead of
@@ -388,7 +397,8 @@ apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scr
  * their own hidden states).
  *
  * apex_decode_create copies the configuration and the per-layer descriptors (the
- * buffers themselves stay caller-owned and must outlive the driver) and allocates the
+ * buffers themselves stay caller-owned and must outlive the driver; every layer's
+ * host_experts must be pinned, as for apex_expert_prefetch) and allocates the
  * driver's own events, pinned staging, attention workspace and shared-expert lists
  * (setup time, not the hot path).  `workspace` must hold
  * apex_moe_ffn_workspace_bytes for both the routed (I, k) and the shared (I_shared,

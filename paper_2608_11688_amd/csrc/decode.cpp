@@ -2,9 +2,25 @@
 //
 // The host only has to see the prefetched set (to plan and issue the copies) and, in
 // the correctness-preserving mode, the routed set (to fetch misses).  Both are written
-// by the kernels straight into pinned host memory; the host polls the events that
-// follow them instead of sleeping, so the hand-off costs microseconds.  Overlap
-// statistics are folded in lazily, once a layer's gate is known to have finished.
+// by the kernels straight into pinned host memory, each followed by a completion flag
+// the host spins on, so the hand-off costs microseconds.  Overlap statistics are folded
+// in lazily, once a layer's gate is known to have finished.
+//
+// Two streams.  The compute stream carries the chain that bounds a layer whenever the
+// copies cannot be hidden: router, expert copies, expert FFN, next layer's router.
+// Kernels back to back on one queue start without a gap, while an event recorded
+// between them costs the queue several microseconds and a wait on another queue's event
+// about ten, so that chain holds no events.  The side stream carries the work that only
+// has to finish before the FFN: the slot-table publish, the attention window and the
+// gate (and the shared experts).  The host orders the two through the flags: it enqueues
+// the side stream's work once it has seen the router's flags (the router follows the
+// previous layer's FFN, so that FFN is done too), and the FFN once it has seen the
+// gate's, where the FFN queues behind the copies still in flight.  Slot and scratch reuse
+// needs no event: a layer's copies follow, on the compute stream, every earlier kernel
+// that read those slots.  Only the shared experts, which publish no flag, are waited for
+// with an event.  A layer-step that copies nothing keeps all of its work on the compute
+// stream: with no copy to hide behind, the hand-offs between streams would only add
+// their latency.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -13,11 +29,13 @@
 #include <vector>
 
 #include "common.h"
+#include "prefetch_internal.h"
 #include "route_internal.h"
 
 struct apex_decode {
     apex_decode_config cfg;
     std::vector<apex_decode_layer> layers;
+    std::vector<const uint4 *> host_view;   // device view of each layer's pinned experts
     uint16_t *scratch = nullptr;
     int32_t *miss_table = nullptr;
     int32_t *exec_idx = nullptr;
@@ -44,12 +62,12 @@ struct apex_decode {
     int32_t *route_done = nullptr;    // [B]
     int32_t *gate_done_h = nullptr;   // [L][B]
     int32_t seq = 0;
-    // events
-    hipEvent_t ev_route = nullptr, ready_miss = nullptr, scratch_free = nullptr;
-    std::vector<hipEvent_t> ready, readers_done, gate_done;
+    // event after the shared experts (side stream)
+    hipEvent_t shared_done = nullptr;
     // statistics of layers whose gate may still be running
     struct Pending {
         int layer;
+        int32_t seq;                   // the layer-step's sequence number
         std::vector<int32_t> pf;       // [B][k_max]
         std::vector<int32_t> cnt;      // [B]
         std::vector<char> resident;    // [E]
@@ -60,12 +78,13 @@ struct apex_decode {
 
 namespace {
 
-// Waits until the kernel enqueued before `ev` has published its outputs: every done[b]
+// Waits until a kernel enqueued on `stream` has published its outputs: every done[b]
 // equals seq (the kernel writes them after its outputs, behind a system-scope fence), or
-// the event completed, whichever the host sees first; the flags arrive before the
-// completion signal.  Busy-polls (lower wake-up latency than a blocking wait) and gives
-// up after 30 s, so that a device that stopped making progress surfaces as an error.
-apex_status poll_done(const int32_t *done, int n, int32_t seq, hipEvent_t ev) {
+// the stream has drained, whichever the host sees first.  Busy-polls (lower wake-up
+// latency than a blocking wait); the stream query, every 256 polls, reports a device
+// error, and after 30 s the call gives up, so that a device that stopped making progress
+// surfaces as an error.
+apex_status poll_done(const int32_t *done, int n, int32_t seq, hipStream_t stream) {
     const auto t0 = std::chrono::steady_clock::now();
     for (unsigned it = 0;; ++it) {
         bool all = true;
@@ -73,12 +92,12 @@ apex_status poll_done(const int32_t *done, int n, int32_t seq, hipEvent_t ev) {
             all = __atomic_load_n(done + b, __ATOMIC_ACQUIRE) == seq;
         if (all) return APEX_OK;
         if ((it & 255u) == 255u) {
-            const hipError_t e = hipEventQuery(ev);
+            const hipError_t e = hipStreamQuery(stream);
             if (e == hipSuccess) return APEX_OK;
             if (e != hipErrorNotReady)
-                return apex::fail(APEX_E_HIP, "hipEventQuery failed: %s", hipGetErrorString(e));
+                return apex::fail(APEX_E_HIP, "hipStreamQuery failed: %s", hipGetErrorString(e));
             if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(30))
-                return apex::fail(APEX_E_HIP, "apex_decode_step: event not reached after 30 s");
+                return apex::fail(APEX_E_HIP, "apex_decode_step: kernel not done after 30 s");
         }
     }
 }
@@ -111,17 +130,17 @@ void fold(apex_decode *dec, const apex_decode::Pending &p, apex_decode_stats *st
 // One expert-FFN pass in the layer's weight format.
 apex_status run_ffn(apex_decode *dec, const float *x, int I, int E, int k, const int32_t *idx,
                     const float *gate, const int32_t *slot_of_expert, const void *slots,
-                    int n_slots, float *y, int accumulate) {
+                    int n_slots, float *y, int accumulate, hipStream_t stream) {
     const apex_decode_config &c = dec->cfg;
     if (c.weights == APEX_WEIGHTS_FP8_E4M3)
         return apex_moe_ffn_fp8(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert, slots, n_slots,
-                                y, accumulate, dec->ws, dec->ws_bytes, dec->compute);
+                                y, accumulate, dec->ws, dec->ws_bytes, stream);
     if (c.weights == APEX_WEIGHTS_MXFP4)
         return apex_moe_ffn_mxfp4(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert, slots,
-                                  n_slots, y, accumulate, dec->ws, dec->ws_bytes, dec->compute);
+                                  n_slots, y, accumulate, dec->ws, dec->ws_bytes, stream);
     return apex_moe_ffn(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert,
                         static_cast<const uint16_t *>(slots), n_slots, y, accumulate, dec->ws,
-                        dec->ws_bytes, dec->compute);
+                        dec->ws_bytes, stream);
 }
 
 // The routed experts' executed sets over the given slot pool.
@@ -129,12 +148,21 @@ apex_status ffn(apex_decode *dec, const float *x, const int32_t *slot_of_expert,
                 const uint16_t *slots, int n_slots, float *y, int accumulate) {
     const apex_decode_config &c = dec->cfg;
     return run_ffn(dec, x, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate, slot_of_expert, slots,
-                   n_slots, y, accumulate);
+                   n_slots, y, accumulate, dec->compute);
 }
 
-void fold_pending(apex_decode *dec, apex_decode_stats *st) {
-    for (const auto &p : dec->pending) fold(dec, p, st);
+// Folds the statistics of every pending layer-step once its gate has published the
+// routed sets (normally long done: it precedes that layer's FFN).
+apex_status fold_pending(apex_decode *dec, apex_decode_stats *st) {
+    const int B = dec->cfg.B;
+    for (const auto &p : dec->pending) {
+        const apex_status s = poll_done(dec->gate_done_h + size_t(p.layer) * B, B, p.seq,
+                                        dec->side);
+        if (s != APEX_OK) return s;
+        fold(dec, p, st);
+    }
     dec->pending.clear();
+    return APEX_OK;
 }
 
 }  // namespace
@@ -204,6 +232,7 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     auto *dec = new apex_decode();
     dec->cfg = c;
     dec->layers.assign(layers, layers + c.L);
+    dec->host_view.assign(c.L, nullptr);
     dec->scratch = scratch;
     dec->miss_table = miss_table_dev;
     dec->exec_idx = exec_idx_dev;
@@ -219,6 +248,12 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
         apex_decode_destroy(dec);
         return st;
     };
+    for (int l = 0; l < c.L; ++l) {
+        const apex_status st = apex::pinned_device_view(fn, layers[l].host_experts,
+                                                        size_t(c.E) * dec->expert_bytes,
+                                                        &dec->host_view[l]);
+        if (st != APEX_OK) return cleanup(st);
+    }
     hipError_t e = hipSuccess;
     e = hipHostMalloc(reinterpret_cast<void **>(&dec->pf_idx_h), sizeof(int32_t) * c.B * c.k_max);
     if (e == hipSuccess)
@@ -244,16 +279,8 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     auto mk = [&](hipEvent_t *ev) {
         return hipEventCreateWithFlags(ev, hipEventDisableTiming);
     };
-    if (mk(&dec->ev_route) != hipSuccess || mk(&dec->ready_miss) != hipSuccess ||
-        mk(&dec->scratch_free) != hipSuccess)
+    if (mk(&dec->shared_done) != hipSuccess)
         return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
-    dec->ready.resize(c.L);
-    dec->readers_done.resize(c.L);
-    dec->gate_done.resize(c.L);
-    for (int l = 0; l < c.L; ++l)
-        if (mk(&dec->ready[l]) != hipSuccess || mk(&dec->readers_done[l]) != hipSuccess ||
-            mk(&dec->gate_done[l]) != hipSuccess)
-            return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
     if (c.n_shared > 0) {
         const size_t pairs = size_t(c.B) * c.n_shared;
         std::vector<int32_t> idx(pairs), table(c.n_shared);
@@ -311,36 +338,43 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
                                       dec->pf_idx_h, dec->pf_count_h, nullptr, dec->route_done,
                                       seq, cs);
             if (st != APEX_OK) return st;
-            APEX_HIP(hipEventRecord(dec->ev_route, cs));
         } else {
             std::fill(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max, -1);
             std::fill(dec->pf_count_h, dec->pf_count_h + c.B, 0);
         }
+        if (route) {
+            st = poll_done(dec->route_done, c.B, seq, cs);
+            if (st != APEX_OK) return st;
+        }
+        // copies on the compute stream (after every earlier reader of the slots), the new
+        // slot table on the stream of the gate, which masks with it: the side stream if
+        // anything is copied (the no-prefetch baseline never copies)
+        int n_copy = 0;
+        st = apex::expert_prefetch(dec->host_view[l], Ly.slots, c.E, c.C, dec->expert_bytes,
+                                   dec->pf_idx_h, dec->pf_count_h, c.B, c.k_max, step,
+                                   Ly.expert_of_slot, Ly.last_used, Ly.slot_of_expert_dev,
+                                   Ly.avail_dev, cs, ss, cs, nullptr, nullptr, copied.data(),
+                                   &n_copy);
+        if (st != APEX_OK) return st;
+        const bool split = n_copy > 0;
+        const hipStream_t ws = split ? ss : cs;
+        // the attention window
         if (c.attn_heads > 0) {
             st = apex_attention_decode(h_pre[l], Ly.w_qkv, Ly.w_o, c.B, c.d, c.attn_heads,
                                        c.attn_kv_heads, c.d / c.attn_heads, Ly.k_cache,
                                        Ly.v_cache, c.attn_ctx + 1, c.attn_ctx, Ly.attn_out,
-                                       dec->attn_ws, dec->attn_ws_bytes, cs);
+                                       dec->attn_ws, dec->attn_ws_bytes, ws);
             if (st != APEX_OK) return st;
         } else if (c.t_attn_us > 0) {
-            st = apex_spin_us(c.t_attn_us, cs);
+            st = apex_spin_us(c.t_attn_us, ws);
             if (st != APEX_OK) return st;
         }
-        if (route) {
-            st = poll_done(dec->route_done, c.B, seq, dec->ev_route);
-            if (st != APEX_OK) return st;
-        }
-        // earlier layers' gates precede this route on the stream: fold their statistics
-        fold_pending(dec, stats);
-        int n_copy = 0;
-        st = apex_expert_prefetch(Ly.host_experts, Ly.slots, c.E, c.C, dec->expert_bytes,
-                                  dec->pf_idx_h, dec->pf_count_h, c.B, c.k_max, step,
-                                  Ly.expert_of_slot, Ly.last_used, Ly.slot_of_expert_dev,
-                                  Ly.avail_dev, ss, cs, dec->readers_done[l], dec->ready[l],
-                                  copied.data(), &n_copy);
+        // earlier layer-steps' statistics, now that this layer's copies are on their way
+        st = fold_pending(dec, stats);
         if (st != APEX_OK) return st;
         apex_decode::Pending p;
         p.layer = l;
+        p.seq = seq;
         p.pf.assign(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max);
         p.cnt.assign(dec->pf_count_h, dec->pf_count_h + c.B);
         p.resident.assign(c.E, 0);
@@ -360,47 +394,55 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
                             sizeof(int32_t) * c.C);
             if (rec->n_copies) rec->n_copies[l] = n_copy;
         }
-        // execution stage: original router, then the experts once the copies landed
+        // execution stage: original router
         int32_t *route_h = dec->route_idx_h + size_t(l) * c.B * c.k;
         float *route_g = dec->route_gate_h + size_t(l) * c.B * c.k;
         int32_t *gate_flags = dec->gate_done_h + size_t(l) * c.B;
         st = apex::gate_topk(h_post[l], Ly.w_g, Ly.b_g, c.B, c.d, c.E, c.k, c.mode,
                              Ly.avail_dev, 0, route_h, route_g, dec->exec_idx, dec->exec_gate,
-                             nullptr, gate_flags, seq, cs);
+                             nullptr, gate_flags, seq, ws);
         if (st != APEX_OK) return st;
-        APEX_HIP(hipEventRecord(dec->gate_done[l], cs));
-        // shared experts first: they need no copy, so they run while the copies land
+        // shared experts: they need no copy, so they run beside the copies
         const bool shared = c.n_shared > 0;
         if (shared) {
             st = run_ffn(dec, h_post[l], c.I_shared, c.n_shared, c.n_shared, dec->shared_idx,
                          dec->shared_gate, dec->shared_table, Ly.shared_slots, c.n_shared, y[l],
-                         0);
+                         0, ws);
+            if (st != APEX_OK) return st;
+            if (split) APEX_HIP(hipEventRecord(dec->shared_done, ss));
+        }
+        // on one stream the first FFN pass follows the gate in stream order; across
+        // streams it is enqueued once the gate has published the executed sets, behind the
+        // copies still in flight
+        const int acc = shared ? 1 : 0;
+        if (!split) {
+            st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], acc);
             if (st != APEX_OK) return st;
         }
-        // the slots this layer's FFN reads: the copies just issued (none: every earlier copy
-        // into them completed before an earlier FFN of this layer read them)
-        if (n_copy > 0) APEX_HIP(hipStreamWaitEvent(cs, dec->ready[l], 0));
-        st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], shared ? 1 : 0);
-        if (st != APEX_OK) return st;
+        // the correctness-preserving mode needs the routed sets in any case
+        if (split || c.mode == APEX_MODE_EXACT) {
+            st = poll_done(gate_flags, c.B, seq, ws);
+            if (st != APEX_OK) return st;
+        }
         int n_miss = 0;
         if (c.mode == APEX_MODE_EXACT) {
-            // asynchronous miss correction: the resident experts run while misses copy
-            st = poll_done(gate_flags, c.B, seq, dec->gate_done[l]);
-            if (st != APEX_OK) return st;
+            // asynchronous miss correction: the misses queue behind the prefetch copies
             st = apex_expert_fetch_misses(Ly.host_experts, dec->scratch, c.n_scratch, c.E, c.C,
                                           dec->expert_bytes, route_h, c.B, c.k,
-                                          Ly.expert_of_slot, dec->miss_table, ss, cs,
-                                          dec->scratch_free, dec->ready_miss, missing.data(),
-                                          &n_miss);
+                                          Ly.expert_of_slot, dec->miss_table, cs, cs, nullptr,
+                                          nullptr, missing.data(), &n_miss);
             if (st != APEX_OK) return st;
-            if (n_miss > 0) {
-                APEX_HIP(hipStreamWaitEvent(cs, dec->ready_miss, 0));
-                st = ffn(dec, h_post[l], dec->miss_table, dec->scratch, c.n_scratch, y[l], 1);
-                if (st != APEX_OK) return st;
-                APEX_HIP(hipEventRecord(dec->scratch_free, cs));
-            }
         }
-        APEX_HIP(hipEventRecord(dec->readers_done[l], cs));
+        if (split) {
+            // the routed experts once the copies landed (stream order)
+            if (shared) APEX_HIP(hipStreamWaitEvent(cs, dec->shared_done, 0));
+            st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], acc);
+            if (st != APEX_OK) return st;
+        }
+        if (n_miss > 0) {
+            st = ffn(dec, h_post[l], dec->miss_table, dec->scratch, c.n_scratch, y[l], 1);
+            if (st != APEX_OK) return st;
+        }
         p.misses = n_miss;
         dec->pending.push_back(std::move(p));
         if (rec) {
@@ -419,7 +461,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
             if (rec->n_missing) rec->n_missing[l] = n_miss;
         }
     }
-    if (rec) fold_pending(dec, stats);
+    if (rec) return fold_pending(dec, stats);
     return APEX_OK;
 }
 
@@ -427,19 +469,14 @@ extern "C" apex_status apex_decode_finish(apex_decode *dec, apex_decode_stats *s
     APEX_REQUIRE(dec, "apex_decode_finish: NULL driver");
     APEX_HIP(hipStreamSynchronize(dec->compute));
     APEX_HIP(hipStreamSynchronize(dec->side));
-    fold_pending(dec, stats);
-    return APEX_OK;
+    return fold_pending(dec, stats);
 }
 
 extern "C" apex_status apex_decode_destroy(apex_decode *dec) {
     if (!dec) return APEX_OK;
     if (dec->compute) (void)hipStreamSynchronize(dec->compute);
     if (dec->side) (void)hipStreamSynchronize(dec->side);
-    for (hipEvent_t e : {dec->ev_route, dec->ready_miss, dec->scratch_free})
-        if (e) (void)hipEventDestroy(e);
-    for (auto *v : {&dec->ready, &dec->readers_done, &dec->gate_done})
-        for (hipEvent_t e : *v)
-            if (e) (void)hipEventDestroy(e);
+    if (dec->shared_done) (void)hipEventDestroy(dec->shared_done);
     for (void *p : {static_cast<void *>(dec->pf_idx_h), static_cast<void *>(dec->pf_count_h),
                     static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h),
                     static_cast<void *>(dec->route_done), static_cast<void *>(dec->gate_done_h)})

@@ -13,14 +13,20 @@
 // cost of about 10 us on top of the transfer (a 3.15 MB expert takes 65-69 us against 55
 // at the link's peak) and about 8 us of host time to issue, and the copies of a layer are
 // on the critical path whenever the attention window cannot hide them.  One launch moves
-// all of a layer's experts at 53-54 GB/s for 2-3 experts; its workgroups mostly wait on
-// PCIe reads and take few compute-unit cycles from the kernels running beside them.
+// all of a layer's experts at 51-54 GB/s; its workgroups mostly wait on PCIe reads and
+// take few compute-unit cycles from the kernels running beside them.
+//
+// The grid is a fixed 24 workgroups, whatever the number of experts: the link is full
+// from about 24 (fewer lose bandwidth: 16 reach 39-44 GB/s), while every read the copy
+// keeps queued on the link delays the PCIe reads of other work (dispatch packets, kernel
+// arguments, completion signals).  Three experts on 96 workgroups took a chain of three
+// small kernels on another stream from 12 to 65 us; on 24 it takes 16.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <vector>
 
 #include "common.h"
+#include "prefetch_internal.h"
 
 namespace {
 
@@ -35,30 +41,19 @@ struct CopyPlan {
     int32_t to[APEX_MAX_EXPERTS];
 };
 
-constexpr int kCopyThreads = 256;
-constexpr int kCopyUnroll = 2;          // 16-byte loads in flight per thread
-constexpr int kCopyGroups = 32;         // workgroups per expert (enough to fill the link)
+constexpr int kCopyThreads = 256;       // one 16-byte word per thread per chunk
+constexpr int kCopyGroups = 24;         // workgroups per launch
 
-// grid (kCopyGroups, n experts); each workgroup strides over its expert in chunks of
-// kCopyThreads * kCopyUnroll 16-byte words.  n16 = expert bytes / 16.
+// The n experts of a launch are cut into chunks of kCopyThreads 16-byte words, numbered
+// expert by expert (chunks_per_expert each, the last one ragged); workgroup g moves
+// chunks g, g + grid, g + 2 * grid, ...  n16 = expert bytes / 16.
 __global__ __launch_bounds__(kCopyThreads) void expert_copy_kernel(
-    const uint4 *__restrict__ src, uint4 *__restrict__ dst, size_t n16, CopyPlan plan) {
-    const uint4 *from = src + size_t(plan.from[blockIdx.y]) * n16;
-    uint4 *to = dst + size_t(plan.to[blockIdx.y]) * n16;
-    const size_t chunk = size_t(kCopyThreads) * kCopyUnroll;
-    const size_t stride = size_t(gridDim.x) * chunk;
-    for (size_t i = size_t(blockIdx.x) * chunk + threadIdx.x; i < n16; i += stride) {
-        uint4 v[kCopyUnroll];
-#pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u) {
-            const size_t j = i + size_t(u) * kCopyThreads;
-            if (j < n16) v[u] = from[j];
-        }
-#pragma unroll
-        for (int u = 0; u < kCopyUnroll; ++u) {
-            const size_t j = i + size_t(u) * kCopyThreads;
-            if (j < n16) to[j] = v[u];
-        }
+    const uint4 *__restrict__ src, uint4 *__restrict__ dst, uint32_t n16,
+    uint32_t chunks_per_expert, uint32_t chunks, CopyPlan plan) {
+    for (uint32_t c = blockIdx.x; c < chunks; c += gridDim.x) {
+        const uint32_t i = c / chunks_per_expert;
+        const uint32_t j = (c - i * chunks_per_expert) * kCopyThreads + threadIdx.x;
+        if (j < n16) dst[size_t(plan.to[i]) * n16 + j] = src[size_t(plan.from[i]) * n16 + j];
     }
 }
 
@@ -80,10 +75,9 @@ apex_status wait_unless_done(hipStream_t stream, hipEvent_t ev) {
     return APEX_OK;
 }
 
-// The device address of `bytes` bytes of pinned host memory at `host`, which the copy
-// kernel reads.  Pageable memory, device memory and ranges that leave the pinned
-// allocation are refused: a kernel cannot read them.
-apex_status pinned_device_view(const char *fn, const void *host, size_t bytes,
+}  // namespace
+
+apex_status apex::pinned_device_view(const char *fn, const void *host, size_t bytes,
                                const uint4 **dev) {
     APEX_REQUIRE(reinterpret_cast<uintptr_t>(host) % 16 == 0,
                  "%s: host_experts %p is not 16-byte aligned", fn, host);
@@ -102,10 +96,18 @@ apex_status pinned_device_view(const char *fn, const void *host, size_t bytes,
     return APEX_OK;
 }
 
+namespace {
+
+// n >= 1 experts of expert_bytes (a multiple of 16, at most 16 * UINT32_MAX; checked by
+// the entry points).
 apex_status copy_experts(const uint4 *src, void *pool, size_t expert_bytes, const CopyPlan &plan,
                          int n, hipStream_t stream) {
-    hipLaunchKernelGGL(expert_copy_kernel, dim3(kCopyGroups, n), dim3(kCopyThreads), 0, stream,
-                       src, static_cast<uint4 *>(pool), expert_bytes / 16, plan);
+    const uint32_t n16 = uint32_t(expert_bytes / 16);
+    const uint32_t per = (n16 + kCopyThreads - 1) / kCopyThreads;
+    const uint32_t chunks = per * uint32_t(n);
+    const uint32_t grid = std::min<uint32_t>(kCopyGroups, chunks);
+    hipLaunchKernelGGL(expert_copy_kernel, dim3(grid), dim3(kCopyThreads), 0, stream, src,
+                       static_cast<uint4 *>(pool), n16, per, chunks, plan);
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }
@@ -120,26 +122,16 @@ apex_status publish(const Table &t, int E, int32_t *slot_dev, uint8_t *avail_dev
 
 }  // namespace
 
-extern "C" apex_status apex_expert_prefetch(
-    const uint16_t *host_experts, uint16_t *slots, int E, int C, size_t expert_bytes,
-    const int32_t *pf_idx, const int32_t *pf_count, int B, int k_max, int64_t step,
-    int32_t *expert_of_slot, int64_t *last_used, int32_t *slot_of_expert_dev,
-    uint8_t *avail_dev, hipStream_t side, hipStream_t compute, hipEvent_t readers_done,
-    hipEvent_t ready, int32_t *copied_experts, int *n_copied) {
-    const char *fn = "apex_expert_prefetch";
-    APEX_REQUIRE(host_experts && slots && slot_of_expert_dev && ready,
-                 "%s: NULL pointer or event", fn);
-    APEX_REQUIRE(E >= 1 && E <= APEX_MAX_EXPERTS, "%s: E=%d out of [1, 64]", fn, E);
-    APEX_REQUIRE(C >= 1 && C <= E, "%s: C=%d out of [1, E=%d]", fn, C, E);
-    APEX_REQUIRE(expert_bytes > 0 && expert_bytes % 16 == 0,
-                 "%s: expert_bytes=%zu must be a positive multiple of 16", fn, expert_bytes);
-    const uint4 *src = nullptr;
-    apex_status st = pinned_device_view(fn, host_experts, size_t(E) * expert_bytes, &src);
-    if (st != APEX_OK) return st;
-    std::vector<int32_t> ce(C), cs(C);
+apex_status apex::expert_prefetch(
+    const uint4 *src, uint16_t *slots, int E, int C, size_t expert_bytes, const int32_t *pf_idx,
+    const int32_t *pf_count, int B, int k_max, int64_t step, int32_t *expert_of_slot,
+    int64_t *last_used, int32_t *slot_of_expert_dev, uint8_t *avail_dev, hipStream_t side,
+    hipStream_t compute, hipStream_t compute_if_none, hipEvent_t readers_done, hipEvent_t ready,
+    int32_t *copied_experts, int *n_copied) {
+    int32_t ce[APEX_MAX_EXPERTS], cs[APEX_MAX_EXPERTS];
     int n = 0;
-    st = apex_plan_residency(E, C, pf_idx, pf_count, B, k_max, step, expert_of_slot,
-                                         last_used, ce.data(), cs.data(), &n);
+    apex_status st = apex_plan_residency(E, C, pf_idx, pf_count, B, k_max, step, expert_of_slot,
+                                         last_used, ce, cs, &n);
     if (st != APEX_OK) return st;
 
     st = wait_unless_done(side, readers_done);
@@ -153,18 +145,40 @@ extern "C" apex_status apex_expert_prefetch(
         st = copy_experts(src, slots, expert_bytes, plan, n, side);
         if (st != APEX_OK) return st;
     }
-    APEX_HIP(hipEventRecord(ready, side));
+    if (ready) APEX_HIP(hipEventRecord(ready, side));
 
     Table t;
     std::fill(t.slot, t.slot + APEX_MAX_EXPERTS, -1);
     for (int s = 0; s < C; ++s)
         if (expert_of_slot[s] >= 0) t.slot[expert_of_slot[s]] = s;
-    st = publish(t, E, slot_of_expert_dev, avail_dev, compute);
+    st = publish(t, E, slot_of_expert_dev, avail_dev, n > 0 ? compute : compute_if_none);
     if (st != APEX_OK) return st;
     if (copied_experts)
         for (int i = 0; i < n; ++i) copied_experts[i] = ce[i];
     if (n_copied) *n_copied = n;
     return APEX_OK;
+}
+
+extern "C" apex_status apex_expert_prefetch(
+    const uint16_t *host_experts, uint16_t *slots, int E, int C, size_t expert_bytes,
+    const int32_t *pf_idx, const int32_t *pf_count, int B, int k_max, int64_t step,
+    int32_t *expert_of_slot, int64_t *last_used, int32_t *slot_of_expert_dev,
+    uint8_t *avail_dev, hipStream_t side, hipStream_t compute, hipEvent_t readers_done,
+    hipEvent_t ready, int32_t *copied_experts, int *n_copied) {
+    const char *fn = "apex_expert_prefetch";
+    APEX_REQUIRE(host_experts && slots && slot_of_expert_dev, "%s: NULL pointer", fn);
+    APEX_REQUIRE(E >= 1 && E <= APEX_MAX_EXPERTS, "%s: E=%d out of [1, 64]", fn, E);
+    APEX_REQUIRE(C >= 1 && C <= E, "%s: C=%d out of [1, E=%d]", fn, C, E);
+    APEX_REQUIRE(expert_bytes > 0 && expert_bytes % 16 == 0 && expert_bytes / 16 <= UINT32_MAX,
+                 "%s: expert_bytes=%zu must be a positive multiple of 16 below 64 GiB", fn,
+                 expert_bytes);
+    const uint4 *src = nullptr;
+    apex_status st = apex::pinned_device_view(fn, host_experts, size_t(E) * expert_bytes, &src);
+    if (st != APEX_OK) return st;
+    return apex::expert_prefetch(src, slots, E, C, expert_bytes, pf_idx, pf_count, B, k_max,
+                                 step, expert_of_slot, last_used, slot_of_expert_dev, avail_dev,
+                                 side, compute, compute, readers_done, ready, copied_experts,
+                                 n_copied);
 }
 
 extern "C" apex_status apex_expert_fetch_misses(
@@ -173,15 +187,16 @@ extern "C" apex_status apex_expert_fetch_misses(
     int32_t *miss_table_dev, hipStream_t side, hipStream_t compute, hipEvent_t scratch_free,
     hipEvent_t ready, int32_t *missing, int *n_missing) {
     const char *fn = "apex_expert_fetch_misses";
-    APEX_REQUIRE(host_experts && scratch && expert_of_slot && miss_table_dev && ready && n_missing,
-                 "%s: NULL pointer or event", fn);
+    APEX_REQUIRE(host_experts && scratch && expert_of_slot && miss_table_dev && n_missing,
+                 "%s: NULL pointer", fn);
     APEX_REQUIRE(E >= 1 && E <= APEX_MAX_EXPERTS, "%s: E=%d out of [1, 64]", fn, E);
     APEX_REQUIRE(C >= 1, "%s: C=%d must be >= 1", fn, C);
     APEX_REQUIRE(n_scratch >= 0, "%s: n_scratch=%d < 0", fn, n_scratch);
     APEX_REQUIRE(B >= 0 && k >= 1 && k <= E, "%s: B=%d k=%d", fn, B, k);
     APEX_REQUIRE(B == 0 || route_idx, "%s: NULL route_idx", fn);
-    APEX_REQUIRE(expert_bytes > 0 && expert_bytes % 16 == 0,
-                 "%s: expert_bytes=%zu must be a positive multiple of 16", fn, expert_bytes);
+    APEX_REQUIRE(expert_bytes > 0 && expert_bytes % 16 == 0 && expert_bytes / 16 <= UINT32_MAX,
+                 "%s: expert_bytes=%zu must be a positive multiple of 16 below 64 GiB", fn,
+                 expert_bytes);
     bool resident[APEX_MAX_EXPERTS] = {false};
     for (int s = 0; s < C; ++s) {
         const int e = expert_of_slot[s];
@@ -203,7 +218,7 @@ extern "C" apex_status apex_expert_fetch_misses(
                           n_scratch);
 
     const uint4 *src = nullptr;
-    apex_status st = pinned_device_view(fn, host_experts, size_t(E) * expert_bytes, &src);
+    apex_status st = apex::pinned_device_view(fn, host_experts, size_t(E) * expert_bytes, &src);
     if (st != APEX_OK) return st;
 
     if (missing)
@@ -219,7 +234,7 @@ extern "C" apex_status apex_expert_fetch_misses(
     }
     st = copy_experts(src, scratch, expert_bytes, plan, n, side);
     if (st != APEX_OK) return st;
-    APEX_HIP(hipEventRecord(ready, side));
+    if (ready) APEX_HIP(hipEventRecord(ready, side));
 
     Table t;
     std::fill(t.slot, t.slot + APEX_MAX_EXPERTS, -1);

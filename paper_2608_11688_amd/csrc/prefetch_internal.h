@@ -1,0 +1,26 @@
+// Expert-copy pieces shared by the prefetch entry points and the decode driver.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "apex.h"
+
+namespace apex {
+
+// The device address of `bytes` bytes of pinned host memory at `host` (16-byte aligned),
+// which the copy kernel reads.  Pageable memory, device memory and ranges whose last byte
+// leaves pinned memory are refused with APEX_E_INVAL naming `fn`: a kernel cannot read them.
+apex_status pinned_device_view(const char *fn, const void *host, size_t bytes, const uint4 **dev);
+
+// apex_expert_prefetch after argument checks, reading the experts at the device view
+// `src`, with one difference: the slot table goes to `compute` when any expert is copied
+// and to `compute_if_none` otherwise.
+apex_status expert_prefetch(const uint4 *src, uint16_t *slots, int E, int C, size_t expert_bytes,
+                            const int32_t *pf_idx, const int32_t *pf_count, int B, int k_max,
+                            int64_t step, int32_t *expert_of_slot, int64_t *last_used,
+                            int32_t *slot_of_expert_dev, uint8_t *avail_dev, hipStream_t side,
+                            hipStream_t compute, hipStream_t compute_if_none,
+                            hipEvent_t readers_done, hipEvent_t ready, int32_t *copied_experts,
+                            int *n_copied);
+
+}  // namespace apex

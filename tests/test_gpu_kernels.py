@@ -552,10 +552,11 @@ def test_expert_prefetch_and_miss_fetch(torch):
 
 
 def test_expert_copies_span_strides_and_refuse_pageable_memory(torch):
-    # experts of 1.63 MB: each copy workgroup row walks several strides and a ragged tail
+    # experts of 1.63 MB: 400 chunks of 4 KB each, the last one ragged, so every copy
+    # workgroup moves many chunks across expert boundaries
     d, I, E, C = 1032, 264, 6, 3
     S = native.apex_expert_bytes(d, I)
-    assert (S // 16) % (32 * 512) != 0
+    assert (S // 16) % 256 != 0 and S // 4096 > 24
     rng = np.random.default_rng(21)
     host = torch.empty(E * S // 2, dtype=torch.int16, pin_memory=True)
     host.copy_(torch.from_numpy(rng.integers(-30000, 30000, E * S // 2).astype(np.int16)))
