@@ -202,6 +202,47 @@ def test_decode_deepseek_shape_with_shared_experts(batch, mode):
     assert st["ffn_checked"] > 0
 
 
+def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers):
+    """Final outputs and counters of the same decode without and with per-layer records."""
+    from paper_2608_11688_amd.runtime import DecodeRunner
+    out = []
+    for record in (False, True):
+        runner = DecodeRunner(cfg, batch=batch, mode=mode, steps=steps, layers=layers,
+                              t_attn_us=2.0, record=record)
+        try:
+            for _ in range(steps):
+                runner.step()
+            runner.finish()
+            s = runner.stats
+            counts = (s.tokens, s.layer_steps, s.copies, s.misses, s.coverage_count,
+                      s.delta_hat_sum, s.overlap_sum, s.hit_sum)
+            out.append((runner.y.cpu().numpy().copy(), counts))
+        finally:
+            runner.close()
+    return out
+
+
+@pytest.mark.parametrize("cfg_name,batch,mode,layers", [
+    ("GRANITE_1B", 1, native.MODE_EXACT, None),
+    ("GRANITE_1B", 1, native.MODE_STALL_FREE, None),
+    ("OLMOE", 16, native.MODE_EXACT, [0, 5, 9, 15]),
+    ("DEEPSEEK_16B", 1, native.MODE_EXACT, [0, 12, 25]),
+])
+def test_decode_without_records_matches_recorded(cfg_name, batch, mode, layers):
+    # The parity tests above record every layer, which synchronizes the host with the
+    # device after each one; the timed path does not, and there the copies, the window,
+    # the gate and the FFN overlap across the two streams.  Same inputs, same state: the
+    # counters must agree exactly and the last step's outputs to rounding.
+    cfg = getattr(configs, cfg_name)
+    layers = list(range(cfg.L)) if layers is None else layers
+    (y_free, c_free), (y_rec, c_rec) = run_unrecorded_and_recorded(cfg, batch, mode, 6, layers)
+    assert c_free == c_rec
+    assert c_free[2] > 0                        # copies happened
+    scale = np.abs(y_rec).max()
+    assert scale > 0
+    assert np.abs(y_free - y_rec).max() <= 1e-5 * scale
+
+
 @pytest.mark.parametrize("batch,mode", [(1, native.MODE_EXACT), (8, native.MODE_STALL_FREE)])
 def test_decode_phi_shape(batch, mode):
     cfg = configs.PHI_7B
