@@ -87,6 +87,60 @@ def pinned_h2d_peak(torch, nbytes=1 << 30, reps=3):
     return nbytes / dt / 1e9
 
 
+def expert_copy_leg(torch, native, expert_bytes, E, link_peak, reps=5):
+    """Times the prefetch's copy kernel (apex_expert_prefetch) on a plan of n experts of
+    the workload (3, or 1 when three would pass 256 MB), event pair on the copy stream
+    around the call (the slot-table publish goes to another stream), against the same
+    bytes moved by one DMA-engine copy per expert and against the link's pinned peak.  A
+    spin kernel holds the stream while the host plans and enqueues, so the pair brackets
+    device time only.
+    """
+    n = 3 if 3 * expert_bytes <= (256 << 20) else 1
+    n = min(n, E)
+    host = torch.empty(n * expert_bytes, dtype=torch.uint8, pin_memory=True)
+    pool = torch.empty(n * expert_bytes, dtype=torch.uint8, device="cuda")
+    slot_dev = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    cs, ts = torch.cuda.Stream(), torch.cuda.Stream()
+    pf_idx = np.arange(n, dtype=np.int32)[None, :]
+    pf_cnt = np.array([n], np.int32)
+
+    def timed(body):
+        out = []
+        for _ in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            native.apex_spin_us(100.0, cs.cuda_stream)
+            e0.record(cs)
+            body()
+            e1.record(cs)
+            e1.synchronize()
+            out.append(e0.elapsed_time(e1) * 1e3)
+        return float(np.median(out[1:]))
+
+    def kernel():
+        eos = np.full(n, -1, np.int32)
+        lu = np.full(n, -1, np.int64)
+        got = native.apex_expert_prefetch(host, pool, n, n, expert_bytes, pf_idx, pf_cnt, 1, n,
+                                          0, eos, lu, slot_dev, None, cs.cuda_stream,
+                                          ts.cuda_stream, None, None)
+        assert got == n
+
+    def dma():
+        with torch.cuda.stream(cs):
+            for i in range(n):
+                a, b = i * expert_bytes, (i + 1) * expert_bytes
+                pool[a:b].copy_(host[a:b], non_blocking=True)
+
+    us_kernel, us_dma = timed(kernel), timed(dma)
+    torch.cuda.synchronize()
+    del host, pool
+    gbps = n * expert_bytes / (us_kernel * 1e-6) / 1e9
+    return {"kernel": "expert_copy_kernel", "experts": n, "bytes": n * expert_bytes,
+            "us": round(us_kernel, 2), "GBps": round(gbps, 2),
+            "dma_per_expert_us": round(us_dma, 2),
+            "link_peak_GBps": round(link_peak, 2),
+            "frac_of_link_peak": round(gbps / link_peak, 4)}
+
+
 def ffn_roofline_leg(torch, native, runner, reps=8, seed=123):
     """Times apex_moe_ffn in the decode timeline's launch configuration.
 
@@ -369,6 +423,7 @@ def main():
     warm = runner.warmup_summary
     copied_bytes_per_step = s["copies_per_layer_step"] * L * S
     runner.close()
+    copy_leg = expert_copy_leg(torch, native, S, cfg.E, h2d_peak)
     # exposed stall: this timeline against the same one with every expert resident
     value_resident = stall = None
     if not args.no_compute_only:
@@ -420,6 +475,7 @@ def main():
         "exposed_stall_us_per_token_layer": None if stall is None else round(stall, 3),
         "h2d_GBps_over_step": round(copied_bytes_per_step / (ms_per_step * 1e-3) / 1e9, 2),
         "h2d_pinned_peak_GBps": round(h2d_peak, 2),
+        "copy_leg": copy_leg,
         "hbm_copy_kernel": calib,
         "roofline": {"bound": "hbm", "kernel": FFN_KERNELS[B == 1],
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",

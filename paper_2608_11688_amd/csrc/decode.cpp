@@ -17,16 +17,10 @@
 // previous layer's FFN, so that FFN is done too), and the FFN once it has seen the
 // gate's, where the FFN queues behind the copies still in flight.  Slot and scratch reuse
 // needs no event: a layer's copies follow, on the compute stream, every earlier kernel
-// that read those slots.  A layer-step that copies nothing keeps all of its work on the
-// compute stream: with no copy to hide behind, the hand-offs between streams would only
-// add their latency.
-//
-// The first FFN pass is split when a layer-step copies: the executed experts whose slots
-// this step's copies leave alone run on the side stream right after the gate, while the
-// copies are in flight (as the correctness-preserving mode's resident experts run while
-// its misses load); only the experts being copied run on the compute stream behind the
-// copies, which shortens the FFN that follows the last transfer.  The host waits for the
-// side stream's pass (normally done long before the copies) before it queues the other.
+// that read those slots.  Only the shared experts, which publish no flag, are waited for
+// with an event.  A layer-step that copies nothing keeps all of its work on the compute
+// stream: with no copy to hide behind, the hand-offs between streams would only add
+// their latency.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -68,10 +62,8 @@ struct apex_decode {
     int32_t *route_done = nullptr;    // [B]
     int32_t *gate_done_h = nullptr;   // [L][B]
     int32_t seq = 0;
-    // event after the side stream's FFN pass (the experts no copy touches)
-    hipEvent_t before_done = nullptr;
-    // the slot table split by this step's copies (device [E] each)
-    int32_t *tab_before = nullptr, *tab_landing = nullptr;
+    // event after the shared experts (side stream)
+    hipEvent_t shared_done = nullptr;
     // statistics of layers whose gate may still be running
     struct Pending {
         int layer;
@@ -157,29 +149,6 @@ apex_status ffn(apex_decode *dec, const float *x, const int32_t *slot_of_expert,
     const apex_decode_config &c = dec->cfg;
     return run_ffn(dec, x, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate, slot_of_expert, slots,
                    n_slots, y, accumulate, dec->compute);
-}
-
-// The routed experts' executed sets over the given slot pool, on `stream`.
-apex_status ffn_on(apex_decode *dec, const float *x, const int32_t *slot_of_expert,
-                   const uint16_t *slots, int n_slots, float *y, int accumulate,
-                   hipStream_t stream) {
-    const apex_decode_config &c = dec->cfg;
-    return run_ffn(dec, x, c.I, c.E, c.k, dec->exec_idx, dec->exec_gate, slot_of_expert, slots,
-                   n_slots, y, accumulate, stream);
-}
-
-// Spins until `ev` has completed (30 s at most), so that later work can be queued on
-// another stream without a device-side wait.
-apex_status wait_event(hipEvent_t ev) {
-    const auto t0 = std::chrono::steady_clock::now();
-    for (;;) {
-        const hipError_t e = hipEventQuery(ev);
-        if (e == hipSuccess) return APEX_OK;
-        if (e != hipErrorNotReady)
-            return apex::fail(APEX_E_HIP, "hipEventQuery failed: %s", hipGetErrorString(e));
-        if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(30))
-            return apex::fail(APEX_E_HIP, "apex_decode_step: event not reached after 30 s");
-    }
 }
 
 // Folds the statistics of every pending layer-step once its gate has published the
@@ -310,14 +279,8 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     auto mk = [&](hipEvent_t *ev) {
         return hipEventCreateWithFlags(ev, hipEventDisableTiming);
     };
-    if (mk(&dec->before_done) != hipSuccess)
+    if (mk(&dec->shared_done) != hipSuccess)
         return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
-    e = hipMalloc(reinterpret_cast<void **>(&dec->tab_before), sizeof(int32_t) * c.E);
-    if (e == hipSuccess)
-        e = hipMalloc(reinterpret_cast<void **>(&dec->tab_landing), sizeof(int32_t) * c.E);
-    if (e != hipSuccess)
-        return cleanup(apex::fail(APEX_E_HIP, "%s: hipMalloc failed: %s", fn,
-                                  hipGetErrorString(e)));
     if (c.n_shared > 0) {
         const size_t pairs = size_t(c.B) * c.n_shared;
         std::vector<int32_t> idx(pairs), table(c.n_shared);
@@ -391,7 +354,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
                                    dec->pf_idx_h, dec->pf_count_h, c.B, c.k_max, step,
                                    Ly.expert_of_slot, Ly.last_used, Ly.slot_of_expert_dev,
                                    Ly.avail_dev, cs, ss, cs, nullptr, nullptr, copied.data(),
-                                   &n_copy, dec->tab_before, dec->tab_landing);
+                                   &n_copy);
         if (st != APEX_OK) return st;
         const bool split = n_copy > 0;
         const hipStream_t ws = split ? ss : cs;
@@ -446,15 +409,13 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
                          dec->shared_gate, dec->shared_table, Ly.shared_slots, c.n_shared, y[l],
                          0, ws);
             if (st != APEX_OK) return st;
+            if (split) APEX_HIP(hipEventRecord(dec->shared_done, ss));
         }
+        // on one stream the first FFN pass follows the gate in stream order; across
+        // streams it is enqueued once the gate has published the executed sets, behind the
+        // copies still in flight
         const int acc = shared ? 1 : 0;
-        if (split) {
-            // the executed experts no copy touches, beside the copies
-            st = ffn_on(dec, h_post[l], dec->tab_before, Ly.slots, c.C, y[l], acc, ss);
-            if (st != APEX_OK) return st;
-            APEX_HIP(hipEventRecord(dec->before_done, ss));
-        } else {
-            // on one stream the first FFN pass follows the gate in stream order
+        if (!split) {
             st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], acc);
             if (st != APEX_OK) return st;
         }
@@ -473,22 +434,10 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
             if (st != APEX_OK) return st;
         }
         if (split) {
-            // the experts being copied, behind the copies (stream order), once the side
-            // stream's pass has added its part; in the correctness-preserving mode only if
-            // one of them was routed
-            bool landing_used = true;
-            if (c.mode == APEX_MODE_EXACT) {
-                landing_used = false;
-                for (int i = 0; i < c.B * c.k && !landing_used; ++i)
-                    for (int j = 0; j < n_copy && !landing_used; ++j)
-                        landing_used = route_h[i] == copied[j];
-            }
-            st = wait_event(dec->before_done);
+            // the routed experts once the copies landed (stream order)
+            if (shared) APEX_HIP(hipStreamWaitEvent(cs, dec->shared_done, 0));
+            st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], acc);
             if (st != APEX_OK) return st;
-            if (landing_used) {
-                st = ffn(dec, h_post[l], dec->tab_landing, Ly.slots, c.C, y[l], 1);
-                if (st != APEX_OK) return st;
-            }
         }
         if (n_miss > 0) {
             st = ffn(dec, h_post[l], dec->miss_table, dec->scratch, c.n_scratch, y[l], 1);
@@ -527,9 +476,7 @@ extern "C" apex_status apex_decode_destroy(apex_decode *dec) {
     if (!dec) return APEX_OK;
     if (dec->compute) (void)hipStreamSynchronize(dec->compute);
     if (dec->side) (void)hipStreamSynchronize(dec->side);
-    if (dec->before_done) (void)hipEventDestroy(dec->before_done);
-    for (void *p : {static_cast<void *>(dec->tab_before), static_cast<void *>(dec->tab_landing)})
-        if (p) (void)hipFree(p);
+    if (dec->shared_done) (void)hipEventDestroy(dec->shared_done);
     for (void *p : {static_cast<void *>(dec->pf_idx_h), static_cast<void *>(dec->pf_count_h),
                     static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h),
                     static_cast<void *>(dec->route_done), static_cast<void *>(dec->gate_done_h)})

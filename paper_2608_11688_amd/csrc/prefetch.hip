@@ -61,19 +61,12 @@ __global__ __launch_bounds__(kCopyThreads) void expert_copy_kernel(
     }
 }
 
-// Writes the slot table (and the resident mask); with `before` and `landing` given, also
-// the table split by the experts of `copied` (bit e: expert e is being copied): `before`
-// keeps the residents whose slots no copy of this plan touches, `landing` the others.
 __global__ void publish_table_kernel(Table t, int E, int32_t *__restrict__ slot_of_expert,
-                                     uint8_t *__restrict__ avail, uint64_t copied,
-                                     int32_t *__restrict__ before, int32_t *__restrict__ landing) {
+                                     uint8_t *__restrict__ avail) {
     const int e = threadIdx.x;
     if (e < E) {
         slot_of_expert[e] = t.slot[e];
         if (avail) avail[e] = t.slot[e] >= 0 ? 1 : 0;
-        const bool c = (copied >> e) & 1;
-        if (before) before[e] = c ? -1 : t.slot[e];
-        if (landing) landing[e] = c ? t.slot[e] : -1;
     }
 }
 
@@ -125,10 +118,9 @@ apex_status copy_experts(const uint4 *src, void *pool, size_t expert_bytes, cons
 }
 
 apex_status publish(const Table &t, int E, int32_t *slot_dev, uint8_t *avail_dev,
-                    hipStream_t stream, uint64_t copied = 0, int32_t *before = nullptr,
-                    int32_t *landing = nullptr) {
+                    hipStream_t stream) {
     hipLaunchKernelGGL(publish_table_kernel, dim3(1), dim3(APEX_MAX_EXPERTS), 0, stream, t, E,
-                       slot_dev, avail_dev, copied, before, landing);
+                       slot_dev, avail_dev);
     APEX_HIP(hipGetLastError());
     return APEX_OK;
 }
@@ -140,7 +132,7 @@ apex_status apex::expert_prefetch(
     const int32_t *pf_count, int B, int k_max, int64_t step, int32_t *expert_of_slot,
     int64_t *last_used, int32_t *slot_of_expert_dev, uint8_t *avail_dev, hipStream_t side,
     hipStream_t compute, hipStream_t compute_if_none, hipEvent_t readers_done, hipEvent_t ready,
-    int32_t *copied_experts, int *n_copied, int32_t *before_dev, int32_t *landing_dev) {
+    int32_t *copied_experts, int *n_copied) {
     int32_t ce[APEX_MAX_EXPERTS], cs[APEX_MAX_EXPERTS];
     int n = 0;
     apex_status st = apex_plan_residency(E, C, pf_idx, pf_count, B, k_max, step, expert_of_slot,
@@ -164,10 +156,7 @@ apex_status apex::expert_prefetch(
     std::fill(t.slot, t.slot + APEX_MAX_EXPERTS, -1);
     for (int s = 0; s < C; ++s)
         if (expert_of_slot[s] >= 0) t.slot[expert_of_slot[s]] = s;
-    uint64_t copied = 0;
-    for (int i = 0; i < n; ++i) copied |= uint64_t(1) << ce[i];
-    st = publish(t, E, slot_of_expert_dev, avail_dev, n > 0 ? compute : compute_if_none, copied,
-                 before_dev, landing_dev);
+    st = publish(t, E, slot_of_expert_dev, avail_dev, n > 0 ? compute : compute_if_none);
     if (st != APEX_OK) return st;
     if (copied_experts)
         for (int i = 0; i < n; ++i) copied_experts[i] = ce[i];
@@ -194,7 +183,7 @@ extern "C" apex_status apex_expert_prefetch(
     return apex::expert_prefetch(src, slots, E, C, expert_bytes, pf_idx, pf_count, B, k_max,
                                  step, expert_of_slot, last_used, slot_of_expert_dev, avail_dev,
                                  side, compute, compute, readers_done, ready, copied_experts,
-                                 n_copied, nullptr, nullptr);
+                                 n_copied);
 }
 
 extern "C" apex_status apex_expert_fetch_misses(

@@ -202,6 +202,24 @@ def test_decode_deepseek_shape_with_shared_experts(batch, mode):
     assert st["ffn_checked"] > 0
 
 
+SMALL_SHARED = configs.MoEConfig("small_shared", 421, L=2, d=512, E=16, k=4, I=256, C=8,
+                                k_max=8, tau=0.9, steps=8, shared=2)
+
+
+@pytest.mark.parametrize("mode", [native.MODE_EXACT, native.MODE_STALL_FREE])
+def test_decode_small_experts_with_shared_experts(mode):
+    # experts of 0.79 MB (short copies) with two shared experts, which run on the side
+    # stream while a layer-step's copies are in flight and are waited for with an event;
+    # parity with records, then the unrecorded timeline against the recorded one
+    cfg = SMALL_SHARED
+    st = check_decode(cfg, 1, mode, cfg.steps, [0, 1])
+    assert st["copies"] > 0 and st["ffn_checked"] > 0
+    (y_free, c_free), (y_rec, c_rec) = run_unrecorded_and_recorded(cfg, 1, mode, cfg.steps,
+                                                                    [0, 1])
+    assert c_free == c_rec
+    assert np.abs(y_free - y_rec).max() <= 1e-5 * np.abs(y_rec).max()
+
+
 def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers):
     """Final outputs and counters of the same decode without and with per-layer records."""
     from paper_2608_11688_amd.runtime import DecodeRunner
