@@ -14,11 +14,15 @@ block's measured device time): the MoE path's own cost including exposed stall; 
 is better.  The same timeline with every expert resident in HBM (no copies, no misses)
 is timed after it; the difference is the exposed stall.
 
-    python bench.py [--steps K] [--warmup W] [--config granite-1b-a400m] [--batch 1]
+    python bench.py [--steps K] [--warmup W] [--config mixtral-8x7b] [--batch 1]
                     [--mode exact|stall_free] [--policy cumprob|ordinal|static|none]
                     [--static-delta D] [--tau T] [--weights bf16|fp8|mxfp4]
                     [--window spin|attention] [--t-attn-us 10] [--ctx 1024]
                     [--no-compute-only] [--no-cpu-baseline]
+
+The default workload is the largest that fits one GPU: eight Mixtral-8x7B-shaped MoE
+layers (d 4096, 8 experts of intermediate size 14336, top-2, 4 experts resident per
+layer), batch 1, bf16 experts, correctness-preserving mode.
 
 With --policy ordinal, every layer's coverage model is first fitted on held-out tokens
 (the method's training stage, outside the timed region).
@@ -26,6 +30,8 @@ With --policy ordinal, every layer's coverage model is first fitted on held-out 
 from __future__ import annotations
 
 import argparse
+import concurrent.futures as cf
+import gc
 import json
 import os
 import sys
@@ -46,7 +52,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=128)
     p.add_argument("--warmup", type=int, default=8)
-    p.add_argument("--config", default="granite-1b-a400m")
+    p.add_argument("--config", default="mixtral-8x7b")
     p.add_argument("--batch", type=int, default=1)
     p.add_argument("--mode", default="exact", choices=["exact", "stall_free"])
     p.add_argument("--tau", type=float, default=None)
@@ -309,11 +315,13 @@ def time_steps(torch, runner, steps, warmup):
     return (t1 - t0) * 1e3 / steps
 
 
-def compute_only_leg(torch, args, cfg, make_runner):
+def compute_only_leg(torch, args, cfg, make_runner, host_runner):
     """The same decode with every expert resident in HBM (C = E): the same kernels, no
-    copies and no misses.  Returns ms per step."""
+    copies and no misses, over the pinned experts of `host_runner` (which stays open).
+    Returns ms per step."""
     import dataclasses
-    runner = make_runner(dataclasses.replace(cfg, C=cfg.E, k_max=min(cfg.k_max, cfg.E)))
+    runner = make_runner(dataclasses.replace(cfg, C=cfg.E, k_max=min(cfg.k_max, cfg.E)),
+                         host_experts_from=host_runner)
     try:
         return time_steps(torch, runner, args.steps, args.warmup)
     finally:
@@ -332,12 +340,33 @@ def delta_star_leg(cfg, tokens=256, max_layers=8):
                 tokens=int(d.size), layers=layers)
 
 
-def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=None,
+def oracle_sample(cfg, batch, weights, policy, cdf, preload_bytes=8e9, threads=16):
+    """The oracle's inputs for the CPU baseline, drawn before any timing, as the GPU leg's
+    are: the first layers of the workload (as many as keep the drawn bf16 experts under
+    `preload_bytes`, at most 4), their routers and every expert's weights, and the hidden
+    states of the first steps (16 for experts of 64 MB and more, else 64)."""
+    from oracle import decode
+    from paper_2608_11688_amd import inputs
+    S = 6 * cfg.d * cfg.I
+    n_layers = max(1, min(cfg.L, 4, int(preload_bytes // (cfg.E * S))))
+    layers = list(range(n_layers))
+    steps = 16 if S >= (64 << 20) else 64
+    states = decode.make_states(cfg, layers, policy=policy, cdf=cdf, weights=weights)
+    with cf.ThreadPoolExecutor(threads) as pool:
+        list(pool.map(lambda le: states[le[0]].expert_bits(le[1]),
+                      [(l, e) for l in layers for e in range(cfg.E)]))
+    hidden = {l: inputs.hidden_states(cfg, l, batch, steps) for l in layers}
+    return dict(layers=layers, steps=steps, states=states, hidden=hidden)
+
+
+def cpu_baseline(cfg, batch, mode, tau, budget_s, sample, policy=0, static_delta=0, cdf=None,
                  weights="bf16", threads_limit=None):
-    """The oracle, as it stands, on the first layer-steps of the same workload; with
-    threads_limit, under that many BLAS threads.  Also counts the near ties the oracle
-    finds in the sample (decision margins below 1e-5 at the gate's top-k cut and at the
-    prefetch selection's cut), the points where a GPU set may differ legitimately."""
+    """The oracle, as it stands, on the first layer-steps of the same workload, over the
+    inputs of `sample` (oracle_sample: drawn beforehand, so the timed region holds the
+    oracle's own arithmetic only); with threads_limit, under that many BLAS threads.  Also
+    counts the near ties the oracle finds in the sample (decision margins below 1e-5 at the
+    gate's top-k cut and at the prefetch selection's cut), the points where a GPU set may
+    differ legitimately."""
     from oracle import decode
     import contextlib
     try:
@@ -346,21 +375,24 @@ def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=
                  else contextlib.nullcontext())
     except Exception:
         threadpoolctl, limit = None, contextlib.nullcontext()
-    layers = list(range(min(cfg.L, 4)))
-    steps = 64
-    n, elapsed, gate_ties, cut_ties, rows = 0, 0.0, 0, 0, 0
+    layers, steps = sample["layers"], sample["steps"]
+    # fresh caches for every timed run, the drawn weights shared
+    states = decode.make_states(cfg, layers, policy=policy, cdf=cdf, weights=weights,
+                                bits_from=sample["states"])
+    n, elapsed, gate_ties, cut_ties, rows, t_last = 0, 0.0, 0, 0, 0, 0
     with limit:
         threads = 1
         if threadpoolctl is not None:
             threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()),
                           default=1)
         gen = decode.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers, policy=policy,
-                         static_delta=static_delta, cdf=cdf, weights=weights)
-        # timed as the oracle runs: its seeded input generation is inside the sample
+                         static_delta=static_delta, cdf=cdf, weights=weights, states=states,
+                         hidden=sample["hidden"])
         it = iter(gen)
         t0 = time.perf_counter()
         for t, l, out in it:
             n += 1
+            t_last = t
             gate_ties += int((out["gate"]["margin"] < 1e-5).sum())
             cut_ties += int((out["route"]["margin"] < 1e-5).sum())
             rows += len(out["gate"]["margin"])
@@ -370,11 +402,24 @@ def cpu_baseline(cfg, batch, mode, tau, budget_s, policy=0, static_delta=0, cdf=
     base = dict(value=elapsed * 1e6 / (n * batch), unit="us/token/layer", cores=int(threads),
                 kind="oracle",
                 sample=f"{cfg.name} batch {batch} {['exact', 'stall_free'][mode]} mode, first {n} "
-                       f"layer-steps (layers {layers[0]}-{layers[-1]}, steps from 0), fp64 "
-                       f"NumPy, includes seeded weight generation of the experts it touches")
+                       f"layer-steps (steps 0-{t_last} of layers {layers[0]}-{layers[-1]}), fp64 "
+                       f"NumPy; hidden states, routers and expert weights drawn before timing")
     ties = dict(token_layers=rows, gate_cut=gate_ties, prefetch_cut=cut_ties, margin_below=1e-5,
                 sample=f"the oracle's {n} layer-steps above")
     return base, ties
+
+
+def release(torch):
+    """Waits for the device and returns every cached block, so that nothing this process
+    allocated on the GPU or in pinned memory is left for interpreter and library teardown."""
+    torch.cuda.synchronize()
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    try:
+        torch._C._host_emptyCache()
+    except Exception:
+        pass
 
 
 def main():
@@ -399,11 +444,11 @@ def main():
         cdf, cdf_report = cdf_fit.fit_model(cfg, tokens=args.cdf_tokens)
     total = args.warmup + args.steps
 
-    def make_runner(c):
+    def make_runner(c, **kw):
         return DecodeRunner(c, batch=args.batch, mode=mode, tau=tau, steps=max(total, 1),
                             t_attn_us=args.t_attn_us, policy=policy,
                             static_delta=args.static_delta, cdf=cdf, weights=args.weights,
-                            window=args.window, ctx=args.ctx)
+                            window=args.window, ctx=args.ctx, **kw)
 
     runner = make_runner(cfg)
     h2d_peak = pinned_h2d_peak(torch)
@@ -422,15 +467,17 @@ def main():
     s = runner.summary()
     warm = runner.warmup_summary
     copied_bytes_per_step = s["copies_per_layer_step"] * L * S
-    runner.close()
-    copy_leg = expert_copy_leg(torch, native, S, cfg.E, h2d_peak)
     # exposed stall: this timeline against the same one with every expert resident
     value_resident = stall = None
     if not args.no_compute_only:
-        ms_res = compute_only_leg(torch, args, cfg, make_runner)
+        ms_res = compute_only_leg(torch, args, cfg, make_runner, runner)
         value_resident = (ms_res * 1e3 / L - window_us) / B
         stall = value - value_resident
+    runner.close()
+    del runner
+    copy_leg = expert_copy_leg(torch, native, S, cfg.E, h2d_peak)
     dstar = delta_star_leg(cfg)
+    release(torch)
     out = {
         "metric": "MoE-layer decode us/token + expert-weight HBM GB/s; prefetch recall vs oracle",
         "value": round(value, 3),
@@ -495,12 +542,15 @@ def main():
     if cdf_report is not None:
         out["ordinal_fit"] = cdf_report
     if not args.no_cpu_baseline:
+        sample = oracle_sample(cfg, B, args.weights, policy, cdf)
         out["cpu_baseline"], out["oracle_near_ties"] = cpu_baseline(
-            cfg, B, mode, tau, args.cpu_budget_s, policy, args.static_delta, cdf, args.weights)
+            cfg, B, mode, tau, args.cpu_budget_s, sample, policy, args.static_delta, cdf,
+            args.weights)
         if args.cpu_1thread_budget_s > 0:
             out["cpu_baseline_1thread"], _ = cpu_baseline(
-                cfg, B, mode, tau, args.cpu_1thread_budget_s, policy, args.static_delta, cdf,
-                args.weights, threads_limit=1)
+                cfg, B, mode, tau, args.cpu_1thread_budget_s, sample, policy, args.static_delta,
+                cdf, args.weights, threads_limit=1)
+        del sample
     print(json.dumps(out), flush=True)
     return 0
 

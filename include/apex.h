@@ -151,7 +151,7 @@ apex_status apex_pack_expert(const uint16_t *w1, const uint16_t *w3, const uint1
                              int d, int I, uint16_t *out);
 
 /*
- * Experts with 8-bit weights (the precision study of Sec. V-H: smaller experts move
+ * Experts with 8-bit weights (the precision study of Sec. V-G: smaller experts move
  * fewer bytes over the host link and out of HBM).  Weights are OCP E4M3 codes (1 sign,
  * 4 exponent bits with bias 7, 3 mantissa bits; no infinities; largest value 448) with
  * one fp32 scale per output row: row r of W1, W3 or W2 is s_r * q, where
@@ -168,7 +168,7 @@ apex_status apex_pack_expert_fp8(const uint16_t *w1, const uint16_t *w3, const u
                                  int d, int I, void *out);
 
 /*
- * Experts with 4-bit weights (the precision study of Sec. V-H), in the OCP MXFP4 form:
+ * Experts with 4-bit weights (the precision study of Sec. V-G), in the OCP MXFP4 form:
  * FP4 E2M1 codes (1 sign, 2 exponent bits with bias 1, 1 mantissa bit: magnitudes 0,
  * 0.5, 1, 1.5, 2, 3, 4, 6), two per byte with element 2j in the low nibble of byte j,
  * and one power-of-two scale 2^X per block of 32 consecutive values of a row (along the
@@ -375,9 +375,11 @@ apex_status apex_expert_fetch_misses(const uint16_t *host_experts, uint16_t *scr
  *            the slot table on side);
  *   side:    apex_gate_topk; the shared experts, if any (apex_moe_ffn over the layer's
  *            shared pool, every token, weight 1);
- *   EXACT:   host waits for the gate, apex_expert_fetch_misses (copies on compute);
  *   compute: after the gate (and the shared experts): apex_moe_ffn pass 1 (added to the
- *            shared experts' output) and, if any expert was missing, pass 2 (accumulate).
+ *            shared experts' output);
+ *   EXACT:   host waits for the gate; apex_expert_fetch_misses copies the missing
+ *            experts on side while pass 1 runs, and, if any expert was missing, pass 2
+ *            (accumulate) runs on compute after an event recorded behind that copy.
  * The copies, the FFN and the next layer's router follow each other on the compute
  * stream with no event between them, so a layer's router starts after the previous
  * layer's FFN, as in a model where each layer feeds the next, and the copies of a layer
@@ -441,7 +443,8 @@ typedef struct {   /* counters the driver adds to at every layer-step */
     double overlap_sum;        /* sum over tokens of |K_r & K_p| / k (Sec. V-C overlap) */
     double hit_sum;            /* sum over tokens of |K_r & resident| / k */
     int64_t coverage_count;    /* tokens with K_r subset of K_p (Eq. 2) */
-    int64_t delta_hat_sum;     /* sum of m - k */
+    int64_t delta_hat_sum;     /* sum of max(m - k, 0): delta_hat of Eq. 9 (0 when nothing
+                                  is prefetched, APEX_SEL_NONE) */
     int64_t tokens, layer_steps, copies, misses;
 } apex_decode_stats;
 

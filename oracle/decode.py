@@ -24,7 +24,10 @@ from .residency import Residency
 
 
 class LayerState:
-    def __init__(self, cfg, layer, seed=0, policy=routing.CUMPROB, cdf=None, weights="bf16"):
+    def __init__(self, cfg, layer, seed=0, policy=routing.CUMPROB, cdf=None, weights="bf16",
+                 bits=None):
+        """bits: an already drawn {expert: weights} dict of the same layer and seed to use
+        (and add to) instead of a new one."""
         self.cfg, self.layer = cfg, layer
         self.wg, self.wpf, self.bias = inputs.router_weights(cfg, layer, seed)
         self.res = Residency(cfg.E, cfg.C)
@@ -32,7 +35,7 @@ class LayerState:
         self.policy = policy
         self.cdf = cdf if cdf is not None else (None, None)
         self.weights = weights
-        self._bits = {}
+        self._bits = {} if bits is None else bits
 
     def expert_bits(self, e):
         if e not in self._bits:
@@ -78,25 +81,41 @@ def layer_step(st: LayerState, t, h_pre, h_post, mode, tau, static_delta=0, run_
         overlap=[metrics.overlap(g["route_idx"][b], pf_lists[b], cfg.k) for b in range(B)],
         coverage=[metrics.full_coverage(g["route_idx"][b], pf_lists[b]) for b in range(B)],
         delta_star=[metrics.delta_star(r["ranked"][b], g["route_idx"][b], cfg.k) for b in range(B)],
-        delta_hat=[int(r["pf_count"][b]) - cfg.k for b in range(B)],
+        # Eq. 9: delta_hat lies in 0..N-k; the no-prefetch baseline takes no extra experts
+        delta_hat=[max(int(r["pf_count"][b]) - cfg.k, 0) for b in range(B)],
         hits=[len(set(int(e) for e in g["route_idx"][b]) & R) / cfg.k for b in range(B)],
         copies=len(copies), misses=len(misses),
     )
     return dict(route=r, gate=g, copies=copies, resident=R, misses=misses, y=y, metrics=m)
 
 
+def make_states(cfg, layers, seed=0, policy=routing.CUMPROB, cdf=None, weights="bf16",
+                bits_from=None):
+    """One LayerState per layer (the per-layer routers, cache and expert weights), each
+    with an empty cache; bits_from: states of the same layers and seed whose drawn expert
+    weights the new states share."""
+    return {l: LayerState(cfg, l, seed, policy, None if cdf is None else cdf[l], weights,
+                          None if bits_from is None else bits_from[l]._bits)
+            for l in layers}
+
+
 def run(cfg, batch, steps, mode=gating.EXACT, tau=None, seed=0, layers=None, run_ffn=True,
-        policy=routing.CUMPROB, static_delta=0, cdf=None, weights="bf16"):
+        policy=routing.CUMPROB, static_delta=0, cdf=None, weights="bf16", states=None,
+        hidden=None):
     """Replay ``steps`` decode steps of ``batch`` tokens; yields (t, layer, result).
 
     cdf: {layer: (w, theta)} ordinal-model parameters when policy is ORDINAL_CDF;
-    weights: "bf16" or "fp8" expert weights (see ``ffn``).
+    weights: "bf16", "fp8" or "mxfp4" expert weights (see ``ffn``);
+    states, hidden: the layers' states (``make_states``) and hidden states
+    ({layer: (h_pre, h_post)} from the seeded generator) when the caller has drawn them
+    already; drawn here otherwise.
     """
     tau = cfg.tau if tau is None else tau
     layers = range(cfg.L) if layers is None else layers
-    states = {l: LayerState(cfg, l, seed, policy, None if cdf is None else cdf[l], weights)
-              for l in layers}
-    hs = {l: inputs.hidden_states(cfg, l, batch, steps, seed) for l in layers}
+    if states is None:
+        states = make_states(cfg, layers, seed, policy, cdf, weights)
+    hs = hidden if hidden is not None else {
+        l: inputs.hidden_states(cfg, l, batch, steps, seed) for l in layers}
     for t in range(steps):
         for l in layers:
             h_pre, h_post = hs[l][0][t], hs[l][1][t]

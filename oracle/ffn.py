@@ -9,7 +9,7 @@ Reading: the expert FFN is SwiGLU without biases, FFN(x) = W2 (silu(W1 x) * (W3 
 silu(u) = u / (1 + exp(-u)), as the workload definitions state.
 
 With weights="fp8" every expert matrix is first quantised row by row to E4M3 with an
-fp32 scale per row (``fp8``, the reading taken for the precision study of Sec. V-H) and
+fp32 scale per row (``fp8``, the reading taken for the precision study of Sec. V-G) and
 the FFN runs on the dequantised values s_r * q, in float64.  With weights="mxfp4" every
 row is quantised in blocks of 32 along the reduction dimension to E2M1 codes with a
 power-of-two scale per block (``mxfp4``) and the FFN runs on 2^X * q.

@@ -7,7 +7,7 @@ bits with bias 7, three mantissa bits.  Exponent field 0 holds the subnormals m/
 exponent field 15 with mantissa 7 is NaN; there are no infinities, so the largest
 finite magnitude is 1.75 * 2^8 = 448.
 
-Quantisation follows the precision study of Sec. V-H, which only scales the bytes of
+Quantisation follows the precision study of Sec. V-G, which only scales the bytes of
 every expert; the format and the scaling are this implementation's reading: each output
 row r of W1, W3 and W2 gets s_r = fp32(max |W[r, :]| / 448) and codes q = the E4M3 value
 nearest to W[r, :] / s_r (ties to the even code, sign bit set for negative inputs), so

@@ -8,7 +8,7 @@ bit, two exponent bits with bias 1 and one mantissa bit; exponent field 0 holds 
 subnormal 0.5 * m, so the magnitudes are 0, 0.5, 1, 1.5, 2, 3, 4 and 6.  A block of 32
 consecutive values shares an E8M0 scale 2^X (the byte X + 127).
 
-Quantisation follows the precision study of Sec. V-H, which only scales the bytes of
+Quantisation follows the precision study of Sec. V-G, which only scales the bytes of
 every expert; the format is this implementation's reading (4-bit weights in the form
 gfx950 converts in hardware), with the MX specification's conversion: for each block,
 X = floor(log2(max |v|)) - 2 (2 being the largest exponent of E2M1), and every element

@@ -65,23 +65,30 @@ def logit(tau: float) -> float:
 def select_cumprob(q_ranked, k: int, k_max: int, tau: float):
     """Smallest m whose ranked prefix mass reaches tau, clamped to [k, k_max].
 
-    Returns (m, margin) where margin = distance of the deciding prefix sums from tau.
+    With S_j the mass of the first j ranked experts, the clamped m depends only on the
+    comparisons S_j >= tau for j = k .. k_max - 1: m = k if S_k >= tau, else the first
+    such j, else k_max.  Returns (m, margin), margin = the smallest |S_j - tau| among the
+    comparisons that decide m (j from k up to min(m, k_max - 1)); infinite when the clamp
+    alone fixes m (k = k_max).
     """
     E = len(q_ranked)
     s = 0.0
-    prev = 0.0
     m_star = E
-    margin = math.inf
+    prefix = []
     for i in range(E):
         s += float(q_ranked[i])
+        prefix.append(s)
         if s >= tau:
             m_star = i + 1
-            margin = min(s - tau, tau - prev)
             break
-        prev = s
-    else:
-        margin = abs(tau - s)          # tau not reached: every prefix stays below
     m = min(max(m_star, k), k_max)
+    margin = math.inf
+    for j in range(k, min(m, k_max - 1) + 1):
+        if j > len(prefix):            # the crossing came earlier: S_j >= S_m* >= tau
+            s_j = sum(float(q) for q in q_ranked[:j])
+        else:
+            s_j = prefix[j - 1]
+        margin = min(margin, abs(s_j - tau))
     return m, margin
 
 
@@ -89,21 +96,24 @@ def select_ordinal(q_ranked, cdf_w, cdf_theta, k: int, k_max: int, tau: float):
     """Eq. 8-9: delta_hat = min{delta in 0..N-k : sigmoid(theta_delta - w.x) >= tau}.
 
     x = the prefetch probabilities in ranked (descending) order.  sigmoid(a) >= tau is
-    tested as a >= logit(tau) (sigmoid is increasing).  Returns (m, delta_hat, margin).
+    tested as a >= logit(tau) (sigmoid is increasing).  m = min(k + delta_hat, k_max)
+    depends only on the tests for delta = 0 .. k_max - k - 1.  Returns (m, delta_hat,
+    margin), margin = the smallest |theta_delta - w.x - logit(tau)| among the tests that
+    decide m (delta up to min(delta_hat, k_max - k - 1)).
     """
     E = len(q_ranked)
     s = float(np.dot(np.asarray(cdf_w, dtype=np.float64), np.asarray(q_ranked, dtype=np.float64)))
     thr = logit(tau)
     delta_hat = E - k
-    margin = math.inf
     for delta in range(E - k + 1):
-        a = float(cdf_theta[delta]) - s
-        if math.isfinite(thr):
-            margin = min(margin, abs(a - thr))
-        if a >= thr:
+        if float(cdf_theta[delta]) - s >= thr:
             delta_hat = delta
             break
     m = min(k + delta_hat, k_max)
+    margin = math.inf
+    if math.isfinite(thr):
+        for delta in range(0, min(delta_hat, k_max - k - 1) + 1):
+            margin = min(margin, abs(float(cdf_theta[delta]) - s - thr))
     return m, delta_hat, margin
 
 

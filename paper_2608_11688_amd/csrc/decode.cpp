@@ -15,12 +15,14 @@
 // gate (and the shared experts).  The host orders the two through the flags: it enqueues
 // the side stream's work once it has seen the router's flags (the router follows the
 // previous layer's FFN, so that FFN is done too), and the FFN once it has seen the
-// gate's, where the FFN queues behind the copies still in flight.  Slot and scratch reuse
-// needs no event: a layer's copies follow, on the compute stream, every earlier kernel
-// that read those slots.  Only the shared experts, which publish no flag, are waited for
-// with an event.  A layer-step that copies nothing keeps all of its work on the compute
-// stream: with no copy to hide behind, the hand-offs between streams would only add
-// their latency.
+// gate's, where the FFN queues behind the copies still in flight.  Slot reuse needs no
+// event: a layer's copies follow, on the compute stream, every earlier kernel that read
+// those slots.  Only the shared experts, which publish no flag, and the miss
+// copy of the correctness-preserving mode are waited for with an event: the missing
+// experts travel on the side stream while the first FFN pass runs, and the second pass
+// waits for them.  A layer-step that copies nothing else keeps its other work on the
+// compute stream: with no copy to hide behind, the hand-offs between streams would only
+// add their latency.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -64,10 +66,13 @@ struct apex_decode {
     int32_t seq = 0;
     // event after the shared experts (side stream)
     hipEvent_t shared_done = nullptr;
+    // event after a layer-step's miss copy (side stream), waited for by the second pass
+    hipEvent_t miss_ready = nullptr;
     // statistics of layers whose gate may still be running
     struct Pending {
         int layer;
         int32_t seq;                   // the layer-step's sequence number
+        hipStream_t gate_stream;       // the stream the layer-step's gate ran on
         std::vector<int32_t> pf;       // [B][k_max]
         std::vector<int32_t> cnt;      // [B]
         std::vector<char> resident;    // [E]
@@ -119,7 +124,9 @@ void fold(apex_decode *dec, const apex_decode::Pending &p, apex_decode_stats *st
         st->overlap_sum += double(both) / c.k;
         st->hit_sum += double(hit) / c.k;
         st->coverage_count += both == c.k ? 1 : 0;
-        st->delta_hat_sum += p.cnt[b] - c.k;
+        // delta_hat in [0, E - k] (Eq. 9); the no-prefetch baseline fetches no extra
+        // experts, so its empty prefetched set counts 0
+        st->delta_hat_sum += std::max(p.cnt[b] - c.k, 0);
     }
     st->tokens += c.B;
     st->layer_steps += 1;
@@ -157,7 +164,7 @@ apex_status fold_pending(apex_decode *dec, apex_decode_stats *st) {
     const int B = dec->cfg.B;
     for (const auto &p : dec->pending) {
         const apex_status s = poll_done(dec->gate_done_h + size_t(p.layer) * B, B, p.seq,
-                                        dec->side);
+                                        p.gate_stream);
         if (s != APEX_OK) return s;
         fold(dec, p, st);
     }
@@ -279,7 +286,7 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     auto mk = [&](hipEvent_t *ev) {
         return hipEventCreateWithFlags(ev, hipEventDisableTiming);
     };
-    if (mk(&dec->shared_done) != hipSuccess)
+    if (mk(&dec->shared_done) != hipSuccess || mk(&dec->miss_ready) != hipSuccess)
         return cleanup(apex::fail(APEX_E_HIP, "%s: event creation failed", fn));
     if (c.n_shared > 0) {
         const size_t pairs = size_t(c.B) * c.n_shared;
@@ -375,6 +382,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         apex_decode::Pending p;
         p.layer = l;
         p.seq = seq;
+        p.gate_stream = ws;
         p.pf.assign(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max);
         p.cnt.assign(dec->pf_count_h, dec->pf_count_h + c.B);
         p.resident.assign(c.E, 0);
@@ -424,22 +432,27 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
             st = poll_done(gate_flags, c.B, seq, ws);
             if (st != APEX_OK) return st;
         }
-        int n_miss = 0;
-        if (c.mode == APEX_MODE_EXACT) {
-            // asynchronous miss correction: the misses queue behind the prefetch copies
-            st = apex_expert_fetch_misses(Ly.host_experts, dec->scratch, c.n_scratch, c.E, c.C,
-                                          dec->expert_bytes, route_h, c.B, c.k,
-                                          Ly.expert_of_slot, dec->miss_table, cs, cs, nullptr,
-                                          nullptr, missing.data(), &n_miss);
-            if (st != APEX_OK) return st;
-        }
         if (split) {
             // the routed experts once the copies landed (stream order)
             if (shared) APEX_HIP(hipStreamWaitEvent(cs, dec->shared_done, 0));
             st = ffn(dec, h_post[l], Ly.slot_of_expert_dev, Ly.slots, c.C, y[l], acc);
             if (st != APEX_OK) return st;
         }
+        int n_miss = 0;
+        if (c.mode == APEX_MODE_EXACT) {
+            // asynchronous miss correction (Sec. IV-E): the missing experts are copied on
+            // the side stream while the first pass runs on the compute stream; the second
+            // pass waits for the copy's event.  The scratch pool is free: the host got here
+            // after seeing the flags of this layer-step's router or gate, kernels that
+            // follow the previous second pass on the compute stream.
+            st = apex::fetch_misses(Ly.host_experts, dec->host_view[l], dec->scratch,
+                                    c.n_scratch, c.E, c.C, dec->expert_bytes, route_h, c.B, c.k,
+                                    Ly.expert_of_slot, dec->miss_table, ss, cs, nullptr,
+                                    dec->miss_ready, missing.data(), &n_miss);
+            if (st != APEX_OK) return st;
+        }
         if (n_miss > 0) {
+            APEX_HIP(hipStreamWaitEvent(cs, dec->miss_ready, 0));
             st = ffn(dec, h_post[l], dec->miss_table, dec->scratch, c.n_scratch, y[l], 1);
             if (st != APEX_OK) return st;
         }
@@ -477,6 +490,7 @@ extern "C" apex_status apex_decode_destroy(apex_decode *dec) {
     if (dec->compute) (void)hipStreamSynchronize(dec->compute);
     if (dec->side) (void)hipStreamSynchronize(dec->side);
     if (dec->shared_done) (void)hipEventDestroy(dec->shared_done);
+    if (dec->miss_ready) (void)hipEventDestroy(dec->miss_ready);
     for (void *p : {static_cast<void *>(dec->pf_idx_h), static_cast<void *>(dec->pf_count_h),
                     static_cast<void *>(dec->route_idx_h), static_cast<void *>(dec->route_gate_h),
                     static_cast<void *>(dec->route_done), static_cast<void *>(dec->gate_done_h)})

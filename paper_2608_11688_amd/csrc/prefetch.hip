@@ -186,22 +186,12 @@ extern "C" apex_status apex_expert_prefetch(
                                  n_copied);
 }
 
-extern "C" apex_status apex_expert_fetch_misses(
-    const uint16_t *host_experts, uint16_t *scratch, int n_scratch, int E, int C,
-    size_t expert_bytes, const int32_t *route_idx, int B, int k, const int32_t *expert_of_slot,
-    int32_t *miss_table_dev, hipStream_t side, hipStream_t compute, hipEvent_t scratch_free,
-    hipEvent_t ready, int32_t *missing, int *n_missing) {
+apex_status apex::fetch_misses(const uint16_t *host_experts, const uint4 *src, uint16_t *scratch,
+                              int n_scratch, int E, int C, size_t expert_bytes, const int32_t *route_idx, int B, int k,
+                              const int32_t *expert_of_slot, int32_t *miss_table_dev,
+                              hipStream_t side, hipStream_t compute, hipEvent_t scratch_free,
+                              hipEvent_t ready, int32_t *missing, int *n_missing) {
     const char *fn = "apex_expert_fetch_misses";
-    APEX_REQUIRE(host_experts && scratch && expert_of_slot && miss_table_dev && n_missing,
-                 "%s: NULL pointer", fn);
-    APEX_REQUIRE(E >= 1 && E <= APEX_MAX_EXPERTS, "%s: E=%d out of [1, 64]", fn, E);
-    APEX_REQUIRE(C >= 1, "%s: C=%d must be >= 1", fn, C);
-    APEX_REQUIRE(n_scratch >= 0, "%s: n_scratch=%d < 0", fn, n_scratch);
-    APEX_REQUIRE(B >= 0 && k >= 1 && k <= E, "%s: B=%d k=%d", fn, B, k);
-    APEX_REQUIRE(B == 0 || route_idx, "%s: NULL route_idx", fn);
-    APEX_REQUIRE(expert_bytes > 0 && expert_bytes % 16 == 0 && expert_bytes / 16 <= UINT32_MAX,
-                 "%s: expert_bytes=%zu must be a positive multiple of 16 below 64 GiB", fn,
-                 expert_bytes);
     bool resident[APEX_MAX_EXPERTS] = {false};
     for (int s = 0; s < C; ++s) {
         const int e = expert_of_slot[s];
@@ -221,11 +211,11 @@ extern "C" apex_status apex_expert_fetch_misses(
     if (n > n_scratch)
         return apex::fail(APEX_E_CAPACITY, "%s: %d missing experts > %d scratch slots", fn, n,
                           n_scratch);
-
-    const uint4 *src = nullptr;
-    apex_status st = apex::pinned_device_view(fn, host_experts, size_t(E) * expert_bytes, &src);
-    if (st != APEX_OK) return st;
-
+    apex_status st = APEX_OK;
+    if (!src) {
+        st = apex::pinned_device_view(fn, host_experts, size_t(E) * expert_bytes, &src);
+        if (st != APEX_OK) return st;
+    }
     if (missing)
         for (int i = 0; i < n; ++i) missing[i] = list[i];
     *n_missing = n;
@@ -245,4 +235,25 @@ extern "C" apex_status apex_expert_fetch_misses(
     std::fill(t.slot, t.slot + APEX_MAX_EXPERTS, -1);
     for (int i = 0; i < n; ++i) t.slot[list[i]] = i;
     return publish(t, E, miss_table_dev, nullptr, compute);
+}
+
+extern "C" apex_status apex_expert_fetch_misses(
+    const uint16_t *host_experts, uint16_t *scratch, int n_scratch, int E, int C,
+    size_t expert_bytes, const int32_t *route_idx, int B, int k, const int32_t *expert_of_slot,
+    int32_t *miss_table_dev, hipStream_t side, hipStream_t compute, hipEvent_t scratch_free,
+    hipEvent_t ready, int32_t *missing, int *n_missing) {
+    const char *fn = "apex_expert_fetch_misses";
+    APEX_REQUIRE(host_experts && scratch && expert_of_slot && miss_table_dev && n_missing,
+                 "%s: NULL pointer", fn);
+    APEX_REQUIRE(E >= 1 && E <= APEX_MAX_EXPERTS, "%s: E=%d out of [1, 64]", fn, E);
+    APEX_REQUIRE(C >= 1, "%s: C=%d must be >= 1", fn, C);
+    APEX_REQUIRE(n_scratch >= 0, "%s: n_scratch=%d < 0", fn, n_scratch);
+    APEX_REQUIRE(B >= 0 && k >= 1 && k <= E, "%s: B=%d k=%d", fn, B, k);
+    APEX_REQUIRE(B == 0 || route_idx, "%s: NULL route_idx", fn);
+    APEX_REQUIRE(expert_bytes > 0 && expert_bytes % 16 == 0 && expert_bytes / 16 <= UINT32_MAX,
+                 "%s: expert_bytes=%zu must be a positive multiple of 16 below 64 GiB", fn,
+                 expert_bytes);
+    return apex::fetch_misses(host_experts, nullptr, scratch, n_scratch, E, C, expert_bytes,
+                              route_idx, B, k, expert_of_slot, miss_table_dev, side, compute,
+                              scratch_free, ready, missing, n_missing);
 }

@@ -23,4 +23,14 @@ apex_status expert_prefetch(const uint4 *src, uint16_t *slots, int E, int C, siz
                             hipEvent_t readers_done, hipEvent_t ready, int32_t *copied_experts,
                             int *n_copied);
 
+// apex_expert_fetch_misses after argument checks, reading the experts at the device view
+// `src` (the decode driver keeps one per layer, so no pointer query per call); with src
+// NULL the view of host_experts is looked up (and pageable memory refused) after the
+// capacity check.
+apex_status fetch_misses(const uint16_t *host_experts, const uint4 *src, uint16_t *scratch,
+                         int n_scratch, int E, int C, size_t expert_bytes, const int32_t *route_idx, int B, int k,
+                         const int32_t *expert_of_slot, int32_t *miss_table_dev,
+                         hipStream_t side, hipStream_t compute, hipEvent_t scratch_free,
+                         hipEvent_t ready, int32_t *missing, int *n_missing);
+
 }  // namespace apex

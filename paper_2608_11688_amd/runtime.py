@@ -45,7 +45,10 @@ class DecodeRunner:
     def __init__(self, cfg: configs.MoEConfig, batch=1, mode=EXACT, tau=None,
                  policy=native.SEL_CUMPROB, static_delta=0, seed=0, steps=None, t_attn_us=10.0,
                  layers=None, n_scratch=None, record=False, cdf=None, gen_threads=16,
-                 weights="bf16", window="spin", ctx=1024):
+                 weights="bf16", window="spin", ctx=1024, host_experts_from=None):
+        """host_experts_from: another runner of the same workload, layers and weight
+        format whose pinned host experts this one uses instead of drawing and pinning its
+        own (the other runner must stay open while this one runs)."""
         torch = _torch()
         self.torch = torch
         self.cfg, self.B, self.mode = cfg, batch, mode
@@ -69,10 +72,17 @@ class DecodeRunner:
         self.n_scratch = min(E, B * k) if n_scratch is None else n_scratch
         L = len(self.layers)
 
+        if host_experts_from is not None:
+            o = host_experts_from
+            if (o.cfg.d, o.cfg.I, o.cfg.E, o.weights, o.seed) != (cfg.d, cfg.I, cfg.E, weights,
+                                                                   seed) or \
+                    not set(self.layers) <= set(o.bufs):
+                raise ValueError("host_experts_from: another workload, format or layer set")
         self.bufs = {}
         with cf.ThreadPoolExecutor(gen_threads) as pool:
             for l in self.layers:
-                self.bufs[l] = self._make_layer(l, pool, cdf)
+                shared = None if host_experts_from is None else host_experts_from.bufs[l]["host"]
+                self.bufs[l] = self._make_layer(l, pool, cdf, shared)
         i32 = dict(dtype=torch.int32, device=self.dev)
         self.exec_idx = torch.empty((B, k), **i32)
         self.exec_gate = torch.empty((B, k), dtype=torch.float32, device=self.dev)
@@ -138,19 +148,20 @@ class DecodeRunner:
     def pack(self, w1, w3, w2, d, I, out):
         self._wpack(w1, w3, w2, d, I, out)
 
-    def _make_layer(self, l, pool, cdf):
+    def _make_layer(self, l, pool, cdf, host=None):
         torch, cfg = self.torch, self.cfg
         wg, wpf, bias = inputs.router_weights(cfg, l, self.seed)
         to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
         S2 = self.S // 2
-        host = torch.empty(cfg.E * S2, dtype=torch.int16, pin_memory=True)
-        hp = host.data_ptr()
+        if host is None:
+            host = torch.empty(cfg.E * S2, dtype=torch.int16, pin_memory=True)
+            hp = host.data_ptr()
 
-        def fill(e):
-            w1, w3, w2 = inputs.expert_weights(cfg, l, e, self.seed)
-            self.pack(w1, w3, w2, cfg.d, cfg.I, hp + e * self.S)
+            def fill(e):
+                w1, w3, w2 = inputs.expert_weights(cfg, l, e, self.seed)
+                self.pack(w1, w3, w2, cfg.d, cfg.I, hp + e * self.S)
 
-        list(pool.map(fill, range(cfg.E)))
+            list(pool.map(fill, range(cfg.E)))
         slots = torch.empty(cfg.C * S2, dtype=torch.int16, device=self.dev)
         n0 = min(cfg.C, cfg.E)
         slots[:n0 * S2].copy_(host[:n0 * S2])
@@ -232,7 +243,11 @@ class DecodeRunner:
                     expert_bytes=self.S, tokens=int(s.tokens), layer_steps=int(s.layer_steps))
 
     def close(self):
+        """Destroys the driver (which first waits for both streams) and drops every
+        device and pinned buffer and the side stream this runner holds."""
         if getattr(self, "dec", None):
             native.apex_decode_destroy(self.dec)
             self.dec = None
         self.bufs = {}
+        for name in ("exec_idx", "exec_gate", "y", "ws", "scratch", "miss_table", "side"):
+            setattr(self, name, None)

@@ -2,13 +2,16 @@
 
 Index sets: bit-exact, except where the oracle's deciding margin is below TIE (a
 near tie: a logit gap, a prefix sum at tau, or an ordinal threshold); such cases are
-counted and reported, never failed.
+counted and reported.  The excuse is bounded: at every point of a test the mismatches
+excused so far may not exceed MAX_EXCUSED_FRAC of the rows checked so far (at least one
+is allowed), so a margin that comes out too small cannot silence a whole test.
 FFN outputs, per (layer, step) tile: max|y - y_ref| <= 1e-2 max|y_ref| and
 sum|y - y_ref| / sum|y_ref| <= 5e-3 (bf16 weights, fp32 accumulation).
 """
 import numpy as np
 
 TIE = 1e-5
+MAX_EXCUSED_FRAC = 0.01
 FFN_MAX_REL = 1e-2
 FFN_L1_REL = 5e-3
 
@@ -29,6 +32,11 @@ class TieLedger:
             if not np.array_equal(gpu[b], ref[b]):
                 assert near, f"{what} row {b}: gpu {gpu[b]} != oracle {ref[b]} (margin {margin[b]:.3g})"
                 self.flagged_mismatch += 1
+                assert self.flagged_mismatch <= self.limit(), (
+                    f"{what} row {b}: too many mismatches excused as near ties: {self}")
+
+    def limit(self):
+        return max(1, int(MAX_EXCUSED_FRAC * self.checked))
 
     def __repr__(self):
         return (f"TieLedger(checked={self.checked}, near_ties={self.flagged}, "

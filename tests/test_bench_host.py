@@ -40,9 +40,22 @@ def test_traffic_record_needs_the_same_source_and_flags(bench, tmp_path, monkeyp
 def test_cpu_baseline_fields(bench):
     from paper_2608_11688_amd import configs
     cfg = configs.CONFIGS["tiny"]
-    base, ties = bench.cpu_baseline(cfg, 1, 0, cfg.tau, budget_s=1.0)
+    sample = bench.oracle_sample(cfg, 1, "bf16", 0, None)
+    assert sample["layers"] == [0] and sample["steps"] == 64
+    # every expert of the sampled layers is drawn before the timed run
+    assert len(sample["states"][0]._bits) == cfg.E
+    base, ties = bench.cpu_baseline(cfg, 1, 0, cfg.tau, 1.0, sample)
     assert set(base) == {"value", "unit", "cores", "kind", "sample"}
     assert base["kind"] == "oracle" and base["unit"] == "us/token/layer" and base["value"] > 0
+    assert "drawn before timing" in base["sample"]
     assert ties["token_layers"] >= 1 and 0 <= ties["gate_cut"] <= ties["token_layers"]
-    one, _ = bench.cpu_baseline(cfg, 1, 0, cfg.tau, budget_s=0.5, threads_limit=1)
+    one, _ = bench.cpu_baseline(cfg, 1, 0, cfg.tau, 0.5, sample, threads_limit=1)
     assert one["cores"] == 1
+
+
+def test_oracle_sample_of_large_experts(bench):
+    # experts of 352 MB: two layers (under 8 GB of drawn weights), 16 steps
+    from paper_2608_11688_amd import configs
+    cfg = configs.CONFIGS["mixtral-8x7b"]
+    S = 6 * cfg.d * cfg.I
+    assert int(8e9 // (cfg.E * S)) == 2 and S >= (64 << 20)

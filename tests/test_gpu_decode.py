@@ -4,23 +4,63 @@ Teacher-forced where the result depends on history: the oracle's cache replay is
 the GPU's prefetched sets (identical to the oracle's except at counted near ties), and
 the oracle FFN is evaluated on the GPU's executed sets and gates, which are checked
 against the oracle's own separately.
+
+The driver's counters (overlap, full coverage, cache hits, delta_hat, copies, misses)
+are checked against the oracle's metric definitions (Sec. V-C overlap accuracy; Eq. 2
+full coverage; Eq. 9 delta_hat) on the oracle's own sets: exactly, except that each
+(token, layer) row where a near tie let the GPU's sets differ may move each sum by at
+most one.
 """
 import numpy as np
 import pytest
 
 from oracle import decode as odecode
 from oracle import ffn as offn
-from oracle import gating, routing
+from oracle import gating, metrics, routing
 from oracle.residency import Residency
 from paper_2608_11688_amd import configs, inputs, native
-from tests.parity import TieLedger, ffn_close
+from tests.parity import TIE, TieLedger, ffn_close
+
+
+class Counters:
+    """The driver's apex_decode_stats, accumulated from the oracle's metric functions."""
+
+    FIELDS = ("tokens", "layer_steps", "copies", "misses", "coverage_count", "delta_hat_sum",
+              "overlap_sum", "hit_sum")
+
+    def __init__(self):
+        self.v = dict.fromkeys(self.FIELDS, 0)
+        self.v["overlap_sum"] = self.v["hit_sum"] = 0.0
+        self.loose_rows = 0        # rows whose sets may differ from the GPU's (near ties)
+
+    def add_layer_step(self, k, pf_lists, route_idx, resident, copies, misses):
+        for b, pf in enumerate(pf_lists):
+            routed = [int(e) for e in route_idx[b]]
+            self.v["overlap_sum"] += metrics.overlap(routed, pf, k)
+            self.v["coverage_count"] += int(metrics.full_coverage(routed, pf))
+            self.v["hit_sum"] += len(set(routed) & set(resident)) / k
+            self.v["delta_hat_sum"] += max(len(pf) - k, 0)
+            self.v["tokens"] += 1
+        self.v["layer_steps"] += 1
+        self.v["copies"] += copies
+        self.v["misses"] += misses
+
+    def check(self, stats, what=""):
+        got = {f: getattr(stats, f) for f in self.FIELDS}
+        slack = self.loose_rows
+        for f in self.FIELDS:
+            tol = slack + (1e-9 * max(1, self.v["tokens"]) if f.endswith("_sum") else 0)
+            assert abs(got[f] - self.v[f]) <= tol, (what, f, got[f], self.v[f], slack)
+        return got
 
 pytestmark = pytest.mark.gpu
 
 
 def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau=None,
-                 ffn_every=1, cdf=None, weights="bf16", window="spin"):
-    """cdf: {layer: (w, theta)} for the ORDINAL policy; seeded random models if None."""
+                 ffn_every=1, cdf=None, weights="bf16", window="spin", ffn_at=None):
+    """cdf: {layer: (w, theta)} for the ORDINAL policy; seeded random models if None.
+    ffn_at: the (step, layer) pairs whose FFN output is checked, instead of every
+    ffn_every-th one."""
     from paper_2608_11688_amd.runtime import DecodeRunner
     tau = cfg.tau if tau is None else tau
     tau32 = float(np.float32(tau))
@@ -28,11 +68,18 @@ def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau
                           layers=layers, t_attn_us=2.0, record=True, cdf=cdf, weights=weights,
                           window=window, ctx=128)
     ledger = TieLedger()
+    oracle_counts = Counters()
     res = {l: Residency(cfg.E, cfg.C) for l in layers}
     routers = {l: inputs.router_weights(cfg, l) for l in layers}
     hs = {l: inputs.hidden_states(cfg, l, batch, steps) for l in layers}
     cdfs = cdf if cdf is not None else {l: inputs.cdf_params(cfg, l) for l in layers}
     stats = dict(copies=0, misses=0, ffn_checked=0, worst_l1=0.0, covered=0, tokens=0)
+    bits_cache = {}
+
+    def expert_bits(l, e):
+        if (l, e) not in bits_cache:
+            bits_cache[(l, e)] = inputs.expert_weights(cfg, l, e)
+        return bits_cache[(l, e)]
     try:
         for t in range(steps):
             logs = runner.step()
@@ -65,8 +112,19 @@ def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau
                 else:
                     assert set(int(e) for e in log.exec_idx.ravel() if e >= 0) <= R
                 stats["copies"] += log.copies
-                if (t * len(layers) + layers.index(l)) % ffn_every == 0:
-                    bits = lambda e, l=l: inputs.expert_weights(cfg, l, e)
+                # the metrics on the oracle's own sets (the cache replay is teacher-forced)
+                o_lists = [list(r["pf_idx"][b, :r["pf_count"][b]]) for b in range(batch)]
+                o_miss = set(int(e) for e in g["route_idx"].ravel()) - R
+                oracle_counts.add_layer_step(
+                    cfg.k, o_lists, g["route_idx"], R, len(copies),
+                    len(o_miss) if mode == native.MODE_EXACT else 0)
+                oracle_counts.loose_rows += sum(
+                    int(not (np.array_equal(log.pf_idx[b], r["pf_idx"][b]) and
+                             np.array_equal(log.route_idx[b], g["route_idx"][b])))
+                    for b in range(batch))
+                if ((t, l) in ffn_at if ffn_at is not None
+                        else (t * len(layers) + layers.index(l)) % ffn_every == 0):
+                    bits = lambda e, l=l: expert_bits(l, e)
                     y_ref = offn.moe_ffn(h_post, log.exec_idx, log.exec_gate.astype(np.float64),
                                          bits, weights=weights)
                     if cfg.shared:
@@ -75,10 +133,28 @@ def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau
                     _, l1 = ffn_close(log.y, y_ref, f"y t{t} l{l}")
                     stats["worst_l1"] = max(stats["worst_l1"], l1)
                     stats["ffn_checked"] += 1
+        runner.finish()
+        stats["counters"] = oracle_counts.check(runner.stats, f"{cfg.name} B{batch} mode {mode}")
     finally:
         runner.close()
     print(cfg.name, batch, mode, ledger, stats)
     return stats
+
+
+def oracle_counters(cfg, batch, mode, steps, layers, policy, tau):
+    """Counters of the oracle's own decode replay (no teacher forcing) and the number of
+    (token, layer) rows where a near tie could let the GPU decide differently."""
+    from oracle import decode as odec
+    c = Counters()
+    for t, l, out in odec.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers,
+                              run_ffn=False, policy=policy):
+        pf = [list(out["route"]["pf_idx"][b, :out["route"]["pf_count"][b]])
+              for b in range(batch)]
+        c.add_layer_step(cfg.k, pf, out["gate"]["route_idx"], out["resident"],
+                         len(out["copies"]), len(out["misses"]))
+        near = (out["route"]["margin"] < TIE) | (out["gate"]["margin"] < TIE)
+        c.loose_rows += int(near.sum())
+    return c
 
 
 @pytest.mark.parametrize("mode", [native.MODE_EXACT, native.MODE_STALL_FREE])
@@ -103,6 +179,15 @@ def test_decode_granite1b_exact():
     cfg = configs.GRANITE_1B
     st = check_decode(cfg, 1, native.MODE_EXACT, 4, list(range(cfg.L)), ffn_every=3)
     assert st["copies"] > 0
+
+
+def test_decode_mixtral_shape_exact_with_a_miss():
+    # 352 MB experts through the whole path: the copy kernel's wide grid for the prefetch
+    # (a copy at every step of these layers) and for the miss fetch (layer 2 misses
+    # expert 7 at step 4), the second FFN pass over the scratch pool
+    cfg = configs.MIXTRAL
+    st = check_decode(cfg, 1, native.MODE_EXACT, 5, [2, 5], ffn_at={(4, 2), (1, 5)})
+    assert st["copies"] > 0 and st["misses"] >= 1 and st["ffn_checked"] == 2
 
 
 def test_decode_granite3b_batch8_stall_free_ordinal():
@@ -214,51 +299,66 @@ def test_decode_small_experts_with_shared_experts(mode):
     cfg = SMALL_SHARED
     st = check_decode(cfg, 1, mode, cfg.steps, [0, 1])
     assert st["copies"] > 0 and st["ffn_checked"] > 0
-    (y_free, c_free), (y_rec, c_rec) = run_unrecorded_and_recorded(cfg, 1, mode, cfg.steps,
-                                                                    [0, 1])
+    (y_free, c_free, _), (y_rec, c_rec, _) = run_unrecorded_and_recorded(cfg, 1, mode,
+                                                                          cfg.steps, [0, 1])
     assert c_free == c_rec
     assert np.abs(y_free - y_rec).max() <= 1e-5 * np.abs(y_rec).max()
 
 
-def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers):
+def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB):
     """Final outputs and counters of the same decode without and with per-layer records."""
     from paper_2608_11688_amd.runtime import DecodeRunner
     out = []
     for record in (False, True):
-        runner = DecodeRunner(cfg, batch=batch, mode=mode, steps=steps, layers=layers,
-                              t_attn_us=2.0, record=record)
+        runner = DecodeRunner(cfg, batch=batch, mode=mode, tau=float(np.float32(cfg.tau)),
+                              policy=policy, steps=steps, layers=layers, t_attn_us=2.0,
+                              record=record)
         try:
             for _ in range(steps):
                 runner.step()
             runner.finish()
             s = runner.stats
-            counts = (s.tokens, s.layer_steps, s.copies, s.misses, s.coverage_count,
-                      s.delta_hat_sum, s.overlap_sum, s.hit_sum)
-            out.append((runner.y.cpu().numpy().copy(), counts))
+            counts = tuple(getattr(s, f) for f in Counters.FIELDS)
+            out.append((runner.y.cpu().numpy().copy(), counts, s))
         finally:
             runner.close()
     return out
 
 
-@pytest.mark.parametrize("cfg_name,batch,mode,layers", [
-    ("GRANITE_1B", 1, native.MODE_EXACT, None),
-    ("GRANITE_1B", 1, native.MODE_STALL_FREE, None),
-    ("OLMOE", 16, native.MODE_EXACT, [0, 5, 9, 15]),
-    ("DEEPSEEK_16B", 1, native.MODE_EXACT, [0, 12, 25]),
-])
-def test_decode_without_records_matches_recorded(cfg_name, batch, mode, layers):
+@pytest.mark.parametrize("cfg_name,batch,mode,layers,policy", [
+    ("GRANITE_1B", 1, native.MODE_EXACT, None, native.SEL_CUMPROB),
+    ("GRANITE_1B", 1, native.MODE_STALL_FREE, None, native.SEL_CUMPROB),
+    ("OLMOE", 16, native.MODE_EXACT, [0, 5, 9, 15], native.SEL_CUMPROB),
+    ("DEEPSEEK_16B", 1, native.MODE_EXACT, [0, 12, 25], native.SEL_CUMPROB),
+    # no router: in stall-free mode nothing orders the gate before the counters are
+    # folded except the poll of the stream it ran on
+    ("GRANITE_1B", 1, native.MODE_STALL_FREE, None, native.SEL_NONE),
+    ("OLMOE", 16, native.MODE_EXACT, [2, 11], native.SEL_NONE),
+], ids=["g1-exact", "g1-stall-free", "olmoe-b16-exact", "deepseek-exact", "g1-none-stall-free",
+        "olmoe-b16-none-exact"])
+def test_decode_without_records_matches_recorded(cfg_name, batch, mode, layers, policy):
     # The parity tests above record every layer, which synchronizes the host with the
     # device after each one; the timed path does not, and there the copies, the window,
     # the gate and the FFN overlap across the two streams.  Same inputs, same state: the
-    # counters must agree exactly and the last step's outputs to rounding.
+    # counters must agree exactly and the last step's outputs to rounding.  The counters
+    # of the timed path must also equal the oracle's own replay: these inputs have no
+    # near tie, so the oracle's decisions are the GPU's.
     cfg = getattr(configs, cfg_name)
     layers = list(range(cfg.L)) if layers is None else layers
-    (y_free, c_free), (y_rec, c_rec) = run_unrecorded_and_recorded(cfg, batch, mode, 6, layers)
+    steps = 6
+    (y_free, c_free, s_free), (y_rec, c_rec, _) = run_unrecorded_and_recorded(
+        cfg, batch, mode, steps, layers, policy)
     assert c_free == c_rec
-    assert c_free[2] > 0                        # copies happened
+    if policy == native.SEL_NONE:
+        assert c_free[2] == 0 and s_free.overlap_sum == 0 and s_free.delta_hat_sum == 0
+    else:
+        assert c_free[2] > 0                    # copies happened
     scale = np.abs(y_rec).max()
     assert scale > 0
     assert np.abs(y_free - y_rec).max() <= 1e-5 * scale
+    ref = oracle_counters(cfg, batch, mode, steps, layers, policy, float(np.float32(cfg.tau)))
+    assert ref.loose_rows == 0
+    print(cfg_name, ref.check(s_free, "unrecorded vs oracle"))
 
 
 @pytest.mark.parametrize("batch,mode", [(1, native.MODE_EXACT), (8, native.MODE_STALL_FREE)])

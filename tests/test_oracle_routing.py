@@ -230,5 +230,7 @@ def test_no_prefetch_decode_keeps_the_initial_cache():
         assert sorted(out["resident"]) == list(range(cfg.C))
         routed = set(int(e) for e in out["gate"]["route_idx"][0])
         assert sorted(out["misses"]) == sorted(routed - set(range(cfg.C)))
+        # nothing prefetched: no overlap, no extra experts (delta_hat >= 0, Eq. 9)
+        assert out["metrics"]["overlap"] == [0.0] and out["metrics"]["delta_hat"] == [0]
         seen.append(len(out["misses"]))
     assert sum(seen) > 0
