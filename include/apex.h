@@ -244,6 +244,30 @@ apex_status apex_moe_ffn_mxfp4(const float *x, int B, int d, int I, int E, int k
                                size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * apex_moe_ffn without a workspace argument, for callers that cannot allocate device
+ * memory: code being captured into a graph, tight serving loops, harnesses that forbid
+ * allocation.  Same computation, arguments and error behaviour as apex_moe_ffn,
+ * apex_moe_ffn_fp8 or apex_moe_ffn_mxfp4, chosen by `weights` (apex_weights), with the
+ * workspace taken from a fixed device array of APEX_NOALLOC_WORKSPACE_BYTES bytes that
+ * the library holds on each GPU it runs on, from the first call on that GPU until the
+ * process ends.  The call allocates and frees nothing.
+ *   weights  APEX_WEIGHTS_BF16, APEX_WEIGHTS_FP8_E4M3 or APEX_WEIGHTS_MXFP4: the layout
+ *            of `slots` (apex_pack_expert, _fp8 or _mxfp4)
+ * Errors, before anything is enqueued: APEX_E_CAPACITY when
+ * apex_moe_ffn_workspace_bytes(B, d, I, k) exceeds APEX_NOALLOC_WORKSPACE_BYTES (every
+ * workload shape here needs at most 34 MiB); the errors of apex_moe_ffn otherwise.
+ * Every call on one GPU uses that GPU's one array: calls that may overlap on one GPU
+ * (on different streams, or from different host threads) race, and the caller must
+ * order them.  The array's contents between calls are not meaningful; nothing in it
+ * has to start at zero.
+ */
+#define APEX_NOALLOC_WORKSPACE_BYTES (64u << 20)
+apex_status apex_moe_ffn_noalloc(const float *x, int B, int d, int I, int E, int k,
+                                 const int32_t *exec_idx, const float *exec_gate,
+                                 const int32_t *slot_of_expert, const void *slots, int n_slots,
+                                 int weights, float *y, int accumulate, hipStream_t stream);
+
+/*
  * The launch plan apex_moe_ffn (weights = APEX_WEIGHTS_BF16), apex_moe_ffn_fp8 and
  * apex_moe_ffn_mxfp4 take for B >= 2 tokens with E experts of which n_slots have a slot
  * (host only; no GPU work): plan[0] = 16-token tiles per pass (1, 2 or 4), plan[1] = K

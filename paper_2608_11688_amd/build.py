@@ -24,7 +24,7 @@ PLAN_LIB = os.path.join(PKG, "libapex_plan.so")
 
 HIP_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "pack_mxfp4.cpp", "decode.cpp",
                "route_gate.hip", "moe_ffn.cpp", "ffn_b1.hip", "ffn_b1_e4m3.hip",
-               "ffn_b1_mxfp4.hip", "ffn_gemm.hip", "attention.hip", "prefetch.hip", "util.hip"]
+               "ffn_b1_mxfp4.hip", "ffn_gemm.hip", "ffn_noalloc.hip", "attention.hip", "prefetch.hip", "util.hip"]
 HOST_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "pack_mxfp4.cpp"]
 
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -46,6 +46,14 @@ apex_status ffn_grouped(const float *x, int B, int d, int I, int E, int k,
                         WeightFormat fmt, float *y, int accumulate, void *workspace,
                         hipStream_t stream);
 
+// apex_moe_ffn in format fmt with its argument checks, `fn` naming the entry point in
+// error messages (moe_ffn.cpp).
+apex_status moe_ffn_checked(const char *fn, WeightFormat fmt, const float *x, int B, int d,
+                            int I, int E, int k, const int32_t *exec_idx, const float *exec_gate,
+                            const int32_t *slot_of_expert, const void *slots, int n_slots,
+                            float *y, int accumulate, void *workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace apex

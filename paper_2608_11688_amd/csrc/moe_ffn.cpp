@@ -26,10 +26,8 @@ extern "C" apex_status apex_moe_ffn_plan(int B, int d, int I, int E, int k, int 
     return APEX_OK;
 }
 
-namespace {
-
-apex_status moe_ffn(const char *fn, apex::WeightFormat fmt, const float *x, int B, int d, int I,
-                    int E, int k,
+apex_status apex::moe_ffn_checked(const char *fn, apex::WeightFormat fmt, const float *x, int B,
+                                  int d, int I, int E, int k,
                     const int32_t *exec_idx, const float *exec_gate,
                     const int32_t *slot_of_expert, const void *slots, int n_slots, float *y,
                     int accumulate, void *workspace, size_t workspace_bytes,
@@ -75,14 +73,12 @@ apex_status moe_ffn(const char *fn, apex::WeightFormat fmt, const float *x, int 
                              n_slots, fmt, y, accumulate, workspace, stream);
 }
 
-}  // namespace
-
 extern "C" apex_status apex_moe_ffn(const float *x, int B, int d, int I, int E, int k,
                                     const int32_t *exec_idx, const float *exec_gate,
                                     const int32_t *slot_of_expert, const uint16_t *slots,
                                     int n_slots, float *y, int accumulate, void *workspace,
                                     size_t workspace_bytes, hipStream_t stream) {
-    return moe_ffn("apex_moe_ffn", apex::WeightFormat::kBf16, x, B, d, I, E, k, exec_idx,
+    return apex::moe_ffn_checked("apex_moe_ffn", apex::WeightFormat::kBf16, x, B, d, I, E, k, exec_idx,
                    exec_gate, slot_of_expert, slots, n_slots, y, accumulate, workspace,
                    workspace_bytes, stream);
 }
@@ -92,7 +88,7 @@ extern "C" apex_status apex_moe_ffn_fp8(const float *x, int B, int d, int I, int
                                         const int32_t *slot_of_expert, const void *slots,
                                         int n_slots, float *y, int accumulate, void *workspace,
                                         size_t workspace_bytes, hipStream_t stream) {
-    return moe_ffn("apex_moe_ffn_fp8", apex::WeightFormat::kE4M3, x, B, d, I, E, k, exec_idx,
+    return apex::moe_ffn_checked("apex_moe_ffn_fp8", apex::WeightFormat::kE4M3, x, B, d, I, E, k, exec_idx,
                    exec_gate, slot_of_expert, slots, n_slots, y, accumulate, workspace,
                    workspace_bytes, stream);
 }
@@ -103,7 +99,7 @@ extern "C" apex_status apex_moe_ffn_mxfp4(const float *x, int B, int d, int I, i
                                           int n_slots, float *y, int accumulate,
                                           void *workspace, size_t workspace_bytes,
                                           hipStream_t stream) {
-    return moe_ffn("apex_moe_ffn_mxfp4", apex::WeightFormat::kMxfp4, x, B, d, I, E, k,
+    return apex::moe_ffn_checked("apex_moe_ffn_mxfp4", apex::WeightFormat::kMxfp4, x, B, d, I, E, k,
                    exec_idx, exec_gate, slot_of_expert, slots, n_slots, y, accumulate,
                    workspace, workspace_bytes, stream);
 }

@@ -27,6 +27,7 @@ WEIGHTS_BF16, WEIGHTS_FP8_E4M3, WEIGHTS_MXFP4 = 0, 1, 2
 ABI_VERSION = 4
 MAX_EXPERTS = 64
 MAX_PAIRS = 1024
+NOALLOC_WORKSPACE_BYTES = 64 << 20
 
 
 class ApexError(RuntimeError):
@@ -88,6 +89,7 @@ SIGNATURES = {
     "apex_moe_ffn_fp8": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_mxfp4": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_plan": (I32, [I32, I32, I32, I32, I32, I32, I32, P]),
+    "apex_moe_ffn_noalloc": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, I32, P, I32, P]),
     "apex_attention_workspace_bytes": (SZ, [I32, I32, I32, I32, I32]),
     "apex_attention_decode": (I32, [P, P, P, I32, I32, I32, I32, I32, P, P, I32, I32, P, P, SZ,
                                     P]),
@@ -253,6 +255,14 @@ def apex_moe_ffn_mxfp4(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, sl
     _call("apex_moe_ffn_mxfp4", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
           ptr(slot_of_expert), ptr(slots), n_slots, ptr(y), int(accumulate), ptr(workspace),
           workspace_bytes, stream)
+
+
+def apex_moe_ffn_noalloc(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots,
+                         weights, y, accumulate, stream=None):
+    """weights: an APEX_WEIGHTS_* code or a format name ("bf16", "fp8", "mxfp4")."""
+    code = WEIGHT_FORMATS[weights][0] if isinstance(weights, str) else int(weights)
+    _call("apex_moe_ffn_noalloc", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
+          ptr(slot_of_expert), ptr(slots), n_slots, code, ptr(y), int(accumulate), stream)
 
 
 # weight format name -> (decode-driver code, bytes of one packed expert, packer, FFN entry)

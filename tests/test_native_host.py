@@ -141,6 +141,15 @@ def test_entry_points_validate_before_enqueue(hip_lib):
             A, 16)
     _expect(native.APEX_E_INVAL, native.apex_moe_ffn, A, 2, 64, 60, 8, 2, A, A, A, A, 1, A, 0, A,
             1 << 20)
+    # the entry point without a workspace: a shape whose workspace exceeds its fixed array,
+    # or an unknown weight format, is refused before any device call
+    need = native.apex_moe_ffn_workspace_bytes(64, 4096, 14336, 16)
+    assert need > native.NOALLOC_WORKSPACE_BYTES
+    msg = _expect(native.APEX_E_CAPACITY, native.apex_moe_ffn_noalloc, A, 64, 4096, 14336, 16,
+                  16, A, A, A, A, 1, "bf16", A, 0)
+    assert "workspace" in msg
+    _expect(native.APEX_E_INVAL, native.apex_moe_ffn_noalloc, A, 2, 64, 64, 8, 2, A, A, A, A, 1,
+            7, A, 0)
     # B = 0 is a no-op that needs no device
     native.apex_prefetch_route(None, None, None, 0, 64, 8, 2, 4, 0, 0.9, 0, None, None, None,
                                None, None)
