@@ -452,7 +452,9 @@ typedef struct {
     const float *cdf_w, *cdf_theta;        /* device (ORDINAL_CDF only) or NULL */
     const uint16_t *host_experts;          /* pinned, [E] experts in the layout of cfg.weights */
     uint16_t *slots;                       /* device, [C] experts */
-    int32_t *slot_of_expert_dev;           /* device int32 [E] (kept equal to the tables) */
+    int32_t *slot_of_expert_dev;           /* device int32 [E]: equal to the host tables at
+                                              creation; the driver rewrites it (and
+                                              avail_dev) whenever a layer-step copies */
     uint8_t *avail_dev;                    /* device uint8 [E] resident mask */
     int32_t *expert_of_slot;               /* host int32 [C] in/out */
     int64_t *last_used;                    /* host int64 [E] in/out */

@@ -361,7 +361,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
                                    dec->pf_idx_h, dec->pf_count_h, c.B, c.k_max, step,
                                    Ly.expert_of_slot, Ly.last_used, Ly.slot_of_expert_dev,
                                    Ly.avail_dev, cs, ss, cs, nullptr, nullptr, copied.data(),
-                                   &n_copy);
+                                   &n_copy, false);
         if (st != APEX_OK) return st;
         const bool split = n_copy > 0;
         const hipStream_t ws = split ? ss : cs;

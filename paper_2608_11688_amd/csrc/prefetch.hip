@@ -132,7 +132,7 @@ apex_status apex::expert_prefetch(
     const int32_t *pf_count, int B, int k_max, int64_t step, int32_t *expert_of_slot,
     int64_t *last_used, int32_t *slot_of_expert_dev, uint8_t *avail_dev, hipStream_t side,
     hipStream_t compute, hipStream_t compute_if_none, hipEvent_t readers_done, hipEvent_t ready,
-    int32_t *copied_experts, int *n_copied) {
+    int32_t *copied_experts, int *n_copied, bool publish_unchanged) {
     int32_t ce[APEX_MAX_EXPERTS], cs[APEX_MAX_EXPERTS];
     int n = 0;
     apex_status st = apex_plan_residency(E, C, pf_idx, pf_count, B, k_max, step, expert_of_slot,
@@ -152,12 +152,16 @@ apex_status apex::expert_prefetch(
     }
     if (ready) APEX_HIP(hipEventRecord(ready, side));
 
-    Table t;
-    std::fill(t.slot, t.slot + APEX_MAX_EXPERTS, -1);
-    for (int s = 0; s < C; ++s)
-        if (expert_of_slot[s] >= 0) t.slot[expert_of_slot[s]] = s;
-    st = publish(t, E, slot_of_expert_dev, avail_dev, n > 0 ? compute : compute_if_none);
-    if (st != APEX_OK) return st;
+    // a plan without copies leaves the table as it was: its device copy needs no rewrite
+    // unless the caller cannot vouch that the device copy is current
+    if (n > 0 || publish_unchanged) {
+        Table t;
+        std::fill(t.slot, t.slot + APEX_MAX_EXPERTS, -1);
+        for (int s = 0; s < C; ++s)
+            if (expert_of_slot[s] >= 0) t.slot[expert_of_slot[s]] = s;
+        st = publish(t, E, slot_of_expert_dev, avail_dev, n > 0 ? compute : compute_if_none);
+        if (st != APEX_OK) return st;
+    }
     if (copied_experts)
         for (int i = 0; i < n; ++i) copied_experts[i] = ce[i];
     if (n_copied) *n_copied = n;
@@ -183,7 +187,7 @@ extern "C" apex_status apex_expert_prefetch(
     return apex::expert_prefetch(src, slots, E, C, expert_bytes, pf_idx, pf_count, B, k_max,
                                  step, expert_of_slot, last_used, slot_of_expert_dev, avail_dev,
                                  side, compute, compute, readers_done, ready, copied_experts,
-                                 n_copied);
+                                 n_copied, true);
 }
 
 apex_status apex::fetch_misses(const uint16_t *host_experts, const uint4 *src, uint16_t *scratch,

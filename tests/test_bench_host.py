@@ -28,8 +28,9 @@ def test_more_than_one_gpu_is_refused():
 
 def test_traffic_record_needs_the_same_source_and_flags(bench, tmp_path, monkeypatch):
     from paper_2608_11688_amd import build, configs
-    cfg = configs.CONFIGS["granite-1b-a400m"]
-    rec = json.load(open(os.path.join(ROOT, "profiles", "moe_ffn_traffic.json")))["records"][0]
+    cfg = configs.CONFIGS["mixtral-8x7b"]          # the bench's default workload
+    recs = json.load(open(os.path.join(ROOT, "profiles", "moe_ffn_traffic.json")))["records"]
+    rec = [r for r in recs if r["workload"] == cfg.name and r["batch"] == 1][0]
     assert bench.measured_traffic(cfg, 1) == rec["traffic_bytes_per_call"]
     assert bench.measured_traffic(cfg, 8) is None                  # no record for batch 8
     assert bench.measured_traffic(cfg, 1, weights="fp8") is None
