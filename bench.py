@@ -43,7 +43,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-FFN_KERNELS = {True: "apex_moe_ffn (up_b1 + down_b1)",
+FFN_KERNELS = {True: "apex_moe_ffn (up_sk or up_b1, then down_b1)",
                False: "apex_moe_ffn (up_gemm + down_gemm + combine_pairs)"}
 
 

@@ -1,8 +1,8 @@
 // Expert FFN for one token (apex_moe_ffn, batch 1): gated SwiGLU experts over HBM
 // cache slots, two launches that each stream their weights once.
 //
-// up_b1 reads the W1/W3 rows of every executed expert with all loads of a row issued
-// before any arithmetic and writes h[j, i] = silu(W1[i] . x) * (W3[i] . x) * gate_j;
+// up_b1 / up_sk read the W1/W3 rows of every executed expert with all loads of a row
+// issued before any arithmetic and write h[j, i] = silu(W1[i] . x) * (W3[i] . x) * gate_j;
 // down_b1 owns output rows of y and sums W2_j[row] . h[j] over the k experts as one
 // flattened dot product, so the k experts share a single launch and y is written once
 // without atomics.  Loads are 16 bytes wide over consecutive chunks of a row.
@@ -91,6 +91,73 @@ __global__ __launch_bounds__(WAVES *kWave) void up_b1(
         if (lane == r) hv = silu(su) * sv * g;
     }
     if (lane < RW && i0 + lane < I) h[size_t(j) * I + i0 + lane] = hv;
+}
+
+// up_sk: the same h with each row's length split over a workgroup.  Grid
+// (I / R, k); the WAVES * 64 lanes cover the d / 8 chunks of a row one chunk each, so a
+// lane loads its 32 bytes of x once and then only weights: the 2R chunks of the R W1/W3
+// row pairs, all issued before the multiplies.  Each wavefront reduces its partial sums,
+// and the WAVES partials of a row are added in LDS in wavefront order (deterministic).
+template <int R, int WAVES>
+__global__ __launch_bounds__(WAVES *kWave) void up_sk(
+    const float *__restrict__ x, int d, int I, int E, int k,
+    const int32_t *__restrict__ exec_idx, const float *__restrict__ exec_gate,
+    const int32_t *__restrict__ slot_of_expert, const uint16_t *__restrict__ slots, int n_slots,
+    size_t slot_elems, float *__restrict__ h) {
+    __shared__ float pu[WAVES][R], pv[WAVES][R];
+    const int j = blockIdx.y;
+    const int e = exec_idx[j];
+    const float g = exec_gate[j];
+    // uniform over the workgroup: the whole workgroup leaves before the barrier
+    if (e < 0 || e >= E) return;
+    const int s = slot_of_expert[e];
+    if (s < 0 || s >= n_slots) return;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int nch = d / 8;
+    const int c = threadIdx.x;
+    const bool on = c < nch;
+    const int i0 = blockIdx.x * R;
+    const uint4 *W = reinterpret_cast<const uint4 *>(slots + size_t(s) * slot_elems);
+    const float4 *x4 = reinterpret_cast<const float4 *>(x);
+    uint4 w1[R], w3[R];
+    float4 xa, xb;
+    if (on) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int i = (i0 + r < I) ? i0 + r : I - 1;
+            const uint4 *row = W + size_t(i) * 2 * nch;
+            w1[r] = row[c];
+            w3[r] = row[nch + c];
+        }
+        xa = x4[2 * c];
+        xb = x4[2 * c + 1];
+    }
+    float u[R], v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        u[r] = on ? dot8(w1[r], xa, xb, 0.f) : 0.f;
+        v[r] = on ? dot8(w3[r], xa, xb, 0.f) : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float su = wave_sum(u[r]);
+        const float sv = wave_sum(v[r]);
+        if (lane == 0) {
+            pu[wave][r] = su;
+            pv[wave][r] = sv;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < R && i0 + int(threadIdx.x) < I) {
+        const int r = threadIdx.x;
+        float su = 0.f, sv = 0.f;
+#pragma unroll
+        for (int q = 0; q < WAVES; ++q) {
+            su += pu[q][r];
+            sv += pv[q][r];
+        }
+        h[size_t(j) * I + i0 + r] = silu(su) * sv * g;
+    }
 }
 
 // down_b1: grid d / (WAVES * RD).  A wavefront owns RD output rows; the gated h of
@@ -184,34 +251,41 @@ apex_status ffn_b1(const float *x, int d, int I, int E, int k, const int32_t *ex
     const size_t slot_elems = size_t(3) * d * I;
     // h holds gated rows per position; tile shapes measured on MI355X (streaming rate
     // of the two launches against the plain read rate at the same sizes)
-    const int npl = (d + 511) / 512;
+    using UpKernel = decltype(&up_b1<1, 1, 4>);
+    UpKernel up;
+    dim3 gu, bu;
+    if (d > 512 && d <= 4096) {
+        // a row pair per workgroup of 2, 4 or 8 wavefronts (one 16-byte chunk of the row
+        // per lane), or two row pairs where one would mean more than 16384 workgroups.
+        // Up projection against one row pair per wavefront (up_b1), us: Granite-1B 5.45 ->
+        // 5.36, Granite-3B 6.79 -> 6.58, OLMoE 13.5 -> 12.5, DeepSeek-16B 14.3 -> 13.3,
+        // Phi-7B 8.0 -> 7.1, Mixtral 76.7 -> 74.0 (two row pairs); at d = 256 up_b1 is
+        // faster (2.6 against 2.8)
+        const bool two = size_t(I) * k > 16384;
+        const int waves = d <= 1024 ? 2 : d <= 2048 ? 4 : 8;
+        if (waves == 2) up = two ? up_sk<2, 2> : up_sk<1, 2>;
+        else if (waves == 4) up = two ? up_sk<2, 4> : up_sk<1, 4>;
+        else up = two ? up_sk<2, 8> : up_sk<1, 8>;
+        gu = dim3(two ? I / 2 + (I % 2 != 0) : I, k);
+        bu = dim3(waves * kWave);
+    } else {
+        // one row pair per wavefront: four wavefronts per workgroup for rows of up to 512
+        // values (one chunk per lane), two for rows longer than 4096 (four chunks per lane)
+        const bool shortrow = d <= 512;
+        up = shortrow ? up_b1<1, 1, 4> : up_b1<4, 1, 2>;
+        gu = shortrow ? dim3(I / 4 + (I % 4 != 0), k) : dim3(I / 2 + (I % 2 != 0), k);
+        bu = dim3(shortrow ? 256 : 128);
+    }
+    hipLaunchKernelGGL(up, gu, bu, 0, stream, x, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                       slots, n_slots, slot_elems, h);
+    APEX_HIP(hipGetLastError());
     if (d <= 2048) {
-        const dim3 gu(I / 4 + (I % 4 != 0), k);
-        if (npl <= 1)
-            hipLaunchKernelGGL((up_b1<1, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-        else if (npl == 2)
-            hipLaunchKernelGGL((up_b1<2, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-        else if (npl == 3)
-            hipLaunchKernelGGL((up_b1<3, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-        else
-            hipLaunchKernelGGL((up_b1<4, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-        APEX_HIP(hipGetLastError());
         hipLaunchKernelGGL((down_b1<1, 1, 8>), dim3(d), dim3(64), 0, stream, d, I, E, k,
                            exec_idx, slot_of_expert, slots, n_slots, slot_elems, h, y,
                            accumulate);
     } else {
-        // rows longer than 2048: one row per wavefront and two wavefronts per workgroup in
-        // the up kernel, two output rows per wavefront in the down kernel (against two rows
-        // per wavefront and four wavefronts, and four output rows per wavefront: Mixtral
+        // rows longer than 2048: two output rows per wavefront (against four: Mixtral
         // 122.1-123.4 -> 120.6 us per call, Phi-7B 15.2 -> 13.2 us)
-        const dim3 gu(I / 2 + (I % 2 != 0), k);
-        hipLaunchKernelGGL((up_b1<4, 1, 2>), gu, dim3(128), 0, stream, x, d, I, E, k,
-                           exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_elems, h);
-        APEX_HIP(hipGetLastError());
         hipLaunchKernelGGL((down_b1<2, 4, 8>), dim3(d / 8 + (d % 8 != 0)), dim3(256), 0,
                            stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
                            slot_elems, h, y, accumulate);

@@ -92,6 +92,79 @@ __global__ __launch_bounds__(WAVES *kWave) void up_b1_mxfp4(
     if (lane < RW && i0 + lane < I) h[size_t(j) * I + i0 + lane] = hv;
 }
 
+// up_sk_mxfp4: the same h with each row's length split over a workgroup, grid
+// (I / R, k).  The WAVES * 64 lanes cover the d / 16 units of a row one unit each: a
+// lane loads its 64 bytes of x once, then for each of the R W1/W3 row pairs two 8-byte
+// units and their two scale bytes, all before the multiplies.  The wavefronts' partial
+// sums meet in LDS and are added in wavefront order.
+template <int R, int WAVES>
+__global__ __launch_bounds__(WAVES *kWave) void up_sk_mxfp4(
+    const float *__restrict__ x, int d, int I, int E, int k,
+    const int32_t *__restrict__ exec_idx, const float *__restrict__ exec_gate,
+    const int32_t *__restrict__ slot_of_expert, const uint8_t *__restrict__ slots, int n_slots,
+    size_t slot_bytes, float *__restrict__ h) {
+    __shared__ float pu[WAVES][R], pv[WAVES][R];
+    const int j = blockIdx.y;
+    const int e = exec_idx[j];
+    const float g = exec_gate[j];
+    // uniform over the workgroup: the whole workgroup leaves before the barrier
+    if (e < 0 || e >= E) return;
+    const int s = slot_of_expert[e];
+    if (s < 0 || s >= n_slots) return;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int nch = d / 16;                       // units per row of W1 (and of W3)
+    const int nsb = d / 32;                       // scale bytes per row
+    const int c = threadIdx.x;
+    const bool on = c < nch;
+    const int i0 = blockIdx.x * R;
+    const uint8_t *slot = slots + size_t(s) * slot_bytes;
+    const uint2 *W = reinterpret_cast<const uint2 *>(slot);     // rows of 2 * nch units
+    const uint8_t *sc1 = slot + size_t(3) * I * d / 2;          // W1 scales [I][d/32]
+    const uint8_t *sc3 = sc1 + size_t(I) * nsb;                 // W3 scales
+    const float4 *x4 = reinterpret_cast<const float4 *>(x);
+    uint2 w1[R], w3[R];
+    uint32_t b1[R], b3[R];
+    float4 xs[4];
+    if (on) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int i = (i0 + r < I) ? i0 + r : I - 1;
+            const uint2 *row = W + size_t(i) * 2 * nch;
+            w1[r] = row[c];
+            w3[r] = row[nch + c];
+            b1[r] = sc1[size_t(i) * nsb + c / 2];
+            b3[r] = sc3[size_t(i) * nsb + c / 2];
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) xs[q] = x4[4 * c + q];
+    }
+    float u[R], v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        u[r] = on ? dot16_mxfp4(w1[r], mx_scale(b1[r]), xs, 0.f) : 0.f;
+        v[r] = on ? dot16_mxfp4(w3[r], mx_scale(b3[r]), xs, 0.f) : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float su = wave_sum(u[r]);
+        const float sv = wave_sum(v[r]);
+        if (lane == 0) {
+            pu[wave][r] = su;
+            pv[wave][r] = sv;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < R && i0 + int(threadIdx.x) < I) {
+        float su = 0.f, sv = 0.f;
+#pragma unroll
+        for (int q = 0; q < WAVES; ++q) {
+            su += pu[q][threadIdx.x];
+            sv += pv[q][threadIdx.x];
+        }
+        h[size_t(j) * I + i0 + threadIdx.x] = silu(su) * sv * g;
+    }
+}
+
 // down_b1_mxfp4: grid d / (WAVES * RD).  A wavefront owns RD output rows; lanes step
 // through (valid position, unit) pairs UNR at a time, as down_b1 does.
 template <int RD, int WAVES, int UNR>
@@ -180,26 +253,41 @@ apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32
                          const uint8_t *slots, int n_slots, float *h, float *y, int accumulate,
                          hipStream_t stream) {
     const size_t slot_bytes = apex_expert_bytes_mxfp4(d, I);
-    const int npl = (d + 1023) / 1024;   // 16-code units per lane for a whole row
-    if (d <= 2048) {
-        const dim3 gu(I / 4 + (I % 4 != 0), k);
-        if (npl <= 1)
-            hipLaunchKernelGGL((up_b1_mxfp4<1, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_bytes, h);
-        else
-            hipLaunchKernelGGL((up_b1_mxfp4<2, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                               exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_bytes, h);
-        APEX_HIP(hipGetLastError());
-        hipLaunchKernelGGL((down_b1_mxfp4<1, 1, 8>), dim3(d), dim3(64), 0, stream, d, I, E, k,
-                           exec_idx, slot_of_expert, slots, n_slots, slot_bytes, h, y,
-                           accumulate);
+    // tile shapes measured on MI355X (timing probe, the calls of one workload cycling over
+    // a 1.5 GB pool)
+    using UpKernel = decltype(&up_b1_mxfp4<1, 1, 4>);
+    UpKernel up;
+    dim3 gu, bu;
+    if (d > 1024 && d <= 4096) {
+        // a workgroup of 2 or 4 wavefronts per two (more than 16384 row pairs: four) row
+        // pairs, one 16-code unit of the row per lane.  Up projection against one row pair
+        // per wavefront (up_b1_mxfp4), us: Granite-3B 5.90 -> 5.10, OLMoE 9.49 -> 7.16,
+        // Phi-7B 6.14 -> 5.04, Mixtral 44.1 -> 28.9; whole 32-code blocks per lane were
+        // slower (Mixtral 29.5-59.1); at d = 1024 the two are level (4.33, 4.28)
+        const bool four = size_t(I) * k > 16384;
+        if (d <= 2048) up = four ? up_sk_mxfp4<4, 2> : up_sk_mxfp4<2, 2>;
+        else up = four ? up_sk_mxfp4<4, 4> : up_sk_mxfp4<2, 4>;
+        gu = four ? dim3(I / 4 + (I % 4 != 0), k) : dim3(I / 2 + (I % 2 != 0), k);
+        bu = dim3((d <= 2048 ? 2 : 4) * kWave);
     } else {
-        // one row per wavefront: 2 rows took 178 VGPRs (2 wavefronts per SIMD) and left the
-        // conversions and the loads of a wavefront little to overlap with
-        const dim3 gu(I / 4 + (I % 4 != 0), k);
-        hipLaunchKernelGGL((up_b1_mxfp4<4, 1, 4>), gu, dim3(256), 0, stream, x, d, I, E, k,
-                           exec_idx, exec_gate, slot_of_expert, slots, n_slots, slot_bytes, h);
-        APEX_HIP(hipGetLastError());
+        // one row pair per wavefront; the whole row in one pass up to 1024 values, 4096
+        // values per pass beyond (2 rows per wavefront took 178 VGPRs, 2 wavefronts per
+        // SIMD, and left the conversions and the loads little to overlap with)
+        const bool shortrow = d <= 1024;
+        up = shortrow ? up_b1_mxfp4<1, 1, 4> : up_b1_mxfp4<4, 1, 4>;
+        gu = dim3(I / 4 + (I % 4 != 0), k);
+        bu = dim3(256);
+    }
+    hipLaunchKernelGGL(up, gu, bu, 0, stream, x, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+                       slots, n_slots, slot_bytes, h);
+    APEX_HIP(hipGetLastError());
+    if (d <= 2048) {
+        // two output rows per wavefront (against one: OLMoE 7.60 -> 6.34 us, Granite-3B
+        // 4.84 -> 4.36, Granite-1B 4.38 -> 4.09)
+        hipLaunchKernelGGL((down_b1_mxfp4<2, 1, 8>), dim3(d / 2 + (d % 2 != 0)), dim3(64), 0,
+                           stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
+                           slot_bytes, h, y, accumulate);
+    } else {
         hipLaunchKernelGGL((down_b1_mxfp4<4, 4, 4>), dim3(d / 16 + (d % 16 != 0)), dim3(256), 0,
                            stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
                            slot_bytes, h, y, accumulate);

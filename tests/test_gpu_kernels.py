@@ -268,6 +268,13 @@ FFN_SHAPES = [
     (shape("ffn_tiny_tiles", 402, 8, 4, 2, I=8), 2),     # one 16-byte chunk per row
     (shape("ffn_b8", 403, 1024, 32, 8, I=512), 8),
     (shape("ffn_wide_k", 404, 264, 64, 16, I=72), 64),   # B*k = 1024 pairs (the maximum)
+    # one token with rows of 513..4096 values: the up projection splits each row over a
+    # workgroup's lanes (one 16-byte chunk per lane, idle lanes past the row's end)
+    (shape("ffn_split_d520", 420, 520, 5, 3, I=72), 1),      # 65 chunks on 128 lanes
+    (shape("ffn_split_d1032", 421, 1032, 6, 2, I=96), 1),    # 129 chunks on 256 lanes
+    (shape("ffn_split_d1800", 408, 1800, 6, 3, I=136), 1),   # 225 chunks on 256 lanes
+    (shape("ffn_split_d2056", 409, 2056, 4, 2, I=40), 1),    # 257 chunks on 512 lanes
+    (shape("ffn_split_two_rows", 418, 2304, 3, 2, I=8200), 1),  # I*k > 16384: 2 rows
 ]
 
 
@@ -279,8 +286,9 @@ def test_ffn_parity_shapes(torch, cfg, B):
 
 
 @pytest.mark.parametrize("name,B", [("granite-1b-a400m", 1), ("granite-3b-a800m", 1),
-                                    ("granite-3b-a800m", 8), ("olmoe-1b-7b", 16),
-                                    ("olmoe-1b-7b", 64), ("tiny", 1)])
+                                    ("granite-3b-a800m", 8), ("olmoe-1b-7b", 1),
+                                    ("olmoe-1b-7b", 16), ("olmoe-1b-7b", 64),
+                                    ("deepseek-16b", 1), ("phi-7b", 1), ("tiny", 1)])
 def test_ffn_parity_workload_shapes(torch, name, B):
     cfg = configs.CONFIGS[name]
     case = FfnCase(torch, cfg, B, seed=cfg.cfg_id * 10 + B)
@@ -384,6 +392,12 @@ FP8_SHAPES = [
     (shape("fp8_split_a", 431, 784, 4, 2, I=1008), 4),     # few experts, ragged K tails
     (shape("fp8_split_b", 432, 1008, 4, 2, I=784), 5),
     (shape("fp8_small", 433, 16, 3, 2, I=48), 3),          # one 16-byte chunk per row
+    # one token, rows of 1025..4096 values: the up projection splits each row over a
+    # workgroup (one 16-code chunk per lane, 1, 2 or 4 row pairs per workgroup)
+    (configs.PHI_7B, 1), (configs.DEEPSEEK_16B, 1),
+    (shape("fp8_b1_split_a", 436, 1040, 6, 3, I=112), 1),  # 65 chunks on 128 lanes
+    (shape("fp8_b1_split_b", 437, 2064, 4, 2, I=1104), 1),  # 129 chunks on 256 lanes
+    (shape("fp8_b1_split_c", 438, 2080, 3, 2, I=8224), 1),  # I*k > 16384: 4 row pairs
 ]
 
 
@@ -420,6 +434,9 @@ MXFP4_SHAPES = [
     (shape("fp4_split_a", 441, 800, 4, 2, I=992), 4),       # few experts; ragged last K block
     (shape("fp4_split_b", 442, 992, 4, 2, I=800), 5),
     (shape("fp4_small", 443, 32, 3, 2, I=64), 3),           # one block per row
+    # one token, rows of 1025..4096 values: split rows, one 16-code unit per lane
+    (shape("fp4_b1_split_a", 445, 1056, 6, 3, I=96), 1),    # 66 units on 128 lanes
+    (shape("fp4_b1_split_b", 446, 2080, 3, 2, I=8224), 1),  # I*k > 16384: 4 row pairs
 ]
 
 
@@ -472,6 +489,29 @@ def test_ffn_two_passes_equal_one(torch):
     none = np.full(cfg.E, -1, np.int32)
     assert np.array_equal(case.run(none, y0=y1, accumulate=1), y1)
     assert (case.run(none) == 0).all()
+
+
+@pytest.mark.parametrize("d,I", [(520, 72), (1800, 136), (2056, 40)])
+def test_ffn_batch1_split_rows_two_passes_and_repeat(torch, d, I):
+    """One token over the split-row up projection: two passes (the second accumulating)
+    equal one, absent experts leave y alone, and a repeated call is bitwise equal."""
+    cfg = shape(f"ffn_split_pass_{d}", 419, d, 6, 3, I=I)
+    case = FfnCase(torch, cfg, 1, seed=d, n_slots_extra=2)
+    full = case.oracle()
+    res = case.resident
+    first, second = res[:1], res[1:]
+    t1 = case.table.copy()
+    t1[second] = -1
+    t2 = case.table.copy()
+    t2[first] = -1
+    y1 = case.run(t1)
+    ffn_close(y1, case.oracle(only=first), "pass 1")
+    y2 = case.run(t2, y0=y1, accumulate=1)
+    ffn_close(y2, full, "pass 1 + pass 2")
+    none = np.full(cfg.E, -1, np.int32)
+    assert np.array_equal(case.run(none, y0=y1, accumulate=1), y1)
+    assert (case.run(none) == 0).all()
+    assert np.array_equal(case.run(), case.run())
 
 
 def test_ffn_slots_beyond_pool_are_skipped(torch):
