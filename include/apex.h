@@ -527,6 +527,7 @@ apex_status apex_copy_kernel(void *dst, const void *src, size_t bytes, hipStream
  * (four 16-byte loads in flight per thread, 256 threads per workgroup, up to 1024
  * workgroups) that writes only one word per workgroup to `sink`: the read-only rate any
  * kernel can reach at that size, the floor against which the expert FFN is measured.
+ * Its loads are non-temporal, as the expert FFN's weight loads are.
  * sink: device uint32 [apex_read_kernel_sink_words(bytes)]. */
 size_t apex_read_kernel_sink_words(size_t bytes);
 apex_status apex_read_kernel(const void *src, size_t bytes, uint32_t *sink, hipStream_t stream);

@@ -15,6 +15,7 @@ namespace {
 
 using apex::ffn::dot8;
 using apex::ffn::kWave;
+using apex::ffn::ld_stream;
 using apex::ffn::silu;
 using apex::ffn::wave_sum;
 
@@ -58,8 +59,8 @@ __global__ __launch_bounds__(WAVES *kWave) void up_b1(
             for (int n = 0; n < NPL; ++n) {
                 const int c = cb + lane + n * kWave;
                 if (c < nch) {
-                    w1[r][n] = row[c];
-                    w3[r][n] = row[nch + c];
+                    w1[r][n] = ld_stream(row + c);
+                    w3[r][n] = ld_stream(row + nch + c);
                 }
             }
         }
@@ -126,8 +127,8 @@ __global__ __launch_bounds__(WAVES *kWave) void up_sk(
         for (int r = 0; r < R; ++r) {
             const int i = (i0 + r < I) ? i0 + r : I - 1;
             const uint4 *row = W + size_t(i) * 2 * nch;
-            w1[r] = row[c];
-            w3[r] = row[nch + c];
+            w1[r] = ld_stream(row + c);
+            w3[r] = ld_stream(row + nch + c);
         }
         xa = x4[2 * c];
         xb = x4[2 * c + 1];
@@ -215,7 +216,7 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1(
 #pragma unroll
                 for (int r = 0; r < RD; ++r) {
                     const int jr = (j0 + r < d) ? j0 + r : d - 1;
-                    w[u][r] = w2[size_t(jr) * nch + cc];
+                    w[u][r] = ld_stream(w2 + size_t(jr) * nch + cc);
                 }
             }
             cc += kWave;

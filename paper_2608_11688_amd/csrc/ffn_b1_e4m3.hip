@@ -9,6 +9,7 @@ namespace {
 
 using apex::ffn::dot16_e4m3;
 using apex::ffn::kWave;
+using apex::ffn::ld_stream;
 using apex::ffn::silu;
 using apex::ffn::wave_sum;
 
@@ -52,8 +53,8 @@ __global__ __launch_bounds__(WAVES *kWave) void up_b1_e4m3(
             for (int n = 0; n < NPL; ++n) {
                 const int c = cb + lane + n * kWave;
                 if (c < nch) {
-                    w1[r][n] = row[c];
-                    w3[r][n] = row[nch + c];
+                    w1[r][n] = ld_stream(row + c);
+                    w3[r][n] = ld_stream(row + nch + c);
                 }
             }
         }
@@ -122,8 +123,8 @@ __global__ __launch_bounds__(WAVES *kWave) void up_sk_e4m3(
         for (int r = 0; r < R; ++r) {
             const int i = (i0 + r < I) ? i0 + r : I - 1;
             const uint4 *row = W + size_t(i) * 2 * nch;
-            w1[r] = row[c];
-            w3[r] = row[nch + c];
+            w1[r] = ld_stream(row + c);
+            w3[r] = ld_stream(row + nch + c);
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) xs[q] = x4[4 * c + q];
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1_e4m3(
 #pragma unroll
                 for (int r = 0; r < RD; ++r) {
                     const int jr = (j0 + r < d) ? j0 + r : d - 1;
-                    w[u][r] = w2[size_t(jr) * nch + cc];
+                    w[u][r] = ld_stream(w2 + size_t(jr) * nch + cc);
                     sc[u][r] = s2[jr];
                 }
             }

@@ -12,6 +12,7 @@ namespace {
 
 using apex::ffn::dot16_mxfp4;
 using apex::ffn::kWave;
+using apex::ffn::ld_stream;
 using apex::ffn::mx_scale;
 using apex::ffn::silu;
 using apex::ffn::wave_sum;
@@ -56,8 +57,8 @@ __global__ __launch_bounds__(WAVES *kWave) void up_b1_mxfp4(
             for (int n = 0; n < NPL; ++n) {
                 const int c = cb + lane + n * kWave;
                 if (c < nch) {
-                    w1[r][n] = row[c];
-                    w3[r][n] = row[nch + c];
+                    w1[r][n] = ld_stream(row + c);
+                    w3[r][n] = ld_stream(row + nch + c);
                     b1[r][n] = sc1[size_t(i) * nsb + c / 2];
                     b3[r][n] = sc3[size_t(i) * nsb + c / 2];
                 }
@@ -130,8 +131,8 @@ __global__ __launch_bounds__(WAVES *kWave) void up_sk_mxfp4(
         for (int r = 0; r < R; ++r) {
             const int i = (i0 + r < I) ? i0 + r : I - 1;
             const uint2 *row = W + size_t(i) * 2 * nch;
-            w1[r] = row[c];
-            w3[r] = row[nch + c];
+            w1[r] = ld_stream(row + c);
+            w3[r] = ld_stream(row + nch + c);
             b1[r] = sc1[size_t(i) * nsb + c / 2];
             b3[r] = sc3[size_t(i) * nsb + c / 2];
         }
@@ -221,7 +222,7 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1_mxfp4(
 #pragma unroll
                 for (int r = 0; r < RD; ++r) {
                     const int jr = (j0 + r < d) ? j0 + r : d - 1;
-                    w[u][r] = w2[size_t(jr) * nch + cc];
+                    w[u][r] = ld_stream(w2 + size_t(jr) * nch + cc);
                     sb[u][r] = s2[size_t(jr) * nsb + cc / 2];
                 }
             }

@@ -32,6 +32,7 @@
 namespace {
 
 using apex::ffn::kWave;
+using apex::ffn::ld_stream;
 using apex::ffn::silu;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -267,7 +268,8 @@ struct WRegs {
             for (int j = 0; j < kLoads; ++j) {
                 const int row = wr0 + kRpp * j;
                 const int rc = row < rows_valid ? row : rows_valid - 1;
-                v[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + wkc);
+                v[m][j] = ld_stream(
+                    reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride + wkc));
             }
     }
     __device__ __forceinline__ void stage(GemmLds<NW, MT, WF> &lds, int rows_valid) const {
@@ -308,8 +310,8 @@ struct WRegs<NW, MT, WF, true> {
             for (int j = 0; j < NL; ++j) {
                 const int row = wr0 + RPP * j;
                 const int rc = row < rows_valid ? row : rows_valid - 1;
-                v[m][j] = *reinterpret_cast<const uint4 *>(wbase[m] + size_t(rc) * wstride +
-                                                           wkc / WF::kKPerElem);
+                v[m][j] = ld_stream(reinterpret_cast<const uint4 *>(
+                    wbase[m] + size_t(rc) * wstride + wkc / WF::kKPerElem));
                 if constexpr (WF::kBlockScale) sc[m][j] = sbase[m][size_t(rc) * sstride + wkc / 32];
             }
     }

@@ -5,8 +5,11 @@
 #include <cmath>
 
 #include "common.h"
+#include "ffn_device.h"
 
 namespace {
+
+using apex::ffn::ld_stream;
 
 // Spins one wavefront until `ticks` of the constant-rate device clock have passed.
 // The iteration cap only guards against a clock that fails to advance.
@@ -24,20 +27,21 @@ __global__ __launch_bounds__(256) void copy_kernel(uint4 *__restrict__ dst,
 }
 
 // Reads n 16-byte chunks with four loads in flight per thread and folds them into one
-// word per workgroup (so the loads cannot be dropped); the fold is the only write.
+// word per workgroup (so the loads cannot be dropped); the fold is the only write.  The
+// loads are non-temporal, as the expert FFN's weight loads are.
 __global__ __launch_bounds__(256) void read_kernel(const uint4 *__restrict__ src, size_t n,
                                                    uint32_t *__restrict__ sink) {
     const size_t stride = size_t(gridDim.x) * blockDim.x;
     uint32_t acc = 0;
     size_t i = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
     for (; i + 3 * stride < n; i += 4 * stride) {
-        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride],
-                    d = src[i + 3 * stride];
+        const uint4 a = ld_stream(src + i), b = ld_stream(src + i + stride),
+                    c = ld_stream(src + i + 2 * stride), d = ld_stream(src + i + 3 * stride);
         acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^
                d.z ^ d.w;
     }
     for (; i < n; i += stride) {
-        const uint4 a = src[i];
+        const uint4 a = ld_stream(src + i);
         acc ^= a.x ^ a.y ^ a.z ^ a.w;
     }
     for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o, 64);
