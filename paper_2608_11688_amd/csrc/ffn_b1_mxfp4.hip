@@ -245,6 +245,104 @@ __global__ __launch_bounds__(WAVES *kWave) void down_b1_mxfp4(
     }
 }
 
+// down_rows_mxfp4: the down projection for long flattened rows (more than 1024 units of
+// 16 codes over the executed experts, Mixtral: 1792).  The WAVES * 64 lanes hold CPL
+// units of the gated h of every valid position in registers, loaded once, so that every
+// later load is codes and their scale bytes; the workgroup then streams RW output rows,
+// G rows per step, one partial sum per row and lane.  Each row's wavefront partials
+// meet in LDS and are added in wavefront order.  Grid d / RW; n_valid * I / 16 must not
+// exceed WAVES * 64 * CPL (the dispatch checks k * I / 16).
+template <int RW, int G, int WAVES, int CPL>
+__global__ __launch_bounds__(WAVES *kWave) void down_rows_mxfp4(
+    int d, int I, int E, int k, const int32_t *__restrict__ exec_idx,
+    const int32_t *__restrict__ slot_of_expert, const uint8_t *__restrict__ slots, int n_slots,
+    size_t slot_bytes, const float *__restrict__ h, float *__restrict__ y, int accumulate) {
+    __shared__ int meta_pos[APEX_MAX_EXPERTS];
+    __shared__ size_t meta_w2[APEX_MAX_EXPERTS];
+    __shared__ size_t meta_s2[APEX_MAX_EXPERTS];
+    __shared__ int n_valid;
+    __shared__ float part[WAVES][RW];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int nch = I / 16, nsb = I / 32;
+    const uint2 *pool = reinterpret_cast<const uint2 *>(slots);
+    if (wave == 0) {
+        const int e = lane < k ? exec_idx[lane] : -1;
+        const int s = (e >= 0 && e < E) ? slot_of_expert[e] : -1;
+        const bool ok = s >= 0 && s < n_slots;
+        const unsigned long long m = __ballot(ok);
+        if (ok) {
+            const int idx = __popcll(m & ((1ull << lane) - 1ull));
+            const size_t base = size_t(s) * slot_bytes;
+            meta_pos[idx] = lane;
+            meta_w2[idx] = (base + size_t(I) * d) / 8;
+            meta_s2[idx] = base + size_t(3) * I * d / 2 + size_t(2) * I * (d / 32);
+        }
+        if (lane == 0) n_valid = __popcll(m);
+    }
+    __syncthreads();
+    const int total = n_valid * nch;
+    const int row0 = blockIdx.x * RW;
+    // this lane's units: flattened index t -> (valid position, unit of its W2 row)
+    size_t woff[CPL], soff[CPL];
+    int hoff[CPL];
+    bool on[CPL];
+#pragma unroll
+    for (int u = 0; u < CPL; ++u) {
+        const int t = threadIdx.x + u * WAVES * kWave;
+        on[u] = t < total;
+        const int it = on[u] ? t / nch : 0, cc = on[u] ? t - it * nch : 0;
+        woff[u] = meta_w2[it] + cc;
+        soff[u] = meta_s2[it] + cc / 2;
+        hoff[u] = meta_pos[it] * I + 16 * cc;
+    }
+    float acc[RW];
+#pragma unroll
+    for (int r = 0; r < RW; ++r) acc[r] = 0.f;
+    float4 hx[CPL][4];
+#pragma unroll
+    for (int rb = 0; rb < RW; rb += G) {
+        uint2 w[G][CPL];
+        uint32_t sb[G][CPL];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int jr = (row0 + rb + g < d) ? row0 + rb + g : d - 1;
+#pragma unroll
+            for (int u = 0; u < CPL; ++u)
+                if (on[u]) {
+                    w[g][u] = ld_stream(pool + woff[u] + size_t(jr) * nch);
+                    sb[g][u] = slots[soff[u] + size_t(jr) * nsb];
+                }
+        }
+        if (rb == 0) {   // h after the first rows' loads are in flight
+#pragma unroll
+            for (int u = 0; u < CPL; ++u)
+                if (on[u])
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        hx[u][q] = reinterpret_cast<const float4 *>(h + hoff[u])[q];
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int u = 0; u < CPL; ++u)
+                if (on[u])
+                    acc[rb + g] = dot16_mxfp4(w[g][u], mx_scale(sb[g][u]), hx[u], acc[rb + g]);
+    }
+#pragma unroll
+    for (int r = 0; r < RW; ++r) {
+        const float sr = wave_sum(acc[r]);
+        if (lane == 0) part[wave][r] = sr;
+    }
+    __syncthreads();
+    if (threadIdx.x < RW && row0 + int(threadIdx.x) < d) {
+        float sr = 0.f;
+#pragma unroll
+        for (int q = 0; q < WAVES; ++q) sr += part[q][threadIdx.x];
+        const int row = row0 + threadIdx.x;
+        y[row] = (accumulate ? y[row] : 0.f) + sr;
+    }
+}
+
 }  // namespace
 
 namespace apex {
@@ -288,6 +386,13 @@ apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32
         hipLaunchKernelGGL((down_b1_mxfp4<2, 1, 8>), dim3(d / 2 + (d % 2 != 0)), dim3(64), 0,
                            stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
                            slot_bytes, h, y, accumulate);
+    } else if (size_t(k) * (I / 16) > 1024 && size_t(k) * (I / 16) <= 2048) {
+        // long flattened rows: h held in registers, 16 output rows streamed per workgroup
+        // of 16 wavefronts (Mixtral call 50.7 -> 47.3 us against four rows per wavefront;
+        // at Phi-7B, 104 units, it lost: 5.5 against 4.5 us for the down projection)
+        hipLaunchKernelGGL((down_rows_mxfp4<16, 2, 16, 2>), dim3(d / 16 + (d % 16 != 0)),
+                           dim3(1024), 0, stream, d, I, E, k, exec_idx, slot_of_expert, slots,
+                           n_slots, slot_bytes, h, y, accumulate);
     } else {
         hipLaunchKernelGGL((down_b1_mxfp4<4, 4, 4>), dim3(d / 16 + (d % 16 != 0)), dim3(256), 0,
                            stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
