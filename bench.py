@@ -16,7 +16,7 @@ is timed after it; the difference is the exposed stall.
 
     python bench.py [--steps K] [--warmup W] [--config mixtral-8x7b] [--batch 1]
                     [--mode exact|stall_free] [--policy cumprob|ordinal|static|none]
-                    [--static-delta D] [--tau T] [--weights bf16|fp8|mxfp4]
+                    [--static-delta D] [--tau T] [--weights bf16|fp8|mxfp4|fp32]
                     [--window spin|attention] [--t-attn-us 10] [--ctx 1024]
                     [--no-compute-only] [--no-cpu-baseline]
 
@@ -59,9 +59,10 @@ def parse():
     p.add_argument("--policy", default="cumprob",
                    choices=["cumprob", "ordinal", "static", "none"])
     p.add_argument("--static-delta", type=int, default=0)
-    p.add_argument("--weights", default="bf16", choices=["bf16", "fp8", "mxfp4"],
+    p.add_argument("--weights", default="bf16", choices=["bf16", "fp8", "mxfp4", "fp32"],
                    help="expert weight format (fp8: E4M3 with fp32 row scales; mxfp4: E2M1 "
-                        "with a power-of-two scale per block of 32)")
+                        "with a power-of-two scale per block of 32; fp32: the bf16 experts "
+                        "stored as fp32, batch 1 only)")
     p.add_argument("--cdf-tokens", type=int, default=1024,
                    help="held-out tokens per layer for the ordinal-model fit")
     p.add_argument("--t-attn-us", type=float, default=10.0,
@@ -489,10 +490,12 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": {"fp8": "fp8-e4m3", "mxfp4": "mxfp4", "bf16": "bf16"}[args.weights],
+        "dtype": {"fp8": "fp8-e4m3", "mxfp4": "mxfp4", "bf16": "bf16",
+                  "fp32": "fp32"}[args.weights],
         "arithmetic": {"fp8": "fp8 e4m3 weights with fp32 row scales, fp32 accumulate",
                        "mxfp4": "mxfp4 (e2m1, e8m0 block scales) weights, fp32 accumulate",
-                       "bf16": "bf16 weights, fp32 accumulate"}[args.weights],
+                       "bf16": "bf16 weights, fp32 accumulate",
+                       "fp32": "fp32 weights, fp32 accumulate"}[args.weights],
         "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) bf16 experts)",
         "config": {"workload": cfg.name, "layers": L, "d": cfg.d, "E": cfg.E, "k": cfg.k,
                    "I": cfg.I, "C": cfg.C, "k_max": cfg.k_max, "tau": tau, "batch": B,

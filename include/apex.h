@@ -65,11 +65,13 @@ typedef enum {
                                  the prefetch router at all under this policy.       */
 } apex_policy;
 
-/* Expert weight format: apex_pack_expert (bf16) or apex_pack_expert_fp8 (E4M3). */
+/* Expert weight format: apex_pack_expert (bf16), apex_pack_expert_fp8 (E4M3),
+ * apex_pack_expert_mxfp4 (MXFP4) or apex_pack_expert_fp32 (fp32). */
 typedef enum {
     APEX_WEIGHTS_BF16 = 0,
     APEX_WEIGHTS_FP8_E4M3 = 1,
-    APEX_WEIGHTS_MXFP4 = 2
+    APEX_WEIGHTS_MXFP4 = 2,
+    APEX_WEIGHTS_FP32 = 3
 } apex_weights;
 
 /* Execution mode of apex_gate_topk (Sec. IV-E). */
@@ -189,6 +191,18 @@ apex_status apex_pack_expert_mxfp4(const uint16_t *w1, const uint16_t *w3, const
                                    int d, int I, void *out);
 
 /*
+ * Experts with 32-bit weights (the widest point of the precision study of Sec. V-G):
+ * fp32 copies of the bf16 experts, twice their bytes over the host link and out of HBM.
+ * apex_expert_bytes_fp32(d, I) = 12 d I bytes:
+ *   rows i = 0..I-1 of [W1[i, 0:d] | W3[i, 0:d]] (fp32), then W2 [d, I] fp32 row-major.
+ * apex_pack_expert_fp32 widens bf16 experts (w1, w3 [I, d], w2 [d, I]) into that layout
+ * exactly (host memory to host memory); d and I must be multiples of 4.
+ */
+size_t apex_expert_bytes_fp32(int d, int I);
+apex_status apex_pack_expert_fp32(const uint16_t *w1, const uint16_t *w3, const uint16_t *w2,
+                                  int d, int I, void *out);
+
+/*
  * Gated SwiGLU experts (Sec. III-A weighted sum; Sec. IV-E aggregation with the
  * original router weights).  For every token b and position j with e = exec_idx[b, j]
  * in [0, E) and s = slot_of_expert[e] in [0, n_slots):
@@ -244,15 +258,31 @@ apex_status apex_moe_ffn_mxfp4(const float *x, int B, int d, int I, int E, int k
                                size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * apex_moe_ffn over experts packed by apex_pack_expert_fp32: slot s starts at byte
+ * s * apex_expert_bytes_fp32(d, I) of `slots` (16-byte aligned); d and I multiples of 4.
+ * The same sum over fp32 weights.  Batch 1 only: B >= 2 returns APEX_E_UNSUPPORTED
+ * before anything is enqueued (the matrix-core path multiplies bf16 operands, which
+ * would drop the format's width).  Same arguments, workspace size
+ * (apex_moe_ffn_workspace_bytes) and other errors as apex_moe_ffn.
+ */
+apex_status apex_moe_ffn_fp32(const float *x, int B, int d, int I, int E, int k,
+                              const int32_t *exec_idx, const float *exec_gate,
+                              const int32_t *slot_of_expert, const void *slots, int n_slots,
+                              float *y, int accumulate, void *workspace,
+                              size_t workspace_bytes, hipStream_t stream);
+
+/*
  * apex_moe_ffn without a workspace argument, for callers that cannot allocate device
  * memory: code being captured into a graph, tight serving loops, harnesses that forbid
  * allocation.  Same computation, arguments and error behaviour as apex_moe_ffn,
- * apex_moe_ffn_fp8 or apex_moe_ffn_mxfp4, chosen by `weights` (apex_weights), with the
+ * apex_moe_ffn_fp8, apex_moe_ffn_mxfp4 or apex_moe_ffn_fp32, chosen by `weights`
+ * (apex_weights), with the
  * workspace taken from a fixed device array of APEX_NOALLOC_WORKSPACE_BYTES bytes that
  * the library holds on each GPU it runs on, from the first call on that GPU until the
  * process ends.  The call allocates and frees nothing.
- *   weights  APEX_WEIGHTS_BF16, APEX_WEIGHTS_FP8_E4M3 or APEX_WEIGHTS_MXFP4: the layout
- *            of `slots` (apex_pack_expert, _fp8 or _mxfp4)
+ *   weights  APEX_WEIGHTS_BF16, APEX_WEIGHTS_FP8_E4M3, APEX_WEIGHTS_MXFP4 or
+ *            APEX_WEIGHTS_FP32: the layout of `slots` (apex_pack_expert, _fp8, _mxfp4
+ *            or _fp32)
  * Errors, before anything is enqueued: APEX_E_CAPACITY when
  * apex_moe_ffn_workspace_bytes(B, d, I, k) exceeds APEX_NOALLOC_WORKSPACE_BYTES (every
  * workload shape here needs at most 34 MiB); the errors of apex_moe_ffn otherwise.
@@ -275,7 +305,8 @@ apex_status apex_moe_ffn_noalloc(const float *x, int B, int d, int I, int E, int
  * each; splits of one projection are added in a fixed order, so the result depends on
  * the plan but not on timing).  B < 2 (the batch-1 kernels) gives {0, 0, 0}.
  *   plan   host int32 [3] out
- * Errors: APEX_E_INVAL for a NULL plan, an unknown weights value or sizes out of range.
+ * Errors: APEX_E_INVAL for a NULL plan, an unknown weights value or sizes out of range;
+ * APEX_E_UNSUPPORTED for APEX_WEIGHTS_FP32 with B >= 2 (batch 1 only).
  */
 apex_status apex_moe_ffn_plan(int B, int d, int I, int E, int k, int n_slots, int weights,
                               int32_t *plan);
@@ -439,6 +470,7 @@ typedef struct {
     double t_attn_us;      /* attention-window stand-in per layer, >= 0 */
     int n_scratch;         /* miss-scratch slots (EXACT), >= min(E, B*k) recommended */
     int weights;           /* apex_weights: layout of host_experts, slots and scratch */
+                           /*   (APEX_WEIGHTS_FP32 needs B = 1)                        */
     int attn_heads;        /* > 0: the attention window is apex_attention_decode with this */
     int attn_kv_heads;     /*   many query / key-value heads over attn_ctx cached positions */
     int attn_ctx;          /*   (caches hold attn_ctx + 1 positions); 0: spin t_attn_us  */

@@ -105,7 +105,7 @@ def run(cfg, batch, steps, mode=gating.EXACT, tau=None, seed=0, layers=None, run
     """Replay ``steps`` decode steps of ``batch`` tokens; yields (t, layer, result).
 
     cdf: {layer: (w, theta)} ordinal-model parameters when policy is ORDINAL_CDF;
-    weights: "bf16", "fp8" or "mxfp4" expert weights (see ``ffn``);
+    weights: "bf16", "fp8", "mxfp4" or "fp32" expert weights (see ``ffn``);
     states, hidden: the layers' states (``make_states``) and hidden states
     ({layer: (h_pre, h_post)} from the seeded generator) when the caller has drawn them
     already; drawn here otherwise.

@@ -12,7 +12,9 @@ With weights="fp8" every expert matrix is first quantised row by row to E4M3 wit
 fp32 scale per row (``fp8``, the reading taken for the precision study of Sec. V-G) and
 the FFN runs on the dequantised values s_r * q, in float64.  With weights="mxfp4" every
 row is quantised in blocks of 32 along the reduction dimension to E2M1 codes with a
-power-of-two scale per block (``mxfp4``) and the FFN runs on 2^X * q.
+power-of-two scale per block (``mxfp4``) and the FFN runs on 2^X * q.  With weights="fp32"
+(the 32-bit point of the same study: the bf16 experts stored as fp32) the weights are the
+bf16 values themselves, since bf16 widens to fp32 exactly.
 """
 from __future__ import annotations
 
@@ -40,10 +42,10 @@ def moe_ffn(x, exec_idx, exec_gate, expert_bits, skip=None, weights="bf16"):
     x: [B, d]; exec_idx int [B, k] (-1 = unused position); exec_gate [B, k];
     expert_bits(e) -> (W1 bits [I,d], W3 bits [I,d], W2 bits [d,I]);
     skip: optional set of expert ids left out (a pass that only covers some experts);
-    weights: "bf16" (the weights as given), "fp8" (quantised per row first) or "mxfp4"
-    (quantised per block of 32 along each row first).
+    weights: "bf16" or "fp32" (the weights as given), "fp8" (quantised per row first) or
+    "mxfp4" (quantised per block of 32 along each row first).
     """
-    if weights not in ("bf16", "fp8", "mxfp4"):
+    if weights not in ("bf16", "fp8", "mxfp4", "fp32"):
         raise ValueError(f"unknown weight format {weights}")
     x = np.atleast_2d(np.asarray(x, dtype=np.float64))
     B, d = x.shape

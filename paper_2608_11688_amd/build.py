@@ -22,10 +22,11 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libapex.so")
 PLAN_LIB = os.path.join(PKG, "libapex_plan.so")
 
-HIP_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "pack_mxfp4.cpp", "decode.cpp",
-               "route_gate.hip", "moe_ffn.cpp", "ffn_b1.hip", "ffn_b1_e4m3.hip",
-               "ffn_b1_mxfp4.hip", "ffn_gemm.hip", "ffn_noalloc.hip", "attention.hip", "prefetch.hip", "util.hip"]
-HOST_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "pack_mxfp4.cpp"]
+HIP_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "pack_mxfp4.cpp", "pack_fp32.cpp",
+               "decode.cpp", "route_gate.hip", "moe_ffn.cpp", "ffn_b1.hip", "ffn_b1_e4m3.hip",
+               "ffn_b1_mxfp4.hip", "ffn_b1_fp32.hip", "ffn_gemm.hip", "ffn_noalloc.hip",
+               "attention.hip", "prefetch.hip", "util.hip"]
+HOST_SOURCES = ["errors.cpp", "residency.cpp", "pack_fp8.cpp", "pack_mxfp4.cpp", "pack_fp32.cpp"]
 
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
                # keep the compiler from forming packed fp32 instructions

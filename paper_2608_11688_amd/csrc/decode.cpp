@@ -145,6 +145,9 @@ apex_status run_ffn(apex_decode *dec, const float *x, int I, int E, int k, const
     if (c.weights == APEX_WEIGHTS_MXFP4)
         return apex_moe_ffn_mxfp4(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert, slots,
                                   n_slots, y, accumulate, dec->ws, dec->ws_bytes, stream);
+    if (c.weights == APEX_WEIGHTS_FP32)
+        return apex_moe_ffn_fp32(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert, slots,
+                                 n_slots, y, accumulate, dec->ws, dec->ws_bytes, stream);
     return apex_moe_ffn(x, c.B, c.d, I, E, k, idx, gate, slot_of_expert,
                         static_cast<const uint16_t *>(slots), n_slots, y, accumulate, dec->ws,
                         dec->ws_bytes, stream);
@@ -189,11 +192,17 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
                  "%s: need 1 <= k <= k_max <= C <= E (k=%d k_max=%d C=%d E=%d)", fn, c.k,
                  c.k_max, c.C, c.E);
     APEX_REQUIRE(c.t_attn_us >= 0.0 && c.t_attn_us <= 1e6, "%s: t_attn_us=%g", fn, c.t_attn_us);
-    APEX_REQUIRE(c.weights == APEX_WEIGHTS_BF16 || c.weights == APEX_WEIGHTS_FP8_E4M3 ||
-                     c.weights == APEX_WEIGHTS_MXFP4,
+    APEX_REQUIRE(c.weights >= APEX_WEIGHTS_BF16 && c.weights <= APEX_WEIGHTS_FP32,
                  "%s: unknown weight format %d", fn, c.weights);
-    // one 16-byte load holds 8 bf16 or 16 E4M3 weights; MXFP4 rows are whole 32-value blocks
-    const int mult = c.weights == APEX_WEIGHTS_BF16 ? 8 : c.weights == APEX_WEIGHTS_FP8_E4M3 ? 16 : 32;
+    if (c.weights == APEX_WEIGHTS_FP32 && c.B != 1)
+        return apex::fail(APEX_E_UNSUPPORTED, "%s: 32-bit experts run at batch 1 only (B=%d)",
+                          fn, c.B);
+    // one 16-byte load holds 4 fp32, 8 bf16 or 16 E4M3 weights; MXFP4 rows are whole
+    // 32-value blocks
+    const int mult = c.weights == APEX_WEIGHTS_FP32          ? 4
+                     : c.weights == APEX_WEIGHTS_BF16        ? 8
+                     : c.weights == APEX_WEIGHTS_FP8_E4M3    ? 16
+                                                             : 32;
     APEX_REQUIRE(c.d % mult == 0 && c.I % mult == 0,
                  "%s: weight format %d needs d and I multiples of %d (d=%d I=%d)", fn, c.weights,
                  mult, c.d, c.I);
@@ -250,6 +259,7 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
     dec->side = side;
     dec->expert_bytes = c.weights == APEX_WEIGHTS_FP8_E4M3 ? apex_expert_bytes_fp8(c.d, c.I)
                         : c.weights == APEX_WEIGHTS_MXFP4  ? apex_expert_bytes_mxfp4(c.d, c.I)
+                        : c.weights == APEX_WEIGHTS_FP32   ? apex_expert_bytes_fp32(c.d, c.I)
                                                            : apex_expert_bytes(c.d, c.I);
     auto cleanup = [&](apex_status st) {
         apex_decode_destroy(dec);

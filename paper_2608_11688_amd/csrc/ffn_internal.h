@@ -13,7 +13,15 @@
 namespace apex {
 
 // Expert weight formats of a slot pool.
-enum class WeightFormat { kBf16, kE4M3, kMxfp4 };
+enum class WeightFormat { kBf16, kE4M3, kMxfp4, kF32 };
+
+// The format of an apex_weights code (checked to be in range by the caller).
+inline WeightFormat format_of(int weights) {
+    return weights == APEX_WEIGHTS_FP8_E4M3 ? WeightFormat::kE4M3
+           : weights == APEX_WEIGHTS_MXFP4  ? WeightFormat::kMxfp4
+           : weights == APEX_WEIGHTS_FP32   ? WeightFormat::kF32
+                                            : WeightFormat::kBf16;
+}
 
 // One token: up_b1 then down_b1.  `h` is k x I fp32 scratch.
 size_t ffn_b1_workspace(int d, int I, int k);
@@ -32,6 +40,12 @@ apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32
                          const float *exec_gate, const int32_t *slot_of_expert,
                          const uint8_t *slots, int n_slots, float *h, float *y, int accumulate,
                          hipStream_t stream);
+
+// The same over apex_pack_expert_fp32 slots (d and I multiples of 4).
+apex_status ffn_b1_fp32(const float *x, int d, int I, int E, int k, const int32_t *exec_idx,
+                        const float *exec_gate, const int32_t *slot_of_expert,
+                        const float *slots, int n_slots, float *h, float *y, int accumulate,
+                        hipStream_t stream);
 
 // Two or more tokens: grouped GEMMs on the matrix cores, over slots of format fmt.  `workspace` is 256-byte aligned and holds ffn_grouped_workspace(B, d, I, k)
 // bytes.

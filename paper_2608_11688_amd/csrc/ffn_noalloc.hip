@@ -52,8 +52,11 @@ extern "C" apex_status apex_moe_ffn_noalloc(const float *x, int B, int d, int I,
                                             int n_slots, int weights, float *y, int accumulate,
                                             hipStream_t stream) {
     const char *fn = "apex_moe_ffn_noalloc";
-    APEX_REQUIRE(weights >= APEX_WEIGHTS_BF16 && weights <= APEX_WEIGHTS_MXFP4,
+    APEX_REQUIRE(weights >= APEX_WEIGHTS_BF16 && weights <= APEX_WEIGHTS_FP32,
                  "%s: weights=%d is not an APEX_WEIGHTS_* value", fn, weights);
+    if (weights == APEX_WEIGHTS_FP32 && B >= 2)
+        return apex::fail(APEX_E_UNSUPPORTED, "%s: 32-bit experts run at batch 1 only (B=%d)",
+                          fn, B);
     if (B > 0 && B <= APEX_MAX_PAIRS && k >= 1 && d >= 1 && I >= 1) {
         const size_t need = apex_moe_ffn_workspace_bytes(B, d, I, k);
         if (need > APEX_NOALLOC_WORKSPACE_BYTES)
@@ -65,10 +68,7 @@ extern "C" apex_status apex_moe_ffn_noalloc(const float *x, int B, int d, int I,
     void *ws = nullptr;
     apex_status st = scratch_on_current_device(fn, &ws);
     if (st != APEX_OK) return st;
-    const apex::WeightFormat fmt = weights == APEX_WEIGHTS_FP8_E4M3 ? apex::WeightFormat::kE4M3
-                                   : weights == APEX_WEIGHTS_MXFP4  ? apex::WeightFormat::kMxfp4
-                                                                    : apex::WeightFormat::kBf16;
-    return apex::moe_ffn_checked(fn, fmt, x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
+    return apex::moe_ffn_checked(fn, apex::format_of(weights), x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert,
                                  slots, n_slots, y, accumulate, ws, APEX_NOALLOC_WORKSPACE_BYTES,
                                  stream);
 }

@@ -23,7 +23,7 @@ PLAN_LIB_PATH = os.path.join(PKG, "libapex_plan.so")
 APEX_OK, APEX_E_INVAL, APEX_E_UNSUPPORTED, APEX_E_HIP, APEX_E_CAPACITY = 0, -1, -2, -3, -4
 SEL_CUMPROB, SEL_ORDINAL_CDF, SEL_STATIC, SEL_NONE = 0, 1, 2, 3
 MODE_EXACT, MODE_STALL_FREE = 0, 1
-WEIGHTS_BF16, WEIGHTS_FP8_E4M3, WEIGHTS_MXFP4 = 0, 1, 2
+WEIGHTS_BF16, WEIGHTS_FP8_E4M3, WEIGHTS_MXFP4, WEIGHTS_FP32 = 0, 1, 2, 3
 ABI_VERSION = 4
 MAX_EXPERTS = 64
 MAX_PAIRS = 1024
@@ -84,10 +84,13 @@ SIGNATURES = {
     "apex_pack_expert_fp8": (I32, [P, P, P, I32, I32, P]),
     "apex_expert_bytes_mxfp4": (SZ, [I32, I32]),
     "apex_pack_expert_mxfp4": (I32, [P, P, P, I32, I32, P]),
+    "apex_expert_bytes_fp32": (SZ, [I32, I32]),
+    "apex_pack_expert_fp32": (I32, [P, P, P, I32, I32, P]),
     "apex_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32, I32]),
     "apex_moe_ffn": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_fp8": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_mxfp4": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
+    "apex_moe_ffn_fp32": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, P, I32, P, SZ, P]),
     "apex_moe_ffn_plan": (I32, [I32, I32, I32, I32, I32, I32, I32, P]),
     "apex_moe_ffn_noalloc": (I32, [P, I32, I32, I32, I32, I32, P, P, P, P, I32, I32, P, I32, P]),
     "apex_attention_workspace_bytes": (SZ, [I32, I32, I32, I32, I32]),
@@ -117,7 +120,8 @@ SIGNATURES = {
 
 HOST_ONLY = ("apex_abi_version", "apex_last_error", "apex_expert_bytes", "apex_pack_expert",
              "apex_expert_bytes_fp8", "apex_pack_expert_fp8", "apex_expert_bytes_mxfp4",
-             "apex_pack_expert_mxfp4", "apex_plan_residency")
+             "apex_pack_expert_mxfp4", "apex_expert_bytes_fp32", "apex_pack_expert_fp32",
+             "apex_plan_residency")
 
 
 def header_functions(path=HEADER):
@@ -224,6 +228,14 @@ def apex_pack_expert_mxfp4(w1, w3, w2, d, I, out, L=None):
     _call("apex_pack_expert_mxfp4", ptr(w1), ptr(w3), ptr(w2), d, I, ptr(out), L=L)
 
 
+def apex_expert_bytes_fp32(d, I, L=None):
+    return (L or lib()).apex_expert_bytes_fp32(d, I)
+
+
+def apex_pack_expert_fp32(w1, w3, w2, d, I, out, L=None):
+    _call("apex_pack_expert_fp32", ptr(w1), ptr(w3), ptr(w2), d, I, ptr(out), L=L)
+
+
 def apex_moe_ffn_workspace_bytes(B, d, I, k):
     return lib().apex_moe_ffn_workspace_bytes(B, d, I, k)
 
@@ -257,9 +269,16 @@ def apex_moe_ffn_mxfp4(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, sl
           workspace_bytes, stream)
 
 
+def apex_moe_ffn_fp32(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots,
+                      y, accumulate, workspace, workspace_bytes, stream=None):
+    _call("apex_moe_ffn_fp32", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
+          ptr(slot_of_expert), ptr(slots), n_slots, ptr(y), int(accumulate), ptr(workspace),
+          workspace_bytes, stream)
+
+
 def apex_moe_ffn_noalloc(x, B, d, I, E, k, exec_idx, exec_gate, slot_of_expert, slots, n_slots,
                          weights, y, accumulate, stream=None):
-    """weights: an APEX_WEIGHTS_* code or a format name ("bf16", "fp8", "mxfp4")."""
+    """weights: an APEX_WEIGHTS_* code or a format name ("bf16", "fp8", "mxfp4", "fp32")."""
     code = WEIGHT_FORMATS[weights][0] if isinstance(weights, str) else int(weights)
     _call("apex_moe_ffn_noalloc", ptr(x), B, d, I, E, k, ptr(exec_idx), ptr(exec_gate),
           ptr(slot_of_expert), ptr(slots), n_slots, code, ptr(y), int(accumulate), stream)
@@ -271,6 +290,7 @@ WEIGHT_FORMATS = {
     "fp8": (WEIGHTS_FP8_E4M3, "apex_expert_bytes_fp8", "apex_pack_expert_fp8", "apex_moe_ffn_fp8"),
     "mxfp4": (WEIGHTS_MXFP4, "apex_expert_bytes_mxfp4", "apex_pack_expert_mxfp4",
               "apex_moe_ffn_mxfp4"),
+    "fp32": (WEIGHTS_FP32, "apex_expert_bytes_fp32", "apex_pack_expert_fp32", "apex_moe_ffn_fp32"),
 }
 
 

@@ -384,6 +384,13 @@ def test_decode_deepseek_shape_mxfp4_batch16():
     check_decode(configs.DEEPSEEK_16B, 16, native.MODE_STALL_FREE, 2, [4], weights="mxfp4")
 
 
+def test_decode_granite1b_fp32_experts():
+    # 32-bit experts through the whole decode path: twice the bytes of every copy
+    cfg = configs.GRANITE_1B
+    st = check_decode(cfg, 1, native.MODE_EXACT, 4, [0, 23], weights="fp32")
+    assert st["copies"] > 0
+
+
 def test_decode_create_rejects_bad_configurations():
     # validation happens before anything is allocated or enqueued
     from paper_2608_11688_amd.runtime import DecodeRunner
@@ -394,6 +401,10 @@ def test_decode_create_rejects_bad_configurations():
     bad_i = dataclasses.replace(cfg, I=80)
     with pytest.raises(native.ApexError):
         DecodeRunner(bad_i, batch=1, steps=1, weights="mxfp4")
+    # 32-bit experts run at batch 1 only
+    with pytest.raises(native.ApexError) as ei:
+        DecodeRunner(cfg, batch=2, steps=1, weights="fp32")
+    assert ei.value.status == native.APEX_E_UNSUPPORTED
     # shared experts need an intermediate size that fits the weight format
     bad_shared = dataclasses.replace(cfg, shared=1, I_shared=40)
     with pytest.raises(native.ApexError):

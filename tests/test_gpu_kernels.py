@@ -463,6 +463,45 @@ def test_ffn_mxfp4_mixtral_batch1_and_two_passes(torch):
     ffn_close(case.run(t2, y0=y1, accumulate=1), case.oracle(), "mxfp4 pass 1 + pass 2")
 
 
+FP32_SHAPES = [
+    # 32-bit experts (apex_moe_ffn_fp32, batch 1 only): d and I multiples of 4; the up
+    # projection's workgroup covers the row one 16-byte chunk (4 values) per lane
+    (configs.GRANITE_1B, 1), (configs.GRANITE_3B, 1), (configs.OLMOE, 1), (configs.TINY, 1),
+    (configs.PHI_7B, 1), (configs.DEEPSEEK_16B, 1),
+    (shape("fp32_d260", 510, 260, 5, 3, I=76), 1),        # 65 chunks on 128 lanes
+    (shape("fp32_d1028", 511, 1028, 4, 2, I=44), 1),      # 257 chunks on 512 lanes
+    (shape("fp32_d4100", 512, 4100, 4, 2, I=36), 1),      # beyond 4096: a row pair per wavefront
+    (shape("fp32_two_rows", 513, 520, 3, 2, I=8200), 1),  # I*k > 16384: two row pairs
+]
+
+
+@pytest.mark.parametrize("cfg,B", FP32_SHAPES, ids=[f"{c.name}-B{b}" for c, b in FP32_SHAPES])
+def test_ffn_fp32_parity(torch, cfg, B):
+    case = FfnCase(torch, cfg, B, seed=cfg.cfg_id * 13 + B, weights="fp32")
+    y = case.run()
+    print(cfg.name, B, ffn_close(y, case.oracle(), f"{cfg.name} B{B} fp32"))
+
+
+def test_ffn_fp32_mixtral_batch1_two_passes_and_repeat(torch):
+    # the Mixtral shape (704 MB experts), then two passes, absent experts and a repeated
+    # call at a small shape
+    case = FfnCase(torch, configs.MIXTRAL, 1, seed=52, weights="fp32")
+    print("mixtral fp32", ffn_close(case.run(), case.oracle(), "mixtral B1 fp32"))
+    cfg = shape("fp32_pass", 514, 1028, 6, 3, I=76)
+    case = FfnCase(torch, cfg, 1, seed=53, n_slots_extra=2, weights="fp32")
+    res = case.resident
+    t1, t2 = case.table.copy(), case.table.copy()
+    t1[res[1:]] = -1
+    t2[res[:1]] = -1
+    y1 = case.run(t1)
+    ffn_close(y1, case.oracle(only=res[:1]), "fp32 pass 1")
+    ffn_close(case.run(t2, y0=y1, accumulate=1), case.oracle(), "fp32 pass 1 + pass 2")
+    none = np.full(cfg.E, -1, np.int32)
+    assert np.array_equal(case.run(none, y0=y1, accumulate=1), y1)
+    assert (case.run(none) == 0).all()
+    assert np.array_equal(case.run(), case.run())
+
+
 def test_ffn_mxfp4_rejects_partial_blocks(torch):
     A = 4096
     with pytest.raises(native.ApexError):

@@ -236,6 +236,44 @@ def test_pack_expert_fp8_matches_the_oracle_quantiser(plan_lib):
         native.apex_pack_expert_fp8(w1, w3, w2, 44, I, out, L=plan_lib)   # d not a multiple of 8
 
 
+def test_pack_expert_fp32_widens_bf16_exactly(plan_lib):
+    # the 32-bit slot holds the bf16 weights widened to fp32, bit for bit, in the bf16
+    # slot's order
+    d, I = 12, 20
+    rng = np.random.default_rng(43)
+    def bf16(a):
+        return (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    w1, w3 = bf16(rng.standard_normal((I, d))), bf16(rng.standard_normal((I, d)) * 1e-3)
+    w2 = bf16(rng.standard_normal((d, I)) * 40.0)
+    nbytes = native.apex_expert_bytes_fp32(d, I, L=plan_lib)
+    assert nbytes == 12 * d * I
+    out = np.zeros(nbytes // 4, np.uint32)
+    native.apex_pack_expert_fp32(w1, w3, w2, d, I, out, L=plan_lib)
+    widen = lambda w: w.astype(np.uint32) << 16
+    rows = out[:2 * I * d].reshape(I, 2 * d)
+    assert np.array_equal(rows[:, :d], widen(w1)) and np.array_equal(rows[:, d:], widen(w3))
+    assert np.array_equal(out[2 * I * d:].reshape(d, I), widen(w2))
+    with pytest.raises(native.ApexError):
+        native.apex_pack_expert_fp32(w1, w3, w2, 10, I, out, L=plan_lib)   # d not a multiple of 4
+
+
+def test_fp32_experts_run_at_batch1_only(hip_lib):
+    # refused before anything is enqueued: more than one token, a size off the 4-value
+    # grid, and the grouped plan for 32-bit experts
+    A = 4096
+    msg = _expect(native.APEX_E_UNSUPPORTED, native.apex_moe_ffn_fp32, A, 2, 64, 64, 8, 2, A, A,
+                  A, A, 1, A, 0, A, 1 << 30)
+    assert "batch 1" in msg
+    _expect(native.APEX_E_UNSUPPORTED, native.apex_moe_ffn_noalloc, A, 2, 64, 64, 8, 2, A, A, A,
+            A, 1, "fp32", A, 0)
+    _expect(native.APEX_E_INVAL, native.apex_moe_ffn_fp32, A, 1, 64, 62, 8, 2, A, A, A, A, 1, A,
+            0, A, 1 << 30)
+    assert native.apex_moe_ffn_plan(1, 64, 64, 8, 2, 8, weights="fp32") == (0, 0, 0)
+    with pytest.raises(native.ApexError) as ei:
+        native.apex_moe_ffn_plan(2, 64, 64, 8, 2, 8, weights="fp32")
+    assert ei.value.status == native.APEX_E_UNSUPPORTED
+
+
 def test_moe_ffn_plan():
     # batch 1 takes the batch-1 kernels; bad arguments are errors
     assert native.apex_moe_ffn_plan(1, 2048, 1024, 64, 8, 24) == (0, 0, 0)

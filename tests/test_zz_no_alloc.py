@@ -53,6 +53,17 @@ def test_noalloc_equals_workspace_entry_point(torch, weights, d, I):
         assert np.array_equal(acc.view(np.uint32), acc_ref.view(np.uint32)), (weights, B)
 
 
+def test_noalloc_fp32_batch1(torch):
+    # 32-bit experts run at batch 1 only: two calls in a row, the second smaller
+    for i, (d, I) in enumerate(((1028, 516), (516, 260))):
+        cfg = shape(f"noalloc_fp32_{d}", 481 + i, d, 24, 6, I=I)
+        case = FfnCase(torch, cfg, 1, seed=910 + i, weights="fp32")
+        ref = case.run()
+        got = run_noalloc(torch, case)
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), d
+        ffn_close(got, case.oracle(), f"noalloc fp32 d{d}")
+
+
 def test_noalloc_largest_workload_shape(torch):
     # the largest workspace any workload needs (Mixtral shape, 32 tokens: 34 MiB) fits,
     # checked on sampled tokens against the workspace entry point
