@@ -329,16 +329,88 @@ def compute_only_leg(torch, args, cfg, make_runner, host_runner):
         runner.close()
 
 
-def delta_star_leg(cfg, tokens=256, max_layers=8):
-    """Mean delta* (Eq. 3: how deep in the prefetch ranking the deepest routed expert
-    sits, beyond k) over held-out tokens of up to `max_layers` evenly spaced layers,
-    from the router and gate kernels."""
-    from paper_2608_11688_amd import cdf_fit
-    layers = sorted(set(np.linspace(0, cfg.L - 1, min(cfg.L, max_layers)).astype(int).tolist()))
-    d = [cdf_fit.collect_samples(cfg, l, tokens)[1] for l in layers]
-    d = np.concatenate(d)
-    return dict(mean=round(float(d.mean()), 4), p90=int(np.percentile(d, 90)),
-                tokens=int(d.size), layers=layers)
+def selection_stats(ranked, routed, pf_sel, pf_count, k):
+    """Prefetch accounting of one layer, per token, from the router's whole ranking
+    `ranked` [n, N] (best first), the routed set `routed` [n, k], the policy's selection
+    `pf_sel` [n, >= max m] (ranked order, -1 after position m) and its size `pf_count`
+    [n]: delta* (Eq. 3), delta_hat = max(m - k, 0) (Eq. 9; 0 when nothing is fetched),
+    the overlap |K_r & K_p| / k and full coverage K_r subset of K_p (Eq. 2)."""
+    ranked = np.asarray(ranked, np.int64)
+    routed = np.asarray(routed, np.int64)
+    pf_sel = np.asarray(pf_sel, np.int64)
+    m = np.asarray(pf_count, np.int64)
+    n, N = ranked.shape
+    rows = np.arange(n)[:, None]
+    pos = np.empty((n, N), np.int64)
+    pos[rows, ranked] = np.arange(N)[None, :]
+    dstar = np.maximum(pos[rows, routed].max(axis=1) + 1 - k, 0)
+    slot = np.arange(pf_sel.shape[1])[None, :]
+    sel = np.where(slot < m[:, None], pf_sel, -1)
+    hit = (routed[:, :, None] == sel[:, None, :]).any(axis=2)
+    return dict(delta_star=dstar, delta_hat=np.maximum(m - k, 0), m=m,
+                overlap=hit.sum(axis=1) / k, coverage=hit.all(axis=1))
+
+
+def per_layer_leg(cfg, policy, tau, static_delta, cdf, tokens=256, seed=2, streams=64):
+    """Prefetch quality of every layer on `tokens` held-out tokens (hidden-state streams of
+    their own seed: disjoint from the timed decode's and from the ordinal fit's), from the
+    router and gate kernels: the router once with the whole ranking (static budget N - k,
+    k_max = N) and once with the bench's policy, then the exact gate top-k.  Returns the
+    per-layer means of delta*, delta_hat, overlap and coverage, the delta* histogram over
+    every layer (index delta* = 0 .. N - k) and the histogram of the prefetched-set size
+    m = k + delta_hat (index m = 0 .. k_max; m = 0 only with no prefetch)."""
+    import torch
+    from paper_2608_11688_amd import inputs, native
+    E, k, d = cfg.E, cfg.k, cfg.d
+    dev = torch.device("cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    steps = -(-tokens // streams)
+    rows = dict(delta_star=[], delta_hat=[], recall=[], full_coverage=[])
+    dstar_all, m_all = [], []
+    for l in range(cfg.L):
+        h_pre, h_post = inputs.hidden_states(cfg, l, streams, steps, seed)
+        h_pre, h_post = h_pre.reshape(-1, d)[:tokens], h_post.reshape(-1, d)[:tokens]
+        wg, wpf, bias = inputs.router_weights(cfg, l, 0)
+        b = None if bias is None else t(bias.astype(np.float32))
+        hp, wp = t(h_pre), t(wpf.view(np.int16))
+        cdf_w = cdf_theta = None
+        if policy == native.SEL_ORDINAL_CDF:
+            w, theta = (inputs.cdf_params(cfg, l, 0) if cdf is None
+                        else cdf[l] if isinstance(cdf, dict) else cdf)
+            cdf_w, cdf_theta = t(np.asarray(w, np.float32)), t(np.asarray(theta, np.float32))
+        full = torch.empty((tokens, E), dtype=torch.int32, device=dev)
+        sel = torch.empty((tokens, cfg.k_max), dtype=torch.int32, device=dev)
+        cnt_full = torch.empty((tokens,), dtype=torch.int32, device=dev)
+        cnt = torch.empty_like(cnt_full)
+        prob = torch.empty((tokens, E), dtype=torch.float32, device=dev)
+        native.apex_prefetch_route(hp, wp, b, tokens, d, E, k, E, native.SEL_STATIC, 0.0,
+                                   E - k, None, None, full, cnt_full, prob, stream)
+        native.apex_prefetch_route(hp, wp, b, tokens, d, E, k, cfg.k_max, policy, tau,
+                                   static_delta, cdf_w, cdf_theta, sel, cnt, prob, stream)
+        route_idx = torch.empty((tokens, k), dtype=torch.int32, device=dev)
+        route_gate = torch.empty((tokens, k), dtype=torch.float32, device=dev)
+        exec_idx, exec_gate = torch.empty_like(route_idx), torch.empty_like(route_gate)
+        native.apex_gate_topk(t(h_post), t(wg.view(np.int16)), b, tokens, d, E, k,
+                              native.MODE_EXACT, None, 0, route_idx, route_gate, exec_idx,
+                              exec_gate, None, stream)
+        torch.cuda.synchronize()
+        st = selection_stats(full.cpu().numpy(), route_idx.cpu().numpy(), sel.cpu().numpy(),
+                             cnt.cpu().numpy(), k)
+        rows["delta_star"].append(round(float(st["delta_star"].mean()), 3))
+        rows["delta_hat"].append(round(float(st["delta_hat"].mean()), 3))
+        rows["recall"].append(round(float(st["overlap"].mean()), 4))
+        rows["full_coverage"].append(round(float(st["coverage"].mean()), 4))
+        dstar_all.append(st["delta_star"])
+        m_all.append(st["m"])
+    dstar_all, m_all = np.concatenate(dstar_all), np.concatenate(m_all)
+    summary = dict(mean=round(float(dstar_all.mean()), 4),
+                   p90=int(np.percentile(dstar_all, 90)), tokens=int(dstar_all.size),
+                   layers=cfg.L)
+    return summary, dict(tokens_per_layer=tokens, **rows,
+                         delta_star_hist=np.bincount(dstar_all, minlength=E - k + 1).tolist(),
+                         prefetch_size_hist=np.bincount(m_all,
+                                                        minlength=cfg.k_max + 1).tolist())
 
 
 def oracle_sample(cfg, batch, weights, policy, cdf, preload_bytes=8e9, threads=16):
@@ -477,7 +549,7 @@ def main():
     runner.close()
     del runner
     copy_leg = expert_copy_leg(torch, native, S, cfg.E, h2d_peak)
-    dstar = delta_star_leg(cfg)
+    dstar, per_layer = per_layer_leg(cfg, policy, tau, args.static_delta, cdf)
     release(torch)
     out = {
         "metric": "MoE-layer decode us/token + expert-weight HBM GB/s; prefetch recall vs oracle",
@@ -511,6 +583,7 @@ def main():
         "cache_hit_rate": round(s["hit_rate"], 5),
         "mean_delta_star": dstar["mean"],
         "delta_star": dstar,
+        "per_layer": per_layer,
         "copies_per_layer_step": round(s["copies_per_layer_step"], 4),
         "copied_MB_per_layer_step": round(s["copies_per_layer_step"] * S / 1e6, 3),
         "misses_per_layer_step": round(s["misses_per_layer_step"], 4),

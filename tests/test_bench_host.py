@@ -6,6 +6,7 @@ import os
 import subprocess
 import sys
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -60,3 +61,27 @@ def test_oracle_sample_of_large_experts(bench):
     cfg = configs.CONFIGS["mixtral-8x7b"]
     S = 6 * cfg.d * cfg.I
     assert int(8e9 // (cfg.E * S)) == 2 and S >= (64 << 20)
+
+
+def test_selection_stats_match_the_oracle_metrics(bench):
+    """The per-layer leg's host accounting against the oracle's enumerations of Eq. 2, Eq. 3
+    and the overlap of Sec. V-C, on random rankings, routed sets and prefix sizes
+    (m = 0, the no-prefetch case, included)."""
+    from oracle import metrics
+    rng = np.random.default_rng(7)
+    N, k, k_max, n = 12, 3, 8, 400
+    ranked = np.stack([rng.permutation(N) for _ in range(n)])
+    routed = np.stack([rng.choice(N, k, replace=False) for _ in range(n)])
+    m = rng.integers(0, k_max + 1, n)
+    m[:10] = 0
+    sel = np.where(np.arange(k_max)[None, :] < m[:, None], ranked[:, :k_max], -1)
+    st = bench.selection_stats(ranked, routed, sel, m, k)
+    for i in range(n):
+        K_p = [int(e) for e in sel[i] if e >= 0]
+        assert st["delta_star"][i] == metrics.delta_star(list(ranked[i]), list(routed[i]), k)
+        assert st["delta_hat"][i] == max(int(m[i]) - k, 0)
+        assert st["overlap"][i] == pytest.approx(metrics.overlap(routed[i], K_p, k))
+        assert bool(st["coverage"][i]) == metrics.full_coverage(routed[i], K_p)
+    # entries past m are ignored even when they hold expert ids
+    st2 = bench.selection_stats(ranked, routed, ranked[:, :k_max], m, k)
+    assert np.array_equal(st2["overlap"], st["overlap"])
