@@ -43,8 +43,19 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-FFN_KERNELS = {True: "apex_moe_ffn (up_sk or up_b1, then down_b1)",
-               False: "apex_moe_ffn (up_gemm + down_gemm + combine_pairs)"}
+# PCIe 5.0 x16, one direction: 32 GT/s x 16 lanes with 128b/130b encoding
+PCIE_PEAK_GBPS = 32.0 * 16 * 128 / 130 / 8
+# the kernels of one FFN call, per weight format, at batch 1 and at batch >= 2
+FFN_KERNELS = {
+    ("bf16", True): "apex_moe_ffn (up_sk or up_b1, then down_b1)",
+    ("fp8", True): "apex_moe_ffn_fp8 (up_sk_e4m3 or up_b1_e4m3, then down_b1_e4m3)",
+    ("mxfp4", True): "apex_moe_ffn_mxfp4 (up_sk_mxfp4 or up_b1_mxfp4, then down_b1_mxfp4 or "
+                     "down_rows_mxfp4)",
+    ("fp32", True): "apex_moe_ffn_fp32 (up_sk_f32 or up_b1_f32, then down_f32)",
+    ("bf16", False): "apex_moe_ffn (up_gemm + down_gemm + combine_pairs)",
+    ("fp8", False): "apex_moe_ffn_fp8 (up_gemm + down_gemm + combine_pairs, E4M3 tiles)",
+    ("mxfp4", False): "apex_moe_ffn_mxfp4 (up_gemm + down_gemm + combine_pairs, MXFP4 tiles)",
+}
 
 
 def parse():
@@ -145,7 +156,9 @@ def expert_copy_leg(torch, native, expert_bytes, E, link_peak, reps=5):
             "us": round(us_kernel, 2), "GBps": round(gbps, 2),
             "dma_per_expert_us": round(us_dma, 2),
             "link_peak_GBps": round(link_peak, 2),
-            "frac_of_link_peak": round(gbps / link_peak, 4)}
+            "frac_of_link_peak": round(gbps / link_peak, 4),
+            "published_link_GBps": round(PCIE_PEAK_GBPS, 2),
+            "frac_of_published_link": round(gbps / PCIE_PEAK_GBPS, 4)}
 
 
 def ffn_roofline_leg(torch, native, runner, reps=8, seed=123):
@@ -600,7 +613,7 @@ def main():
         "h2d_pinned_peak_GBps": round(h2d_peak, 2),
         "copy_leg": copy_leg,
         "hbm_copy_kernel": calib,
-        "roofline": {"bound": "hbm", "kernel": FFN_KERNELS[B == 1],
+        "roofline": {"bound": "hbm", "kernel": FFN_KERNELS[(args.weights, B == 1)],
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic(cfg, B, args.weights),

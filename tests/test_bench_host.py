@@ -85,3 +85,11 @@ def test_selection_stats_match_the_oracle_metrics(bench):
     # entries past m are ignored even when they hold expert ids
     st2 = bench.selection_stats(ranked, routed, ranked[:, :k_max], m, k)
     assert np.array_equal(st2["overlap"], st["overlap"])
+
+
+def test_every_weight_format_names_its_kernels(bench):
+    for w in ("bf16", "fp8", "mxfp4", "fp32"):
+        assert (w, True) in bench.FFN_KERNELS
+        if w != "fp32":                    # fp32 experts run at batch 1 only
+            assert (w, False) in bench.FFN_KERNELS
+    assert abs(bench.PCIE_PEAK_GBPS - 63.015) < 1e-2
