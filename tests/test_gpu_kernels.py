@@ -5,6 +5,7 @@ the CPU in float64.  Index sets must match exactly except at near ties (counted)
 FFN outputs within the tolerance stated in tests/parity.py.
 """
 import dataclasses
+import os
 
 import numpy as np
 import pytest
@@ -754,3 +755,12 @@ def test_read_kernel_reads_every_chunk(torch):
         assert got == want, n_words
     with pytest.raises(native.ApexError):
         native.apex_read_kernel(src, 12, sink, s)
+
+
+def test_readme_example_runs(torch):
+    """The Python example of README.md, run as written."""
+    import re
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    text = open(os.path.join(root, "README.md")).read()
+    code = re.search(r"<!-- example: moe_ffn -->\s*```python\n(.*?)```", text, re.S).group(1)
+    exec(compile(code, "README.md example", "exec"), {})
