@@ -71,10 +71,3 @@ def quantize_rows(W):
 
 def dequantize_rows(codes, scales) -> np.ndarray:
     return decode_array(codes) * np.asarray(scales, dtype=np.float64)[:, None]
-
-
-def expert_fp8(w1, w3, w2):
-    """Quantise one expert given as float64 matrices (W1 [I, d], W3 [I, d], W2 [d, I]).
-
-    Returns ((codes, scales) for W1, W3 and W2)."""
-    return quantize_rows(w1), quantize_rows(w3), quantize_rows(w2)

@@ -105,7 +105,3 @@ def stall_free_algorithm1(K_r, q_r, K_p):
     candidates = K_p - kept
     ranked = sorted(candidates, key=lambda e: (-alpha[e], e))
     return kept | set(ranked[:len(missing)])
-
-
-def top_k_ids(z_row, k):
-    return rank_experts(z_row)[:k]

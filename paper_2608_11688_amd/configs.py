@@ -10,7 +10,7 @@ Values the workload descriptions leave open are fixed here and listed with the o
 readings in the design notes: the Granite-3B cache and cap (C = 16, k_max = 16) and
 the OLMoE cap and target (k_max = 16, tau = 0.9, 256 steps).
 """
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 from typing import Tuple
 
 

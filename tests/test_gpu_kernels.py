@@ -4,7 +4,6 @@ Inputs come from the seeded generators; the oracle computes the expected values 
 the CPU in float64.  Index sets must match exactly except at near ties (counted);
 FFN outputs within the tolerance stated in tests/parity.py.
 """
-import dataclasses
 import os
 
 import numpy as np

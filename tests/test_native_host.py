@@ -6,7 +6,6 @@
 * invalid arguments are rejected before anything is enqueued (no HIP call is made on
   these paths, so they run without a GPU).
 """
-import ctypes
 
 import numpy as np
 import pytest
