@@ -115,7 +115,7 @@ __device__ __forceinline__ uint4 swiglu8(const float *r, size_t stride) {
 // the row and kRowsPerPass rows are loaded per pass of the workgroup.
 struct WBf16 {           // apex_pack_expert slots: bf16 weights
     using T = uint16_t;
-    static constexpr bool kFp8 = false, kBlockScale = false, kCodes = false;
+    [[maybe_unused]] static constexpr bool kFp8 = false, kBlockScale = false, kCodes = false;
     template <int MT> static constexpr int kb() { return kKB; }
     static constexpr int kUpGroups = 400;
     static constexpr int kKPerElem = 1;
@@ -224,7 +224,6 @@ template <int NW, int MT, class WF>
 __device__ __forceinline__ uint4 widen8(const GemmLds<NW, MT, WF, true> &lds, int m, int rr,
                                         int kc) {
     if constexpr (WF::kBlockScale) {
-        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
         const uint32_t c = *reinterpret_cast<const uint32_t *>(&lds.Wc[m][rr][kc / 2]);
         const float sc = apex::ffn::mx_scale(lds.Sc[m][rr][kc / 32]);
         return make_uint4(
