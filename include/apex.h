@@ -28,6 +28,10 @@
  *    message of the last failing call on the calling thread is apex_last_error().
  *  - Supported sizes: 1 <= E <= 64 experts, 1 <= k <= k_max <= E, d and I multiples
  *    of 8 (16-byte rows of bf16), B >= 0 tokens (B = 0 enqueues nothing).
+ *  - apex_prefetch_route, apex_gate_topk and the apex_moe_ffn entry points only launch
+ *    kernels on the given stream (no allocation, memory set, copy or synchronisation),
+ *    so a caller may capture them in a HIP graph; apex_moe_ffn_noalloc's first call on
+ *    a device looks up that device's scratch array and must come before the capture.
  */
 #ifndef APEX_H
 #define APEX_H

@@ -763,3 +763,118 @@ def test_readme_example_runs(torch):
     text = open(os.path.join(root, "README.md")).read()
     code = re.search(r"<!-- example: moe_ffn -->\s*```python\n(.*?)```", text, re.S).group(1)
     exec(compile(code, "README.md example", "exec"), {})
+
+
+GRAPH_CASES = [(configs.GRANITE_1B, 1, "bf16"), (configs.MIXTRAL, 1, "bf16"),
+               (configs.GRANITE_3B, 8, "bf16"), (configs.OLMOE, 16, "fp8"),
+               (configs.OLMOE, 1, "mxfp4"), (configs.GRANITE_1B, 1, "fp32")]
+
+
+@pytest.mark.parametrize("cfg,B,weights", GRAPH_CASES,
+                         ids=[f"{c.name}-B{b}-{w}" for c, b, w in GRAPH_CASES])
+def test_ffn_replayed_from_a_captured_graph_matches_eager(torch, cfg, B, weights):
+    """The FFN entry points allocate nothing and set no memory inside a call, so a caller can
+    capture them in a HIP graph: every replay, with new activations copied in, eager calls
+    and synchronisations between the replays, equals the eager call on the same inputs bit
+    for bit (the workspace entry point and the one that allocates nothing)."""
+    case = FfnCase(torch, cfg, B, seed=cfg.cfg_id * 7 + B, weights=weights)
+    d, I, E, k = cfg.d, cfg.I, cfg.E, cfg.k
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    x, idx, gate, table = dev(case.x), dev(case.exec_idx), dev(case.gate), dev(case.table)
+    ws_bytes = native.apex_moe_ffn_workspace_bytes(B, d, I, k)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    calls = {
+        "workspace": lambda out, s: case.ffn(x, B, d, I, E, k, idx, gate, table, case.pool,
+                                             case.n_slots, out, 0, ws, ws_bytes, s),
+        "noalloc": lambda out, s: native.apex_moe_ffn_noalloc(
+            x, B, d, I, E, k, idx, gate, table, case.pool, case.n_slots, weights, out, 0, s),
+    }
+    rng = np.random.default_rng(cfg.cfg_id)
+    for name, call in calls.items():
+        y = torch.zeros((B, d), device="cuda")
+        y_eager = torch.zeros_like(y)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            call(y, side.cuda_stream)          # first call outside the capture
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            call(y, side.cuda_stream)
+        torch.cuda.synchronize()
+        for r in range(3):
+            x.copy_(dev(rng.standard_normal((B, d)).astype(np.float32)))
+            y.fill_(float("nan"))
+            graph.replay()
+            torch.cuda.synchronize()
+            call(y_eager, torch.cuda.current_stream().cuda_stream)
+            torch.cuda.synchronize()
+            assert torch.equal(y, y_eager), (name, r)
+            assert torch.isfinite(y).all(), (name, r)
+        del graph
+
+
+@pytest.mark.parametrize("cfg,B", [(configs.GRANITE_1B, 1), (configs.OLMOE, 4)],
+                         ids=["granite-1b-a400m-B1", "olmoe-1b-7b-B4"])
+def test_router_gate_ffn_chain_replayed_from_a_captured_graph(torch, cfg, B):
+    """The device side of a layer-step with every expert resident (prefetch router, gate
+    top-k, expert FFN reading the gate's executed sets from device memory) captured as one
+    HIP graph: each replay, with new hidden states copied in and eager work between the
+    replays, gives the eager chain's sets and outputs bit for bit."""
+    d, I, E, k = cfg.d, cfg.I, cfg.E, cfg.k
+    S = native.apex_expert_bytes(d, I)
+    host = np.empty(E * S // 2, np.uint16)
+    for e in range(E):
+        w1, w3, w2 = inputs.expert_weights(cfg, 0, e)
+        native.apex_pack_expert(w1, w3, w2, d, I, host[e * S // 2:])
+    pool = dev(torch, host.view(np.int16))
+    table = dev(torch, np.arange(E, dtype=np.int32))
+    wg, wpf, bias = inputs.router_weights(cfg, 0)
+    wg, wpf = dev(torch, wg.view(np.int16)), dev(torch, wpf.view(np.int16))
+    bias = None if bias is None else dev(torch, bias.astype(np.float32))
+    h_pre, h_post = inputs.hidden_states(cfg, 0, B, 4)
+    x_pre, x_post = dev(torch, h_pre[0]), dev(torch, h_post[0])
+    ws_bytes = native.apex_moe_ffn_workspace_bytes(B, d, I, k)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    i32 = dict(dtype=torch.int32, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+
+    def buffers():
+        return dict(pf_idx=torch.empty((B, cfg.k_max), **i32), pf_count=torch.empty(B, **i32),
+                    route_idx=torch.empty((B, k), **i32), route_gate=torch.empty((B, k), **f32),
+                    exec_idx=torch.empty((B, k), **i32), exec_gate=torch.empty((B, k), **f32),
+                    y=torch.empty((B, d), **f32))
+
+    def chain(o, s):
+        native.apex_prefetch_route(x_pre, wpf, bias, B, d, E, k, cfg.k_max,
+                                   native.SEL_CUMPROB, cfg.tau, 0, None, None, o["pf_idx"],
+                                   o["pf_count"], None, s)
+        native.apex_gate_topk(x_post, wg, bias, B, d, E, k, native.MODE_EXACT, None, 0,
+                              o["route_idx"], o["route_gate"], o["exec_idx"], o["exec_gate"],
+                              None, s)
+        native.apex_moe_ffn(x_post, B, d, I, E, k, o["exec_idx"], o["exec_gate"], table, pool,
+                            E, o["y"], 0, ws, ws_bytes, s)
+
+    graph_out, eager_out = buffers(), buffers()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        chain(graph_out, side.cuda_stream)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        chain(graph_out, side.cuda_stream)
+    torch.cuda.synchronize()
+    for t in range(1, 4):
+        x_pre.copy_(dev(torch, h_pre[t]))
+        x_post.copy_(dev(torch, h_post[t]))
+        for v in graph_out.values():
+            v.fill_(-7)
+        graph.replay()
+        torch.cuda.synchronize()
+        chain(eager_out, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        for name in graph_out:
+            assert torch.equal(graph_out[name], eager_out[name]), (name, t)
+        assert (graph_out["exec_idx"] >= 0).all()
+    del graph
