@@ -209,9 +209,10 @@ def stream_floor_leg(torch, native, cs, nbytes, n=192, buf_bytes=1 << 30):
     """Device time of a plain read of the FFN call's weight bytes, split into two
     launches as the FFN splits them (W1/W3 rows, then W2 rows): the fastest any kernel
     can bring those bytes in at that size on this GPU.  Each launch reads fresh memory
-    (a 1 GB buffer, far larger than the 256 MB Infinity Cache).  Returns mean us per
-    call."""
+    (a buffer of 1 GB, or twice the larger launch's bytes, far larger than the 256 MB
+    Infinity Cache).  Returns mean us per call."""
     parts = [int(nbytes * 2 / 3) // 256 * 256, int(nbytes / 3) // 256 * 256]
+    buf_bytes = max(buf_bytes, 2 * max(parts))   # every read stays inside the buffer
     buf = torch.empty(buf_bytes, dtype=torch.uint8, device="cuda")
     sink = torch.empty(native.apex_read_kernel_sink_words(max(parts)), dtype=torch.int32,
                        device="cuda")
@@ -536,7 +537,11 @@ def main():
                             static_delta=args.static_delta, cdf=cdf, weights=args.weights,
                             window=args.window, ctx=args.ctx, **kw)
 
-    runner = make_runner(cfg)
+    try:
+        runner = make_runner(cfg)
+    except ValueError as e:       # a workload the runner refuses, before anything is drawn
+        print(f"bench.py: {e}", file=sys.stderr)
+        return 2
     h2d_peak = pinned_h2d_peak(torch)
     ms_per_step = time_steps(torch, runner, args.steps, args.warmup)
     leg_ms, leg_bytes, leg_n = ffn_roofline_leg(torch, native, runner)

@@ -27,6 +27,9 @@ def _torch():
     return torch
 
 
+MAX_PINNED_EXPERT_BYTES = 32 << 30
+
+
 @dataclass
 class StepLog:
     pf_idx: np.ndarray
@@ -72,6 +75,15 @@ class DecodeRunner:
         self.n_scratch = min(E, B * k) if n_scratch is None else n_scratch
         L = len(self.layers)
 
+        # every layer's experts are held in pinned host memory at once; a Mixtral-shaped
+        # stack with fp32 experts (8 x 8 experts of 705 MB, 45 GB) ended in a host
+        # segmentation fault before its first output, cause not established, so the
+        # runner stays within what has run
+        pinned = L * E * self.S
+        if host_experts_from is None and pinned > MAX_PINNED_EXPERT_BYTES:
+            raise ValueError(f"{L} layers of {E} {weights} experts need {pinned / 1e9:.1f} GB "
+                             f"of pinned host memory; the runner holds at most "
+                             f"{MAX_PINNED_EXPERT_BYTES / 2**30:.0f} GiB")
         if host_experts_from is not None:
             o = host_experts_from
             if (o.cfg.d, o.cfg.I, o.cfg.E, o.weights, o.seed) != (cfg.d, cfg.I, cfg.E, weights,

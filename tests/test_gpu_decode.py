@@ -409,6 +409,9 @@ def test_decode_create_rejects_bad_configurations():
     bad_shared = dataclasses.replace(cfg, shared=1, I_shared=40)
     with pytest.raises(native.ApexError):
         DecodeRunner(bad_shared, batch=1, steps=1, weights="fp8")
+    # more pinned host experts than the runner holds: refused before anything is drawn
+    with pytest.raises(ValueError, match="pinned host memory"):
+        DecodeRunner(configs.MIXTRAL, batch=1, steps=1, weights="fp32")
     # a good configuration still builds and steps
     r = DecodeRunner(dataclasses.replace(cfg, shared=1, I_shared=64), batch=1, steps=1,
                      weights="mxfp4")
