@@ -31,10 +31,12 @@ def test_traffic_record_needs_the_same_source_and_flags(bench, tmp_path, monkeyp
     from paper_2608_11688_amd import build, configs
     cfg = configs.CONFIGS["mixtral-8x7b"]          # the bench's default workload
     recs = json.load(open(os.path.join(ROOT, "profiles", "moe_ffn_traffic.json")))["records"]
-    rec = [r for r in recs if r["workload"] == cfg.name and r["batch"] == 1][0]
-    assert bench.measured_traffic(cfg, 1) == rec["traffic_bytes_per_call"]
+    pick = lambda w: [r for r in recs if r["workload"] == cfg.name and r["batch"] == 1 and
+                      r["weights"] == w][0]
+    assert bench.measured_traffic(cfg, 1) == pick("bf16")["traffic_bytes_per_call"]
+    assert bench.measured_traffic(cfg, 1, weights="fp8") == pick("fp8")["traffic_bytes_per_call"]
     assert bench.measured_traffic(cfg, 8) is None                  # no record for batch 8
-    assert bench.measured_traffic(cfg, 1, weights="fp8") is None
+    assert bench.measured_traffic(cfg, 1, weights="fp32") is None  # nor for fp32 experts
     monkeypatch.setattr(build, "HIPCC_FLAGS", build.HIPCC_FLAGS + ["-DOTHER"])
     assert bench.measured_traffic(cfg, 1) is None                  # other compiler flags
 
