@@ -420,3 +420,25 @@ def test_decode_create_rejects_bad_configurations():
         r.finish()
     finally:
         r.close()
+
+
+@pytest.mark.parametrize("cfg,batch,mode,layers", [
+    (configs.GRANITE_1B, 1, native.MODE_EXACT, [0, 23]),
+    (configs.GRANITE_3B, 1, native.MODE_STALL_FREE, [7]),
+    (configs.OLMOE, 1, native.MODE_EXACT, [4]),
+], ids=["granite-1b-a400m-exact", "granite-3b-a800m-stall-free", "olmoe-1b-7b-exact"])
+def test_decode_every_step_of_the_workload(cfg, batch, mode, layers):
+    """Every decode step of the workload (256) on some of its layers: after hundreds of
+    cache plans (eviction by last use, ties between equal last uses) the resident sets,
+    the prefetched, routed and executed sets, the misses and the driver's counters still
+    match the oracle's replay; the FFN output is checked every 64th layer-step."""
+    st = check_decode(cfg, batch, mode, cfg.steps, layers, ffn_every=64)
+    assert st["copies"] > 0 and st["ffn_checked"] >= 4
+
+
+def test_decode_mixtral_shape_first_16_steps():
+    """Steps 0-15 of a Mixtral-shaped layer: a 352 MB expert copied at most steps, the
+    sets and cache state against the oracle at every step, the FFN output at the last."""
+    cfg = configs.MIXTRAL
+    st = check_decode(cfg, 1, native.MODE_EXACT, 16, [6], ffn_at={(15, 6)})
+    assert st["copies"] > 0 and st["ffn_checked"] == 1
