@@ -100,15 +100,23 @@ __device__ void token_logits(const float *__restrict__ h, const uint16_t *__rest
 }
 
 // Position of expert `lane` when experts are ordered by descending logit, lower id
-// first on equal logits, counting only experts whose bit is set in `mask`.  Other
-// lanes' logits are read with readlane (register to scalar), not through LDS.
-__device__ __forceinline__ int masked_rank(float z, int E, int lane, unsigned long long mask) {
+// first on equal logits, counting only experts whose bit is set in `mask` (no bit at or
+// beyond E).  The logits are read from LDS four at a time, every lane at the same address
+// (a broadcast): against other lanes' logits read with readlane (register to scalar, one
+// at a time) the router took 6.20 -> 5.51 us at the Granite-1B shape and 11.34 -> 10.63
+// at OLMoE's, with the same ranks.  z_lds is 16-byte aligned and holds 64 entries.
+__device__ __forceinline__ int masked_rank(const float *z_lds, float z, int E, int lane,
+                                           unsigned long long mask) {
     int r = 0;
-    const int zi = __float_as_int(z);
-    for (int j = 0; j < E; ++j) {
-        const float zj = __int_as_float(__builtin_amdgcn_readlane(zi, j));
-        const bool beats = (zj > z) || (zj == z && j < lane);
-        r += (beats && ((mask >> j) & 1ull)) ? 1 : 0;
+    const float4 *z4 = reinterpret_cast<const float4 *>(z_lds);
+    for (int j4 = 0; j4 < (E + 3) / 4; ++j4) {
+        const float4 q = z4[j4];
+        const int j = 4 * j4;
+        const unsigned long long mb = mask >> j;
+        r += ((mb & 1ull) && (q.x > z || (q.x == z && j < lane))) ? 1 : 0;
+        r += ((mb & 2ull) && (q.y > z || (q.y == z && j + 1 < lane))) ? 1 : 0;
+        r += ((mb & 4ull) && (q.z > z || (q.z == z && j + 2 < lane))) ? 1 : 0;
+        r += ((mb & 8ull) && (q.w > z || (q.w == z && j + 3 < lane))) ? 1 : 0;
     }
     return r;
 }
@@ -134,7 +142,7 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     int static_delta, const float *__restrict__ cdf_w, const float *__restrict__ cdf_theta,
     int32_t *__restrict__ pf_idx, int32_t *__restrict__ pf_count, float *__restrict__ pf_prob,
     int32_t *__restrict__ done, int32_t seq) {
-    __shared__ float z_lds[APEX_MAX_EXPERTS];
+    __shared__ __align__(16) float z_lds[APEX_MAX_EXPERTS];
     __shared__ float sorted_q[APEX_MAX_EXPERTS];
     __shared__ int sorted_id[APEX_MAX_EXPERTS];
 
@@ -150,7 +158,7 @@ __global__ __launch_bounds__(kThreads) void prefetch_route_kernel(
     const float p = live ? expf(z - mx) : 0.f;
     const float q = p / wave_sum(p);
     const unsigned long long all = (E == 64) ? ~0ull : ((1ull << E) - 1ull);
-    const int r = masked_rank(z, E, lane, all);   // whole wavefront: readlane inside
+    const int r = masked_rank(z_lds, z, E, lane, all);
     if (live) {
         sorted_q[r] = q;
         sorted_id[r] = lane;
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     float *__restrict__ route_gate, int32_t *__restrict__ exec_idx,
     float *__restrict__ exec_gate, float *__restrict__ gate_prob, int32_t *__restrict__ done,
     int32_t seq) {
-    __shared__ float z_lds[APEX_MAX_EXPERTS];
+    __shared__ __align__(16) float z_lds[APEX_MAX_EXPERTS];
 
     const int b = blockIdx.x;
     token_logits<NC, EPP>(h_post + size_t(b) * d, w_g, b_g, d, E, z_lds);
@@ -212,7 +220,7 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     const float psum = wave_sum(p);
     const unsigned long long all = (E == 64) ? ~0ull : ((1ull << E) - 1ull);
 
-    const int r = masked_rank(z, E, lane, all);
+    const int r = masked_rank(z_lds, z, E, lane, all);
     const bool sel_r = live && r < k;
     const float rsum = wave_sum(sel_r ? p : 0.f);
     const size_t row = size_t(b) * k;
@@ -228,7 +236,7 @@ __global__ __launch_bounds__(kThreads) void gate_topk_kernel(
     } else {
         const bool a = live && avail[size_t(b) * avail_stride + lane] != 0;
         const unsigned long long amask = __ballot(a);
-        const int ra = masked_rank(z, E, lane, amask);
+        const int ra = masked_rank(z_lds, z, E, lane, amask);
         const bool sel = a && ra < k;
         const int n_sel = __popcll(__ballot(sel));
         const float xsum = wave_sum(sel ? p : 0.f);
