@@ -422,17 +422,25 @@ def test_decode_create_rejects_bad_configurations():
         r.close()
 
 
-@pytest.mark.parametrize("cfg,batch,mode,layers", [
-    (configs.GRANITE_1B, 1, native.MODE_EXACT, [0, 23]),
-    (configs.GRANITE_3B, 1, native.MODE_STALL_FREE, [7]),
-    (configs.OLMOE, 1, native.MODE_EXACT, [4]),
-], ids=["granite-1b-a400m-exact", "granite-3b-a800m-stall-free", "olmoe-1b-7b-exact"])
-def test_decode_every_step_of_the_workload(cfg, batch, mode, layers):
+@pytest.mark.parametrize("cfg,batch,mode,layers,weights", [
+    (configs.GRANITE_1B, 1, native.MODE_EXACT, [0, 23], "bf16"),
+    (configs.GRANITE_3B, 1, native.MODE_STALL_FREE, [7], "bf16"),
+    (configs.OLMOE, 1, native.MODE_EXACT, [4], "bf16"),
+    (configs.GRANITE_3B, 8, native.MODE_EXACT, [30], "bf16"),
+    (configs.DEEPSEEK_16B, 1, native.MODE_STALL_FREE, [12], "bf16"),
+    (configs.PHI_7B, 1, native.MODE_EXACT, [3], "fp8"),
+    (configs.GRANITE_1B, 1, native.MODE_EXACT, [9], "mxfp4"),
+], ids=["granite-1b-a400m-exact", "granite-3b-a800m-stall-free", "olmoe-1b-7b-exact",
+        "granite-3b-a800m-B8-exact", "deepseek-16b-shared-stall-free", "phi-7b-fp8-exact",
+        "granite-1b-a400m-mxfp4-exact"])
+def test_decode_every_step_of_the_workload(cfg, batch, mode, layers, weights):
     """Every decode step of the workload (256) on some of its layers: after hundreds of
-    cache plans (eviction by last use, ties between equal last uses) the resident sets,
-    the prefetched, routed and executed sets, the misses and the driver's counters still
-    match the oracle's replay; the FFN output is checked every 64th layer-step."""
-    st = check_decode(cfg, batch, mode, cfg.steps, layers, ffn_every=64)
+    cache plans (eviction by last use, ties between equal last uses; at batch 8 the union
+    of the tokens' sets) the resident sets, the prefetched, routed and executed sets, the
+    misses and the driver's counters still match the oracle's replay; the FFN output
+    (with DeepSeek's shared experts, and over E4M3 or MXFP4 slots) is checked every 64th
+    layer-step."""
+    st = check_decode(cfg, batch, mode, cfg.steps, layers, ffn_every=64, weights=weights)
     assert st["copies"] > 0 and st["ffn_checked"] >= 4
 
 
