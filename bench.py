@@ -205,6 +205,32 @@ def ffn_roofline_leg(torch, native, runner, reps=8, seed=123):
     return ms, nbytes, n
 
 
+def router_leg(torch, native, runner, reps=8):
+    """Device time of the prefetch router (apex_prefetch_route with the bench's policy) on
+    every layer's weights in turn, queued behind a spin kernel, one event pair around
+    them.  Returns us per call."""
+    cfg, B = runner.cfg, runner.B
+    pf_idx = torch.empty((B, cfg.k_max), dtype=torch.int32, device="cuda")
+    pf_count = torch.empty((B,), dtype=torch.int32, device="cuda")
+    n = reps * len(runner.layers)
+    e0, e1 = native.apex_event_create(True), native.apex_event_create(True)
+    torch.cuda.synchronize()
+    native.apex_spin_us(min(2000.0 + 20.0 * n, 1e6), runner.cs)
+    native.apex_event_record(e0, runner.cs)
+    for i in range(n):
+        b = runner.bufs[runner.layers[i % len(runner.layers)]]
+        native.apex_prefetch_route(b["h_pre"][0], b["wpf"], b["bias"], B, cfg.d, cfg.E, cfg.k,
+                                   cfg.k_max, runner.policy, runner.tau, runner.static_delta,
+                                   b["cdf_w"], b["cdf_theta"], pf_idx, pf_count, None,
+                                   runner.cs)
+    native.apex_event_record(e1, runner.cs)
+    native.apex_event_synchronize(e1)
+    us = native.apex_event_elapsed_ms(e0, e1) * 1e3 / n
+    native.apex_event_destroy(e0)
+    native.apex_event_destroy(e1)
+    return us
+
+
 def stream_floor_leg(torch, native, cs, nbytes, n=192, buf_bytes=1 << 30):
     """Device time of a plain read of the FFN call's weight bytes, split into two
     launches as the FFN splits them (W1/W3 rows, then W2 rows): the fastest any kernel
@@ -545,6 +571,7 @@ def main():
     h2d_peak = pinned_h2d_peak(torch)
     ms_per_step = time_steps(torch, runner, args.steps, args.warmup)
     leg_ms, leg_bytes, leg_n = ffn_roofline_leg(torch, native, runner)
+    router_us = None if policy == native.SEL_NONE else router_leg(torch, native, runner)
     floor_us = stream_floor_leg(torch, native, runner.cs, leg_bytes)
     calib = copy_calibration(torch, native, runner.cs)
 
@@ -602,6 +629,14 @@ def main():
         "mean_delta_star": dstar["mean"],
         "delta_star": dstar,
         "per_layer": per_layer,
+        "router": None if router_us is None else {
+            "us_per_call": round(router_us, 3),
+            "share_of_layer_step": round(router_us / us_layer_step, 5),
+            "share_of_compute_only_layer_step": (
+                None if value_resident is None
+                else round(router_us / (value_resident * B + window_us), 5)),
+            # the paper's overhead count per layer: the router's d x E weights plus 2E
+            "extra_params_per_layer": cfg.d * cfg.E + 2 * cfg.E},
         "copies_per_layer_step": round(s["copies_per_layer_step"], 4),
         "copied_MB_per_layer_step": round(s["copies_per_layer_step"] * S / 1e6, 3),
         "misses_per_layer_step": round(s["misses_per_layer_step"], 4),
