@@ -16,7 +16,9 @@
  *                         mode                                       (Sec. IV-E)
  *
  * Conventions, for every entry point:
- *  - Buffers are owned by the caller.  No entry point allocates or frees memory.
+ *  - Buffers are owned by the caller.  No entry point allocates or frees memory, except
+ *    apex_decode_create and apex_decode_destroy, which set up and release the decode
+ *    driver's own staging and tables (setup time, not the hot path).
  *  - "device" pointers are HBM addresses (hipMalloc or equivalent); "host" pointers
  *    are ordinary host memory; "pinned" pointers are page-locked host memory
  *    (hipHostMalloc or equivalent).  Device pointers must be 16-byte aligned.
