@@ -6,6 +6,13 @@
 // the host spins on, so the hand-off costs microseconds.  Overlap statistics are folded
 // in lazily, once a layer's gate is known to have finished.
 //
+// A layer whose every expert is resident (C = E, no slot empty) can neither copy nor
+// miss, so the host needs neither set in time: its router, window, gate and FFN go to
+// the compute stream back to back with no wait, and the prefetched sets, the statistics
+// and the host's cache plan (which then only renews last uses) are taken when the
+// layer-step is folded, before the layer's next router writes its staging again.
+// Recorded steps take the general route.
+//
 // Two streams.  The compute stream carries the chain that bounds a layer whenever the
 // copies cannot be hidden: router, expert copies, expert FFN, next layer's router.
 // Kernels back to back on one queue start without a gap, while an event recorded
@@ -55,8 +62,8 @@ struct apex_decode {
     float *shared_gate = nullptr;      // device [B][n_shared]
     int32_t *shared_table = nullptr;   // device [n_shared]
     // pinned staging
-    int32_t *pf_idx_h = nullptr;      // [B][k_max]
-    int32_t *pf_count_h = nullptr;    // [B]
+    int32_t *pf_idx_h = nullptr;      // [L][B][k_max], one slice per layer
+    int32_t *pf_count_h = nullptr;    // [L][B]
     int32_t *route_idx_h = nullptr;   // [L][B][k]
     float *route_gate_h = nullptr;    // [L][B][k]
     // completion flags the router and gate kernels write into pinned memory after their
@@ -77,6 +84,11 @@ struct apex_decode {
         std::vector<int32_t> cnt;      // [B]
         std::vector<char> resident;    // [E]
         int copies, misses;
+        // a layer-step whose every expert was resident, enqueued without waiting for the
+        // router: its prefetched sets are read (and the host's cache plan, which then
+        // only renews last uses, is run) when it is folded
+        bool deferred = false;
+        int64_t step = 0;
     };
     std::vector<Pending> pending;
 };
@@ -161,17 +173,122 @@ apex_status ffn(apex_decode *dec, const float *x, const int32_t *slot_of_expert,
                    n_slots, y, accumulate, dec->compute);
 }
 
-// Folds the statistics of every pending layer-step once its gate has published the
-// routed sets (normally long done: it precedes that layer's FFN).
-apex_status fold_pending(apex_decode *dec, apex_decode_stats *st) {
-    const int B = dec->cfg.B;
-    for (const auto &p : dec->pending) {
-        const apex_status s = poll_done(dec->gate_done_h + size_t(p.layer) * B, B, p.seq,
-                                        p.gate_stream);
+// Folds one pending layer-step once its gate has published the routed sets (normally
+// long done: it precedes that layer's FFN).  A deferred layer-step first takes its
+// prefetched sets from the layer's staging slice (the router ran before the gate on the
+// same stream) and runs the host's cache plan on them, which with every expert resident
+// copies nothing and only renews last uses.
+apex_status fold_one(apex_decode *dec, apex_decode::Pending &p, apex_decode_stats *st) {
+    const apex_decode_config &c = dec->cfg;
+    const int B = c.B;
+    apex_status s = poll_done(dec->gate_done_h + size_t(p.layer) * B, B, p.seq, p.gate_stream);
+    if (s != APEX_OK) return s;
+    if (p.deferred) {
+        const int32_t *pf = dec->pf_idx_h + size_t(p.layer) * B * c.k_max;
+        const int32_t *cnt = dec->pf_count_h + size_t(p.layer) * B;
+        p.pf.assign(pf, pf + size_t(B) * c.k_max);
+        p.cnt.assign(cnt, cnt + B);
+        const apex_decode_layer &Ly = dec->layers[p.layer];
+        int32_t ce[APEX_MAX_EXPERTS], cs[APEX_MAX_EXPERTS];
+        int n = 0;
+        s = apex_plan_residency(c.E, c.C, pf, cnt, B, c.k_max, p.step, Ly.expert_of_slot,
+                                Ly.last_used, ce, cs, &n);
         if (s != APEX_OK) return s;
-        fold(dec, p, st);
+        APEX_REQUIRE(n == 0, "apex_decode_step: layer %d planned %d copies with every expert "
+                     "resident", p.layer, n);
     }
-    dec->pending.clear();
+    fold(dec, p, st);
+    return APEX_OK;
+}
+
+// Folds every pending layer-step (layer < 0), or those of one layer.
+apex_status fold_pending(apex_decode *dec, apex_decode_stats *st, int layer = -1) {
+    auto &v = dec->pending;
+    size_t keep = 0;
+    for (size_t i = 0; i < v.size(); ++i) {
+        if (layer >= 0 && v[i].layer != layer) {
+            if (keep != i) v[keep] = std::move(v[i]);
+            ++keep;
+            continue;
+        }
+        const apex_status s = fold_one(dec, v[i], st);
+        if (s != APEX_OK) return s;
+    }
+    v.resize(keep);
+    return APEX_OK;
+}
+
+// Every expert of the layer is resident (C = E, no slot empty): no copy and no miss can
+// happen, so nothing of the layer-step waits for the host.
+bool all_resident(const apex_decode_config &c, const apex_decode_layer &Ly) {
+    if (c.C < c.E) return false;
+    for (int s = 0; s < c.C; ++s)
+        if (Ly.expert_of_slot[s] < 0) return false;
+    return true;
+}
+
+// The attention window of layer l on `stream`: the layer's decode attention, or the
+// spin of t_attn_us.
+apex_status window(apex_decode *dec, int l, const float *h_pre, hipStream_t stream) {
+    const apex_decode_config &c = dec->cfg;
+    const apex_decode_layer &Ly = dec->layers[l];
+    if (c.attn_heads > 0)
+        return apex_attention_decode(h_pre, Ly.w_qkv, Ly.w_o, c.B, c.d, c.attn_heads,
+                                     c.attn_kv_heads, c.d / c.attn_heads, Ly.k_cache,
+                                     Ly.v_cache, c.attn_ctx + 1, c.attn_ctx, Ly.attn_out,
+                                     dec->attn_ws, dec->attn_ws_bytes, stream);
+    if (c.t_attn_us > 0) return apex_spin_us(c.t_attn_us, stream);
+    return APEX_OK;
+}
+
+// A layer-step with every expert resident: router, window, gate (with the shared
+// experts) and FFN queued back to back on the compute stream, no host wait.  Nothing is
+// copied or missed; the statistics and the host's cache plan wait for the fold.
+apex_status enqueue_resident(apex_decode *dec, int l, int64_t step, int32_t seq,
+                             const float *h_pre, const float *h_post, float *y) {
+    const apex_decode_config &c = dec->cfg;
+    const apex_decode_layer &Ly = dec->layers[l];
+    const hipStream_t cs = dec->compute;
+    int32_t *pf_h = dec->pf_idx_h + size_t(l) * c.B * c.k_max;
+    int32_t *pfc_h = dec->pf_count_h + size_t(l) * c.B;
+    apex_status st;
+    if (c.policy != APEX_SEL_NONE) {
+        // the flag is not waited for, but its system-scope fence orders the sets in host
+        // memory before the gate's flag, which the fold waits for
+        st = apex::prefetch_route(h_pre, Ly.w_pf, Ly.b_pf, c.B, c.d, c.E, c.k, c.k_max,
+                                  c.policy, c.tau, c.static_delta, Ly.cdf_w, Ly.cdf_theta, pf_h,
+                                  pfc_h, nullptr, dec->route_done, seq, cs);
+        if (st != APEX_OK) return st;
+    } else {
+        std::fill(pf_h, pf_h + size_t(c.B) * c.k_max, -1);
+        std::fill(pfc_h, pfc_h + c.B, 0);
+    }
+    st = window(dec, l, h_pre, cs);
+    if (st != APEX_OK) return st;
+    st = apex::gate_topk(h_post, Ly.w_g, Ly.b_g, c.B, c.d, c.E, c.k, c.mode, Ly.avail_dev, 0,
+                         dec->route_idx_h + size_t(l) * c.B * c.k,
+                         dec->route_gate_h + size_t(l) * c.B * c.k, dec->exec_idx,
+                         dec->exec_gate, nullptr, dec->gate_done_h + size_t(l) * c.B, seq, cs);
+    if (st != APEX_OK) return st;
+    const bool shared = c.n_shared > 0;
+    if (shared) {
+        st = run_ffn(dec, h_post, c.I_shared, c.n_shared, c.n_shared, dec->shared_idx,
+                     dec->shared_gate, dec->shared_table, Ly.shared_slots, c.n_shared, y, 0,
+                     cs);
+        if (st != APEX_OK) return st;
+    }
+    st = ffn(dec, h_post, Ly.slot_of_expert_dev, Ly.slots, c.C, y, shared ? 1 : 0);
+    if (st != APEX_OK) return st;
+    apex_decode::Pending p;
+    p.layer = l;
+    p.seq = seq;
+    p.gate_stream = cs;
+    p.resident.assign(c.E, 1);
+    p.copies = 0;
+    p.misses = 0;
+    p.deferred = true;
+    p.step = step;
+    dec->pending.push_back(std::move(p));
     return APEX_OK;
 }
 
@@ -272,9 +389,11 @@ extern "C" apex_status apex_decode_create(apex_decode **out, const apex_decode_c
         if (st != APEX_OK) return cleanup(st);
     }
     hipError_t e = hipSuccess;
-    e = hipHostMalloc(reinterpret_cast<void **>(&dec->pf_idx_h), sizeof(int32_t) * c.B * c.k_max);
+    e = hipHostMalloc(reinterpret_cast<void **>(&dec->pf_idx_h),
+                      sizeof(int32_t) * c.L * c.B * c.k_max);
     if (e == hipSuccess)
-        e = hipHostMalloc(reinterpret_cast<void **>(&dec->pf_count_h), sizeof(int32_t) * c.B);
+        e = hipHostMalloc(reinterpret_cast<void **>(&dec->pf_count_h),
+                          sizeof(int32_t) * c.L * c.B);
     if (e == hipSuccess)
         e = hipHostMalloc(reinterpret_cast<void **>(&dec->route_idx_h),
                           sizeof(int32_t) * c.L * c.B * c.k);
@@ -349,15 +468,24 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         // sequence number of this layer-step (never 0, the flags' initial value)
         dec->seq = dec->seq == INT32_MAX ? 1 : dec->seq + 1;
         const int32_t seq = dec->seq;
+        // this layer's previous layer-step is folded before its staging is written again
+        st = fold_pending(dec, stats, l);
+        if (st != APEX_OK) return st;
+        if (!rec && all_resident(c, Ly)) {
+            st = enqueue_resident(dec, l, step, seq, h_pre[l], h_post[l], y[l]);
+            if (st != APEX_OK) return st;
+            continue;
+        }
+        int32_t *pf_h = dec->pf_idx_h + size_t(l) * c.B * c.k_max;
+        int32_t *pfc_h = dec->pf_count_h + size_t(l) * c.B;
         if (route) {
             st = apex::prefetch_route(h_pre[l], Ly.w_pf, Ly.b_pf, c.B, c.d, c.E, c.k, c.k_max,
                                       c.policy, c.tau, c.static_delta, Ly.cdf_w, Ly.cdf_theta,
-                                      dec->pf_idx_h, dec->pf_count_h, nullptr, dec->route_done,
-                                      seq, cs);
+                                      pf_h, pfc_h, nullptr, dec->route_done, seq, cs);
             if (st != APEX_OK) return st;
         } else {
-            std::fill(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max, -1);
-            std::fill(dec->pf_count_h, dec->pf_count_h + c.B, 0);
+            std::fill(pf_h, pf_h + size_t(c.B) * c.k_max, -1);
+            std::fill(pfc_h, pfc_h + c.B, 0);
         }
         if (route) {
             st = poll_done(dec->route_done, c.B, seq, cs);
@@ -368,7 +496,7 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         // anything is copied (the no-prefetch baseline never copies)
         int n_copy = 0;
         st = apex::expert_prefetch(dec->host_view[l], Ly.slots, c.E, c.C, dec->expert_bytes,
-                                   dec->pf_idx_h, dec->pf_count_h, c.B, c.k_max, step,
+                                   pf_h, pfc_h, c.B, c.k_max, step,
                                    Ly.expert_of_slot, Ly.last_used, Ly.slot_of_expert_dev,
                                    Ly.avail_dev, cs, ss, cs, nullptr, nullptr, copied.data(),
                                    &n_copy, false);
@@ -376,16 +504,8 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         const bool split = n_copy > 0;
         const hipStream_t ws = split ? ss : cs;
         // the attention window
-        if (c.attn_heads > 0) {
-            st = apex_attention_decode(h_pre[l], Ly.w_qkv, Ly.w_o, c.B, c.d, c.attn_heads,
-                                       c.attn_kv_heads, c.d / c.attn_heads, Ly.k_cache,
-                                       Ly.v_cache, c.attn_ctx + 1, c.attn_ctx, Ly.attn_out,
-                                       dec->attn_ws, dec->attn_ws_bytes, ws);
-            if (st != APEX_OK) return st;
-        } else if (c.t_attn_us > 0) {
-            st = apex_spin_us(c.t_attn_us, ws);
-            if (st != APEX_OK) return st;
-        }
+        st = window(dec, l, h_pre[l], ws);
+        if (st != APEX_OK) return st;
         // earlier layer-steps' statistics, now that this layer's copies are on their way
         st = fold_pending(dec, stats);
         if (st != APEX_OK) return st;
@@ -393,8 +513,8 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         p.layer = l;
         p.seq = seq;
         p.gate_stream = ws;
-        p.pf.assign(dec->pf_idx_h, dec->pf_idx_h + size_t(c.B) * c.k_max);
-        p.cnt.assign(dec->pf_count_h, dec->pf_count_h + c.B);
+        p.pf.assign(pf_h, pf_h + size_t(c.B) * c.k_max);
+        p.cnt.assign(pfc_h, pfc_h + c.B);
         p.resident.assign(c.E, 0);
         for (int s = 0; s < c.C; ++s)
             if (Ly.expert_of_slot[s] >= 0) p.resident[Ly.expert_of_slot[s]] = 1;
@@ -402,10 +522,10 @@ extern "C" apex_status apex_decode_step(apex_decode *dec, int64_t step,
         p.misses = 0;
         if (rec) {
             if (rec->pf_idx)
-                std::memcpy(rec->pf_idx + size_t(l) * c.B * c.k_max, dec->pf_idx_h,
+                std::memcpy(rec->pf_idx + size_t(l) * c.B * c.k_max, pf_h,
                             sizeof(int32_t) * c.B * c.k_max);
             if (rec->pf_count)
-                std::memcpy(rec->pf_count + size_t(l) * c.B, dec->pf_count_h,
+                std::memcpy(rec->pf_count + size_t(l) * c.B, pfc_h,
                             sizeof(int32_t) * c.B);
             if (rec->resident)
                 std::memcpy(rec->resident + size_t(l) * c.C, Ly.expert_of_slot,

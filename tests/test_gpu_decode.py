@@ -299,7 +299,7 @@ def test_decode_small_experts_with_shared_experts(mode):
     cfg = SMALL_SHARED
     st = check_decode(cfg, 1, mode, cfg.steps, [0, 1])
     assert st["copies"] > 0 and st["ffn_checked"] > 0
-    (y_free, c_free, _), (y_rec, c_rec, _) = run_unrecorded_and_recorded(cfg, 1, mode,
+    (y_free, c_free, _, _), (y_rec, c_rec, _, _) = run_unrecorded_and_recorded(cfg, 1, mode,
                                                                           cfg.steps, [0, 1])
     assert c_free == c_rec
     assert np.abs(y_free - y_rec).max() <= 1e-5 * np.abs(y_rec).max()
@@ -319,7 +319,8 @@ def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers, policy=native.S
             runner.finish()
             s = runner.stats
             counts = tuple(getattr(s, f) for f in Counters.FIELDS)
-            out.append((runner.y.cpu().numpy().copy(), counts, s))
+            lu = {l: runner.bufs[l]["last_used"].copy() for l in runner.layers}
+            out.append((runner.y.cpu().numpy().copy(), counts, s, lu))
         finally:
             runner.close()
     return out
@@ -346,7 +347,7 @@ def test_decode_without_records_matches_recorded(cfg_name, batch, mode, layers, 
     cfg = getattr(configs, cfg_name)
     layers = list(range(cfg.L)) if layers is None else layers
     steps = 6
-    (y_free, c_free, s_free), (y_rec, c_rec, _) = run_unrecorded_and_recorded(
+    (y_free, c_free, s_free, _), (y_rec, c_rec, _, _) = run_unrecorded_and_recorded(
         cfg, batch, mode, steps, layers, policy)
     assert c_free == c_rec
     if policy == native.SEL_NONE:
@@ -450,3 +451,35 @@ def test_decode_mixtral_shape_first_16_steps():
     cfg = configs.MIXTRAL
     st = check_decode(cfg, 1, native.MODE_EXACT, 16, [6], ffn_at={(15, 6)})
     assert st["copies"] > 0 and st["ffn_checked"] == 1
+
+
+@pytest.mark.parametrize("cfg_name,batch,mode,layers,policy", [
+    ("GRANITE_1B", 1, native.MODE_EXACT, None, native.SEL_CUMPROB),
+    ("GRANITE_1B", 1, native.MODE_STALL_FREE, [0, 7, 23], native.SEL_ORDINAL_CDF),
+    ("GRANITE_1B", 1, native.MODE_EXACT, [3, 4], native.SEL_NONE),
+    ("DEEPSEEK_16B", 2, native.MODE_EXACT, [0, 12], native.SEL_CUMPROB),
+], ids=["g1-exact", "g1-stall-free-ordinal", "g1-none", "deepseek-b2-shared"])
+def test_decode_with_every_expert_resident_skips_the_host_waits(cfg_name, batch, mode, layers,
+                                                                policy):
+    """Every expert resident (C = E): the timed path queues router, window, gate, shared
+    experts and FFN without waiting for the host and folds the statistics later; the
+    recorded path takes the general route.  Counters, outputs and the host's last-use
+    table agree, and the counters equal the oracle's replay."""
+    import dataclasses
+    base = getattr(configs, cfg_name)
+    cfg = dataclasses.replace(base, C=base.E)
+    layers = list(range(cfg.L)) if layers is None else layers
+    steps = 6
+    (y_free, c_free, s_free, lu_free), (y_rec, c_rec, _, lu_rec) = run_unrecorded_and_recorded(
+        cfg, batch, mode, steps, layers, policy)
+    assert c_free == c_rec
+    assert s_free.copies == 0 and s_free.misses == 0
+    for l in layers:
+        assert np.array_equal(lu_free[l], lu_rec[l]), l
+    scale = np.abs(y_rec).max()
+    assert scale > 0
+    assert np.abs(y_free - y_rec).max() <= 1e-5 * scale
+    if policy != native.SEL_ORDINAL_CDF:      # the oracle replay draws its own CDF models
+        ref = oracle_counters(cfg, batch, mode, steps, layers, policy,
+                              float(np.float32(cfg.tau)))
+        ref.check(s_free, "unrecorded, every expert resident, vs oracle")
