@@ -141,13 +141,24 @@ def check_decode(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB, tau
     return stats
 
 
-def oracle_counters(cfg, batch, mode, steps, layers, policy, tau):
+def oracle_counters(cfg, batch, mode, steps, layers, policy, tau, empty=None):
     """Counters of the oracle's own decode replay (no teacher forcing) and the number of
-    (token, layer) rows where a near tie could let the GPU decide differently."""
+    (token, layer) rows where a near tie could let the GPU decide differently.
+
+    empty: {layer: experts} whose slots start empty instead of holding them; the first
+    step after which each layer holds all E experts is left in ``full_at``."""
     from oracle import decode as odec
     c = Counters()
+    states = odec.make_states(cfg, layers, policy=policy)
+    for l, experts in (empty or {}).items():
+        eos = states[l].res.expert_of_slot
+        for e in experts:
+            eos[eos.index(e)] = -1
+    c.full_at = {}
     for t, l, out in odec.run(cfg, batch, steps, mode=mode, tau=tau, layers=layers,
-                              run_ffn=False, policy=policy):
+                              run_ffn=False, policy=policy, states=states):
+        if len(out["resident"]) == cfg.E:
+            c.full_at.setdefault(l, t)
         pf = [list(out["route"]["pf_idx"][b, :out["route"]["pf_count"][b]])
               for b in range(batch)]
         c.add_layer_step(cfg.k, pf, out["gate"]["route_idx"], out["resident"],
@@ -305,8 +316,27 @@ def test_decode_small_experts_with_shared_experts(mode):
     assert np.abs(y_free - y_rec).max() <= 1e-5 * np.abs(y_rec).max()
 
 
-def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB):
-    """Final outputs and counters of the same decode without and with per-layer records."""
+def empty_slots(runner, empty):
+    """Empties, before the first step, the slots of the given {layer: experts}: the host
+    table, the device table and the availability mask the driver reads."""
+    torch = runner.torch
+    for l, experts in empty.items():
+        b = runner.bufs[l]
+        for e in experts:
+            b["eos"][int(np.flatnonzero(b["eos"] == e)[0])] = -1
+        table = np.full(runner.cfg.E, -1, np.int32)
+        for s, e in enumerate(b["eos"]):
+            if e >= 0:
+                table[e] = s
+        b["slot_dev"].copy_(torch.from_numpy(table))
+        b["avail_dev"].copy_(torch.from_numpy((table >= 0).astype(np.uint8)))
+    torch.cuda.synchronize()
+
+
+def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB,
+                                empty=None):
+    """Final outputs and counters of the same decode without and with per-layer records
+    (empty: {layer: experts} whose slots start empty)."""
     from paper_2608_11688_amd.runtime import DecodeRunner
     out = []
     for record in (False, True):
@@ -314,6 +344,8 @@ def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers, policy=native.S
                               policy=policy, steps=steps, layers=layers, t_attn_us=2.0,
                               record=record)
         try:
+            if empty:
+                empty_slots(runner, empty)
             for _ in range(steps):
                 runner.step()
             runner.finish()
@@ -483,3 +515,36 @@ def test_decode_with_every_expert_resident_skips_the_host_waits(cfg_name, batch,
         ref = oracle_counters(cfg, batch, mode, steps, layers, policy,
                               float(np.float32(cfg.tau)))
         ref.check(s_free, "unrecorded, every expert resident, vs oracle")
+
+
+@pytest.mark.parametrize("cfg_name,batch,mode,empty", [
+    ("TINY", 1, native.MODE_EXACT, {0: [4, 0]}),
+    ("TINY", 1, native.MODE_STALL_FREE, {0: [4, 0]}),
+    ("GRANITE_1B", 1, native.MODE_EXACT, {1: [30, 14, 29, 11], 5: [3, 19, 30]}),
+    ("GRANITE_1B", 1, native.MODE_STALL_FREE, {1: [30, 14, 29, 11], 5: [3, 19, 30]}),
+], ids=["tiny-exact", "tiny-stall-free", "g1-exact", "g1-stall-free"])
+def test_decode_fills_empty_slots_then_skips_the_host_waits(cfg_name, batch, mode, empty):
+    """C = E with some slots empty at the start: the layers take the general route, whose
+    cache plan fills the empty slots as the experts enter prefetched sets, then the route
+    without host waits, each layer from its own step on.  Against the recorded run (always
+    the general route) and the oracle's replay from the same initial cache."""
+    import dataclasses
+    base = getattr(configs, cfg_name)
+    cfg = dataclasses.replace(base, C=base.E)
+    layers = sorted(empty)
+    steps = 12
+    tau = float(np.float32(cfg.tau))
+    ref = oracle_counters(cfg, batch, mode, steps, layers, native.SEL_CUMPROB, tau, empty)
+    assert ref.loose_rows == 0
+    # every layer switches routes with steps to spare
+    assert all(0 < ref.full_at.get(l, steps) < steps - 2 for l in layers), ref.full_at
+    (y_free, c_free, s_free, lu_free), (y_rec, c_rec, _, lu_rec) = run_unrecorded_and_recorded(
+        cfg, batch, mode, steps, layers, native.SEL_CUMPROB, empty)
+    assert c_free == c_rec
+    assert s_free.copies == sum(len(v) for v in empty.values())
+    for l in layers:
+        assert np.array_equal(lu_free[l], lu_rec[l]), l
+    scale = np.abs(y_rec).max()
+    assert scale > 0
+    assert np.abs(y_free - y_rec).max() <= 1e-5 * scale
+    print(cfg_name, ref.full_at, ref.check(s_free, "unrecorded, slots filled, vs oracle"))
