@@ -534,7 +534,12 @@ apex_status apex_decode_create(apex_decode **out, const apex_decode_config *cfg,
                                hipStream_t compute, hipStream_t side);
 /* One decode step.  h_pre, h_post, y: host arrays of L device pointers to [B, d] fp32.
  * Returns when everything is enqueued (with `record`, after the step has completed and
- * the record is filled).  stats (may be NULL) is added to. */
+ * the record is filled).  stats (may be NULL) is added to; a layer-step's counters are
+ * added once its gate has finished, by this call, a later one or apex_decode_finish.
+ * A layer whose every expert is resident (C = E, no slot empty) is enqueued without
+ * waiting for its router: its cache plan, which then only renews last_used, runs when
+ * the layer-step is counted, so last_used is current after apex_decode_finish, or
+ * after a step with `record` (which always waits). */
 apex_status apex_decode_step(apex_decode *dec, int64_t step, const float *const *h_pre,
                              const float *const *h_post, float *const *y,
                              apex_decode_stats *stats, apex_decode_record *record);
