@@ -374,7 +374,7 @@ def test_ffn_parity_mixtral_batch1(torch):
 def test_ffn_parity_mixtral_batched_sampled_tokens(torch, B):
     # the bench's launch configuration at full size: 4 of the 8 experts resident, so the
     # down projection splits K four ways (and the gate/up projection two ways at B = 8);
-    # the oracle checks three of the tokens, one at a time
+    # the oracle checks three of the tokens, one at a time, and a permuted batch the rest
     cfg = configs.MIXTRAL
     case = FfnCase(torch, cfg, B, seed=45 + B, resident_frac=0.5)
     y = case.run()
@@ -382,6 +382,14 @@ def test_ffn_parity_mixtral_batched_sampled_tokens(torch, B):
     want = case.oracle_rows(rows)
     for i, r in enumerate(rows):
         print("mixtral", B, r, ffn_close(y[r:r + 1], want[i:i + 1], f"mixtral B{B} token {r}"))
+    # every other token: a token's output depends on its own row alone, in a fixed order
+    # of operations, so the same batch in another token order gives the same rows, bit
+    # for bit (the plan depends on the sizes only); the three checked tokens move to other
+    # positions, tiles and split partials
+    perm = np.random.default_rng(B).permutation(B)
+    case.x, case.exec_idx, case.gate = case.x[perm], case.exec_idx[perm], case.gate[perm]
+    y_perm = case.run()
+    assert np.array_equal(y_perm, y[perm])
 
 
 FP8_SHAPES = [
