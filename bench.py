@@ -6,8 +6,9 @@ prefetch router + adaptive K_p, cache plan + host-to-HBM expert copies (a copy k
 on the compute stream, which the attention window and the gate run beside on the side
 stream), the attention window (a spin of --t-attn-us, or with --window attention the
 layer's real decode attention), gate top-k (correctness-preserving mode by default),
-expert FFN over the HBM slots, miss correction (its copies on the side stream).  Inputs (hidden states, routers, the
-HBM slot pools and the pinned host copy of every expert) are resident before timing.
+expert FFN over the HBM slots, miss correction (its copies on the side stream).  Inputs
+(hidden states, routers, the HBM slot pools and the pinned host copy of every expert) are
+resident before timing.
 
 Prints one JSON line.  ``value`` is microseconds per token per MoE layer of the decode
 timeline with the attention window subtracted (the spin's length, or the attention
