@@ -284,9 +284,21 @@ apex_status ffn_b1(const float *x, int d, int I, int E, int k, const int32_t *ex
         hipLaunchKernelGGL((down_b1<1, 1, 8>), dim3(d), dim3(64), 0, stream, d, I, E, k,
                            exec_idx, slot_of_expert, slots, n_slots, slot_elems, h, y,
                            accumulate);
+    } else if (size_t(k) * I >= 8192) {
+        // more than 2048 output rows, each a dot product of at least 8192 values: four
+        // rows per wavefront (h loaded once for the four), two wavefronts per workgroup,
+        // four chunks of every row in flight per lane.  Down projection alone at the
+        // Mixtral shape (k I = 28672), against down_b1<2,4,8>: 40.6-40.8 -> 38.1 us, the
+        // call 109.1-110.4 -> 106.4-107.3 us; two or four wavefronts per workgroup, or
+        // four rows with 2, 3 or 6 chunks in flight, 38.6-40.3 us; six or eight rows
+        // 42.3-55.2 us.
+        hipLaunchKernelGGL((down_b1<4, 2, 4>), dim3(d / 8 + (d % 8 != 0)), dim3(128), 0,
+                           stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
+                           slot_elems, h, y, accumulate);
     } else {
-        // rows longer than 2048: two output rows per wavefront (against four: Mixtral
-        // 122.1-123.4 -> 120.6 us per call, Phi-7B 15.2 -> 13.2 us)
+        // more than 2048 output rows over short dot products: two rows per wavefront
+        // (at the Phi-7B shape, k I = 1664, four rows per wavefront take 5.6 us against
+        // 5.0 us)
         hipLaunchKernelGGL((down_b1<2, 4, 8>), dim3(d / 8 + (d % 8 != 0)), dim3(256), 0,
                            stream, d, I, E, k, exec_idx, slot_of_expert, slots, n_slots,
                            slot_elems, h, y, accumulate);

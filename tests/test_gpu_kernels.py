@@ -538,10 +538,12 @@ def test_ffn_two_passes_equal_one(torch):
     assert (case.run(none) == 0).all()
 
 
-@pytest.mark.parametrize("d,I", [(520, 72), (1800, 136), (2056, 40)])
+@pytest.mark.parametrize("d,I", [(520, 72), (1800, 136), (2056, 40), (2056, 4104)])
 def test_ffn_batch1_split_rows_two_passes_and_repeat(torch, d, I):
     """One token over the split-row up projection: two passes (the second accumulating)
-    equal one, absent experts leave y alone, and a repeated call is bitwise equal."""
+    equal one, absent experts leave y alone, and a repeated call is bitwise equal.  Past
+    2048 output rows the down projection takes two rows per wavefront over short dot
+    products (3 x 40 values) and four over long ones (3 x 4104, a ragged chunk count)."""
     cfg = shape(f"ffn_split_pass_{d}", 419, d, 6, 3, I=I)
     case = FfnCase(torch, cfg, 1, seed=d, n_slots_extra=2)
     full = case.oracle()
