@@ -334,7 +334,7 @@ def empty_slots(runner, empty):
 
 
 def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers, policy=native.SEL_CUMPROB,
-                                empty=None):
+                                empty=None, window="spin"):
     """Final outputs and counters of the same decode without and with per-layer records
     (empty: {layer: experts} whose slots start empty)."""
     from paper_2608_11688_amd.runtime import DecodeRunner
@@ -342,7 +342,7 @@ def run_unrecorded_and_recorded(cfg, batch, mode, steps, layers, policy=native.S
     for record in (False, True):
         runner = DecodeRunner(cfg, batch=batch, mode=mode, tau=float(np.float32(cfg.tau)),
                               policy=policy, steps=steps, layers=layers, t_attn_us=2.0,
-                              record=record)
+                              record=record, window=window, ctx=256)
         try:
             if empty:
                 empty_slots(runner, empty)
@@ -485,25 +485,28 @@ def test_decode_mixtral_shape_first_16_steps():
     assert st["copies"] > 0 and st["ffn_checked"] == 1
 
 
-@pytest.mark.parametrize("cfg_name,batch,mode,layers,policy", [
-    ("GRANITE_1B", 1, native.MODE_EXACT, None, native.SEL_CUMPROB),
-    ("GRANITE_1B", 1, native.MODE_STALL_FREE, [0, 7, 23], native.SEL_ORDINAL_CDF),
-    ("GRANITE_1B", 1, native.MODE_EXACT, [3, 4], native.SEL_NONE),
-    ("DEEPSEEK_16B", 2, native.MODE_EXACT, [0, 12], native.SEL_CUMPROB),
-], ids=["g1-exact", "g1-stall-free-ordinal", "g1-none", "deepseek-b2-shared"])
+@pytest.mark.parametrize("cfg_name,batch,mode,layers,policy,window", [
+    ("GRANITE_1B", 1, native.MODE_EXACT, None, native.SEL_CUMPROB, "spin"),
+    ("GRANITE_1B", 1, native.MODE_STALL_FREE, [0, 7, 23], native.SEL_ORDINAL_CDF, "spin"),
+    ("GRANITE_1B", 1, native.MODE_EXACT, [3, 4], native.SEL_NONE, "spin"),
+    ("DEEPSEEK_16B", 2, native.MODE_EXACT, [0, 12], native.SEL_CUMPROB, "spin"),
+    ("OLMOE", 4, native.MODE_STALL_FREE, [1, 9], native.SEL_CUMPROB, "attention"),
+], ids=["g1-exact", "g1-stall-free-ordinal", "g1-none", "deepseek-b2-shared",
+        "olmoe-b4-attention"])
 def test_decode_with_every_expert_resident_skips_the_host_waits(cfg_name, batch, mode, layers,
-                                                                policy):
-    """Every expert resident (C = E): the timed path queues router, window, gate, shared
-    experts and FFN without waiting for the host and folds the statistics later; the
-    recorded path takes the general route.  Counters, outputs and the host's last-use
-    table agree, and the counters equal the oracle's replay."""
+                                                                policy, window):
+    """Every expert resident (C = E): the timed path queues router, window (the spin, or
+    the layer's decode attention), gate, shared experts and FFN without waiting for the
+    host and folds the statistics later; the recorded path takes the general route.
+    Counters, outputs and the host's last-use table agree, and the counters equal the
+    oracle's replay."""
     import dataclasses
     base = getattr(configs, cfg_name)
     cfg = dataclasses.replace(base, C=base.E)
     layers = list(range(cfg.L)) if layers is None else layers
     steps = 6
     (y_free, c_free, s_free, lu_free), (y_rec, c_rec, _, lu_rec) = run_unrecorded_and_recorded(
-        cfg, batch, mode, steps, layers, policy)
+        cfg, batch, mode, steps, layers, policy, window=window)
     assert c_free == c_rec
     assert s_free.copies == 0 and s_free.misses == 0
     for l in layers:
