@@ -388,9 +388,12 @@ apex_status ffn_b1_mxfp4(const float *x, int d, int I, int E, int k, const int32
                            slot_bytes, h, y, accumulate);
     } else if (size_t(k) * (I / 16) > 1024 && size_t(k) * (I / 16) <= 2048) {
         // long flattened rows: h held in registers, 16 output rows streamed per workgroup
-        // of 16 wavefronts (Mixtral call 50.7 -> 47.3 us against four rows per wavefront;
-        // at Phi-7B, 104 units, it lost: 5.5 against 4.5 us for the down projection)
-        hipLaunchKernelGGL((down_rows_mxfp4<16, 2, 16, 2>), dim3(d / 16 + (d % 16 != 0)),
+        // of 16 wavefronts, four at a time (Mixtral call 50.7 -> 47.3 us against four rows
+        // per wavefront; at Phi-7B, 104 units, it lost: 5.5 against 4.5 us for the down
+        // projection).  Four rows per step against two, Mixtral, down alone 18.5 -> 17.8
+        // us, the call 45.6-47.9 -> 44.6 us; eight 18.4-18.5 us; eight rows per workgroup
+        // 24.5-25.4 us; eight wavefronts of four units per lane 18.7-20.2 us
+        hipLaunchKernelGGL((down_rows_mxfp4<16, 4, 16, 2>), dim3(d / 16 + (d % 16 != 0)),
                            dim3(1024), 0, stream, d, I, E, k, exec_idx, slot_of_expert, slots,
                            n_slots, slot_bytes, h, y, accumulate);
     } else {
